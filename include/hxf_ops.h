@@ -1,0 +1,95 @@
+/*
+ * hxf_ops.h -- the individual gfx950 kernels of one decoder iteration, exposed
+ * for kernel-level parity tests, benchmarks and callers that drive their own
+ * forward pass.
+ *
+ * All pointers are DEVICE pointers unless marked "host".  bf16 tensors are
+ * uint16 bit patterns.  Every call enqueues work on `stream` (hipStream_t, may
+ * be 0) and returns HXF_OK (0) or a negative hxf error code; errors are not
+ * sticky and leave nothing enqueued.  The caller owns every buffer.  Calls
+ * that build a work list on the host (attention) copy it into the caller's
+ * `workspace` with an asynchronous host-to-device copy and synchronise the
+ * stream before returning, so their host arguments may be freed afterwards.
+ *
+ * Physical KV layout (one layer): K pool [n_blocks][Hkv][16][dh] then a
+ * separate V pool [n_blocks][Hkv][dh][16] (V transposed inside a page); the
+ * token at position p of a sequence with block table bt lives in slot
+ * bt[p/16]*16 + p%16.
+ */
+#ifndef HXF_OPS_H
+#define HXF_OPS_H
+
+#include <stdint.h>
+
+#include "hxf.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* GEMM epilogues */
+enum { HXF_EPI_BF16 = 0, HXF_EPI_RESID = 1, HXF_EPI_SWIGLU = 2, HXF_EPI_F32 = 3 };
+
+/* C = A[M,K] . B[N,K]^T, bf16 inputs, fp32 accumulation.
+ *   HXF_EPI_BF16:   C bf16 [M, ldc]            C = bf16(acc)
+ *   HXF_EPI_RESID:  C fp32 [M, ldc]            C += acc          (residual stream)
+ *   HXF_EPI_SWIGLU: B = W_gate [F,K], B2 = W_up [F,K], N = 2F; C bf16 [M, ldc],
+ *                   C[:, f] = bf16(silu(gate_f) * up_f), silu(z) = z / (1 + e^-z)
+ *   HXF_EPI_F32:    C fp32 [M, ldc]            C = acc
+ * K % 8 == 0, lda >= K.  workspace: hxf_op_gemm_workspace_bytes(M, N, K) bytes
+ * (split-K partials for small M; may be 0 bytes).  */
+int64_t hxf_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
+int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void* C, int32_t ldc, int32_t M, int32_t N,
+                int32_t K, int32_t epilogue, void* workspace, int64_t workspace_bytes, void* stream);
+
+/* out[r] = bf16(x[rows[r]] / sqrt(mean(x[rows[r]]^2) + eps) * g); rows may be NULL (identity).
+ * x fp32 [*, d], g bf16 [d], out bf16 [n_rows, d]; d % 4 == 0. */
+int hxf_op_rmsnorm(const float* x, const int32_t* rows, const void* g, void* out, int32_t n_rows, int32_t d,
+                   float eps, void* stream);
+
+/* resid[t] = float(E[ids[t]]); out[t] = rmsnorm(resid[t]) * g.  E bf16 [V, d]. */
+int hxf_op_embed_rmsnorm(const int32_t* ids, const void* E, const void* g, float* resid, void* out, int32_t T,
+                         int32_t d, float eps, void* stream);
+
+/* RoPE table for positions [0, max_pos): float pairs (cos, sin) of p * base^(-2i/dh), i < dh/2,
+ * computed in double on the host and copied to dst (max_pos * dh/2 * 8 bytes). */
+int hxf_op_rope_table(void* dst, int32_t max_pos, int32_t head_dim, float base, void* stream);
+
+/* qkv bf16 [T, (Hq+2Hkv)*dh] rows (q heads, k heads, v heads): rotate-half RoPE of q (in place)
+ * and k at pos[t]; write rotated k and v to slot[t] of the K and V pools. */
+int hxf_op_rope_kv_write(void* qkv, const int32_t* pos, const int32_t* slot, const void* rope_table, void* k_pool,
+                         void* v_pool, int32_t T, int32_t Hq, int32_t Hkv, int32_t head_dim, void* stream);
+
+/* Write k, v bf16 [T, Hkv, dh] to slot[t] of the pools (no rotation). */
+int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k_pool, void* v_pool, int32_t T,
+                      int32_t Hkv, int32_t head_dim, void* stream);
+
+/* Decode attention, one query token per sequence: q bf16 [B, Hq, dh] (rotated), attends to positions
+ * [0, ctx_host[b]) of sequence b through block table bt [B, bt_stride] (device); out bf16 [B, Hq, dh].
+ * Split into partitions of 256 tokens per (sequence, kv-head), merged by log-sum-exp.
+ * workspace: hxf_op_decode_attention_workspace_bytes(...) bytes. */
+int64_t hxf_op_decode_attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                                                const int32_t* ctx_host);
+int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_pool, const int32_t* bt,
+                            int32_t bt_stride, const int32_t* ctx_host, void* out, int32_t B, int32_t Hq, int32_t Hkv,
+                            int32_t head_dim, void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Causal prefill attention over chunks: chunk s has n_host[s] queries at positions
+ * pos0_host[s] .. pos0_host[s]+n-1, stored at rows row0_host[s].. of q bf16 [*, Hq, dh];
+ * it attends to positions [0, pos0+i] of its block table row bt[s] (device).  out rows as q. */
+int64_t hxf_op_prefill_attention_workspace_bytes(int32_t S, int32_t Hq, int32_t Hkv, const int32_t* n_host);
+int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_pool, const int32_t* bt,
+                             int32_t bt_stride, const int32_t* row0_host, const int32_t* pos0_host,
+                             const int32_t* n_host, void* out, int32_t S, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                             void* workspace, int64_t workspace_bytes, void* stream);
+
+/* out[r] = argmax over v of logits fp32 [R, V]; the lowest index wins ties. */
+int hxf_op_argmax(const float* logits, int32_t* out, int32_t R, int32_t V, void* stream);
+
+/* dst = src, bytes % 16 == 0 (HBM bandwidth probe). */
+int hxf_op_copy(const void* src, void* dst, int64_t bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HXF_OPS_H */

@@ -1,0 +1,412 @@
+// HIP executor of one continuous-batched iteration (chunked prefill + paged
+// decode + greedy sampling) of a Llama-style decoder.
+#include "executor.hpp"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+
+#include "kernels/kernels.hpp"
+
+namespace hxf {
+
+namespace {
+
+constexpr int kMaxSplits = 8;
+
+int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+#define HXF_HIP(call)                                                           \
+  do {                                                                          \
+    hipError_t e_ = (call);                                                     \
+    if (e_ != hipSuccess) {                                                     \
+      err = std::string("hip: ") + #call + ": " + hipGetErrorString(e_);        \
+      return HXF_EDEVICE;                                                       \
+    }                                                                           \
+  } while (0)
+
+}  // namespace
+
+int validate_model(const hxf_model_cfg& m, std::string& err) {
+  if (m.n_layers <= 0 || m.d_model <= 0 || m.n_q_heads <= 0 || m.n_kv_heads <= 0 || m.ffn_dim <= 0 ||
+      m.vocab <= 0 || m.max_context <= 0) {
+    err = "model: sizes must be positive";
+    return HXF_EINVAL;
+  }
+  if (m.page_size != kPage) { err = "model: page_size must be 16"; return HXF_EINVAL; }
+  if (m.head_dim != 64 && m.head_dim != 128) { err = "model: head_dim must be 64 or 128"; return HXF_EINVAL; }
+  if (m.n_q_heads % m.n_kv_heads != 0 || m.n_q_heads / m.n_kv_heads > 16) {
+    err = "model: n_q_heads must be a multiple of n_kv_heads, group <= 16";
+    return HXF_EINVAL;
+  }
+  if (m.d_model % 64 != 0 || m.ffn_dim % 16 != 0 || m.vocab % 8 != 0) {
+    err = "model: d_model % 64, ffn_dim % 16 and vocab % 8 must be 0";
+    return HXF_EINVAL;
+  }
+  if (!(m.rms_eps > 0.f) || !(m.rope_base > 1.f)) { err = "model: bad eps or rope base"; return HXF_EINVAL; }
+  return HXF_OK;
+}
+
+int64_t kv_pool_bytes(const hxf_model_cfg& m, int64_t n_blocks) {
+  return (int64_t)m.n_layers * 2 * n_blocks * m.n_kv_heads * kPage * m.head_dim * 2;
+}
+
+WsPlan plan_workspace(const hxf_model_cfg& m, const hxf_sched_cfg& s) {
+  WsPlan p;
+  const int64_t d = m.d_model, dh = m.head_dim, hq = m.n_q_heads, hkv = m.n_kv_heads, f = m.ffn_dim;
+  const int64_t G = hq / hkv;
+  const int64_t qkv = (hq + 2 * hkv) * dh;
+  p.t_max = (int64_t)s.chunk_tokens + s.max_seqs;
+  p.r_max = s.max_seqs;
+  p.e_max = s.max_seqs;
+  p.bt_w = ceil_div(m.max_context, kPage);
+  p.dec_items_max = (int64_t)s.max_seqs * hkv * ceil_div(m.max_context, kDecodePartition);
+  p.merges_max = (int64_t)s.max_seqs * hkv;
+  const int qpi = prefill_queries_per_item((int)G);
+  p.pf_items_max = hkv * (ceil_div(s.chunk_tokens, qpi) + s.max_seqs);
+  // metadata (int32 words), sections packed in this order, each 64-word aligned
+  auto words = [](int64_t n) { return (n + 63) & ~int64_t(63); };
+  const int64_t meta_words = words(p.t_max) * 3 + words(p.r_max) + words(p.e_max) * 2 +
+                             words(p.e_max * p.bt_w) + words(p.dec_items_max * 8) + words(p.merges_max * 4) +
+                             words(p.pf_items_max * 4);
+  p.meta_bytes = meta_words * 4;
+  // split-K partials: largest splits*M*N over the GEMM shapes at M <= 256
+  int64_t part = 0;
+  const int64_t shapes[5][2] = {{qkv, d}, {d, hq * dh}, {2 * f, d}, {d, f}, {m.vocab, d}};
+  for (int64_t M = 1; M <= std::min<int64_t>(256, p.t_max); ++M)
+    for (auto& sh : shapes) {
+      GemmPlan g = gemm_plan((int)M, (int)sh[0], (int)sh[1], kMaxSplits);
+      if (g.splits > 1) part = std::max(part, (int64_t)g.splits * M * sh[0] * 4);
+    }
+  int64_t o = 0;
+  auto take = [&](int64_t bytes) { int64_t at = o; o = align256(o + bytes); return at; };
+  p.off_meta = take(p.meta_bytes);
+  p.off_rope = take((int64_t)m.max_context * (dh / 2) * 8);
+  p.off_resid = take(p.t_max * d * 4);
+  p.off_h = take(p.t_max * d * 2);
+  p.off_qkv = take(p.t_max * qkv * 2);
+  p.off_attn = take(p.t_max * hq * dh * 2);
+  p.off_act = take(p.t_max * f * 2);
+  p.part_bytes = part;
+  p.off_part = take(std::max<int64_t>(part, 256));
+  p.off_attn_o = take(p.dec_items_max * G * dh * 4);
+  p.off_attn_ml = take(p.dec_items_max * G * 2 * 4);
+  p.off_logits = take(p.r_max * m.vocab * 4);
+  p.off_hr = take(p.r_max * d * 2);
+  p.off_sampled = take(p.r_max * 4);
+  p.total = o;
+  return p;
+}
+
+void build_rope_table(std::vector<float>& out, int max_pos, int dh, float base) {
+  const int half = dh / 2;
+  out.resize((size_t)max_pos * half * 2);
+  for (int i = 0; i < half; ++i) {
+    const double theta = std::pow((double)base, -2.0 * i / dh);
+    for (int p = 0; p < max_pos; ++p) {
+      const double a = (double)p * theta;
+      out[((size_t)p * half + i) * 2] = (float)std::cos(a);
+      out[((size_t)p * half + i) * 2 + 1] = (float)std::sin(a);
+    }
+  }
+}
+
+namespace {
+
+class HipExecutor : public Executor {
+ public:
+  HipExecutor(const hxf_model_cfg& m, const hxf_sched_cfg& s, const hxf_device_buffers& b, void* stream)
+      : m_(m), s_(s), b_(b), st_((hipStream_t)stream) {
+    layers_.assign(b.layers, b.layers + m.n_layers);
+    plan_ = plan_workspace(m, s);
+    ws_ = reinterpret_cast<uint8_t*>(b.workspace);
+  }
+
+  ~HipExecutor() override {
+    if (host_meta_) (void)hipHostFree(host_meta_);
+    if (host_sampled_) (void)hipHostFree(host_sampled_);
+    if (ev_) {
+      for (auto& e : ev_pool_) (void)hipEventDestroy(e);
+    }
+  }
+
+  int init(std::string& err) {
+    HXF_HIP(hipHostMalloc(&host_meta_, plan_.meta_bytes, hipHostMallocDefault));
+    HXF_HIP(hipHostMalloc(reinterpret_cast<void**>(&host_sampled_), plan_.r_max * 4, hipHostMallocDefault));
+    std::vector<float> tab;
+    build_rope_table(tab, m_.max_context, m_.head_dim, m_.rope_base);
+    HXF_HIP(hipMemcpyAsync(ws_ + plan_.off_rope, tab.data(), tab.size() * 4, hipMemcpyHostToDevice, st_));
+    HXF_HIP(hipStreamSynchronize(st_));
+    ev_ = true;
+    return HXF_OK;
+  }
+
+  int run(const std::vector<BatchEntry>& batch, std::vector<int32_t>& sampled, std::string& err) override;
+  int last_logits(uint64_t id, float* dst, int32_t cap, std::string& err) override;
+
+  Profile prof;
+
+ private:
+  template <typename T>
+  T* dev(int64_t off) { return reinterpret_cast<T*>(ws_ + off); }
+  int gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M, int N, int K,
+           int epi, std::string& err);
+
+  hxf_model_cfg m_;
+  hxf_sched_cfg s_;
+  hxf_device_buffers b_;
+  hipStream_t st_;
+  std::vector<hxf_layer_weights> layers_;
+  WsPlan plan_;
+  uint8_t* ws_ = nullptr;
+  void* host_meta_ = nullptr;
+  int32_t* host_sampled_ = nullptr;
+  std::vector<uint64_t> last_rows_;   // request id per logits row of the last iteration
+  bool ev_ = false;
+  std::vector<hipEvent_t> ev_pool_;
+};
+
+int HipExecutor::gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M,
+                      int N, int K, int epi, std::string& err) {
+  GemmArgs a{};
+  a.A = A;
+  a.B = B;
+  a.B2 = B2;
+  a.C = C;
+  a.partial = dev<float>(plan_.off_part);
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.lda = lda;
+  a.ldc = ldc;
+  GemmPlan p = gemm_plan(M, N, K, kMaxSplits);
+  if (p.splits > 1 && (int64_t)p.splits * M * N * 4 > plan_.part_bytes) {
+    err = "gemm: split-K partial buffer too small";
+    return HXF_EINVAL;
+  }
+  HXF_HIP(gemm_launch(a, epi, p, st_));
+  return HXF_OK;
+}
+
+int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>& sampled, std::string& err) {
+  const int E = (int)batch.size();
+  const int d = m_.d_model, dh = m_.head_dim, hq = m_.n_q_heads, hkv = m_.n_kv_heads, f = m_.ffn_dim;
+  const int G = hq / hkv;
+  const int qkv_w = (hq + 2 * hkv) * dh;
+  int T = 0, R = 0, n_dec = 0, bt_w = 1;
+  for (const auto& e : batch) {
+    T += e.n;
+    R += e.logits ? 1 : 0;
+    n_dec += e.decode ? 1 : 0;
+    bt_w = std::max<int>(bt_w, (int)ceil_div((int64_t)e.pos0 + e.n, kPage));
+  }
+  if (T > plan_.t_max || R > plan_.r_max || E > plan_.e_max) {
+    err = "run: batch exceeds the workspace plan";
+    return HXF_EINVAL;
+  }
+  // ---------------------------------------------------------- metadata
+  int32_t* hm = reinterpret_cast<int32_t*>(host_meta_);
+  int64_t w = 0;
+  auto sec = [&](int64_t n) { int64_t at = w; w += (n + 63) & ~int64_t(63); return at; };
+  const int64_t o_ids = sec(T), o_pos = sec(T), o_slot = sec(T), o_lrow = sec(R), o_row0 = sec(E), o_pos0 = sec(E),
+                o_bt = sec((int64_t)E * bt_w);
+  int row = 0, r = 0;
+  int n_part = 0;
+  std::vector<DecodeItem> ditems;
+  std::vector<MergeItem> merges;
+  std::vector<PrefillItem> pitems;
+  const int qpi = prefill_queries_per_item(G);
+  last_rows_.clear();
+  for (int e = 0; e < E; ++e) {
+    const BatchEntry& be = batch[e];
+    const std::vector<int32_t>& bt = be.r->bt;
+    for (int k = 0; k < be.n; ++k) {
+      const int p = be.pos0 + k;
+      hm[o_ids + row + k] = be.toks[k];
+      hm[o_pos + row + k] = p;
+      hm[o_slot + row + k] = bt[p / kPage] * kPage + p % kPage;
+    }
+    if (be.logits) {
+      hm[o_lrow + r++] = row + be.n - 1;
+      last_rows_.push_back(be.r->id);
+    }
+    hm[o_row0 + e] = row;
+    hm[o_pos0 + e] = be.pos0;
+    const int np = (int)ceil_div((int64_t)be.pos0 + be.n, kPage);
+    for (int j = 0; j < bt_w; ++j) hm[o_bt + (int64_t)e * bt_w + j] = j < np ? bt[j] : 0;
+    if (be.decode) {
+      const int ctx = be.pos0 + 1;
+      for (int h = 0; h < hkv; ++h) {
+        MergeItem mi{e, h, n_part, 0};
+        for (int t0 = 0; t0 < ctx; t0 += kDecodePartition) {
+          ditems.push_back(DecodeItem{e, h, t0, std::min(ctx, t0 + kDecodePartition), n_part++, 0, 0, 0});
+          ++mi.n_part;
+        }
+        merges.push_back(mi);
+      }
+    } else {
+      for (int h = 0; h < hkv; ++h)
+        for (int q0 = 0; q0 < be.n; q0 += qpi) pitems.push_back(PrefillItem{e, h, q0, std::min(qpi, be.n - q0)});
+    }
+    row += be.n;
+  }
+  if ((int64_t)ditems.size() > plan_.dec_items_max || (int64_t)pitems.size() > plan_.pf_items_max) {
+    err = "run: attention work list exceeds the workspace plan";
+    return HXF_EINVAL;
+  }
+  const int64_t o_ditems = sec((int64_t)ditems.size() * 8), o_merges = sec((int64_t)merges.size() * 4),
+                o_pitems = sec((int64_t)pitems.size() * 4);
+  if (w * 4 > plan_.meta_bytes) {
+    err = "run: metadata exceeds the workspace plan";
+    return HXF_EINVAL;
+  }
+  std::memcpy(hm + o_ditems, ditems.data(), ditems.size() * sizeof(DecodeItem));
+  std::memcpy(hm + o_merges, merges.data(), merges.size() * sizeof(MergeItem));
+  std::memcpy(hm + o_pitems, pitems.data(), pitems.size() * sizeof(PrefillItem));
+  int32_t* dm = dev<int32_t>(plan_.off_meta);
+  HXF_HIP(hipMemcpyAsync(dm, hm, w * 4, hipMemcpyHostToDevice, st_));
+
+  // ---------------------------------------------------------- forward
+  float* resid = dev<float>(plan_.off_resid);
+  uint16_t* h = dev<uint16_t>(plan_.off_h);
+  uint16_t* qkv = dev<uint16_t>(plan_.off_qkv);
+  uint16_t* attn = dev<uint16_t>(plan_.off_attn);
+  uint16_t* act = dev<uint16_t>(plan_.off_act);
+  const float2* rope = dev<float2>(plan_.off_rope);
+  const float scale_log2 = 1.4426950408889634f / std::sqrt((float)dh);
+  const int64_t layer_pool = (int64_t)s_.n_blocks * hkv * kPage * dh;   // bf16 elements per K (or V) pool
+  uint16_t* pool = reinterpret_cast<uint16_t*>(b_.kv_pool);
+
+  DecodeAttnArgs da{};
+  da.q = qkv;
+  da.q_row = dm + o_row0;
+  da.q_stride = qkv_w;
+  da.bt = dm + o_bt;
+  da.bt_stride = bt_w;
+  da.items = reinterpret_cast<const DecodeItem*>(dm + o_ditems);
+  da.n_items = (int)ditems.size();
+  da.merges = reinterpret_cast<const MergeItem*>(dm + o_merges);
+  da.n_merges = (int)merges.size();
+  da.part_o = dev<float>(plan_.off_attn_o);
+  da.part_ml = dev<float>(plan_.off_attn_ml);
+  da.out = attn;
+  da.out_stride = hq * dh;
+  da.Hq = hq;
+  da.Hkv = hkv;
+  da.dh = dh;
+  da.scale_log2 = scale_log2;
+  PrefillAttnArgs pa{};
+  pa.q = qkv;
+  pa.q_stride = qkv_w;
+  pa.row0 = dm + o_row0;
+  pa.pos0 = dm + o_pos0;
+  pa.bt = dm + o_bt;
+  pa.bt_stride = bt_w;
+  pa.items = reinterpret_cast<const PrefillItem*>(dm + o_pitems);
+  pa.n_items = (int)pitems.size();
+  pa.out = attn;
+  pa.out_stride = hq * dh;
+  pa.Hq = hq;
+  pa.Hkv = hkv;
+  pa.dh = dh;
+  pa.scale_log2 = scale_log2;
+
+  int64_t kv_tokens = 0;
+  for (const auto& it : ditems) kv_tokens += it.t1 - it.t0;
+
+  HXF_HIP(embed_rmsnorm_launch(dm + o_ids, (const uint16_t*)b_.embed, (const uint16_t*)layers_[0].attn_norm, resid,
+                               h, T, d, m_.rms_eps, st_));
+  for (int l = 0; l < m_.n_layers; ++l) {
+    const hxf_layer_weights& L = layers_[l];
+    uint16_t* kp = pool + (int64_t)l * 2 * layer_pool;
+    uint16_t* vp = kp + layer_pool;
+    if (l > 0) HXF_HIP(rmsnorm_launch(resid, nullptr, (const uint16_t*)L.attn_norm, h, T, d, m_.rms_eps, st_));
+    if (int rc = gemm(h, d, (const uint16_t*)L.wqkv, nullptr, qkv, qkv_w, T, qkv_w, d, EPI_BF16, err)) return rc;
+    HXF_HIP(rope_kv_launch(qkv, dm + o_pos, dm + o_slot, rope, kp, vp, T, hq, hkv, dh, st_));
+    da.k_pool = pa.k_pool = kp;
+    da.v_pool = pa.v_pool = vp;
+    if (da.n_items) {
+      hipEvent_t e0 = nullptr, e1 = nullptr;
+      if (prof.on) {
+        HXF_HIP(hipEventCreate(&e0));
+        HXF_HIP(hipEventCreate(&e1));
+        HXF_HIP(hipEventRecord(e0, st_));
+      }
+      HXF_HIP(decode_attn_launch(da, st_));
+      if (prof.on) {
+        HXF_HIP(hipEventRecord(e1, st_));
+        ev_pool_.push_back(e0);
+        ev_pool_.push_back(e1);
+        prof.decode_attn_launches += 1;
+        prof.decode_attn_bytes += kv_tokens * 2 * dh * 2;
+      }
+    }
+    HXF_HIP(prefill_attn_launch(pa, st_));
+    if (int rc = gemm(attn, hq * dh, (const uint16_t*)L.wo, nullptr, resid, d, T, d, hq * dh, EPI_RESID, err))
+      return rc;
+    HXF_HIP(rmsnorm_launch(resid, nullptr, (const uint16_t*)L.ffn_norm, h, T, d, m_.rms_eps, st_));
+    if (int rc = gemm(h, d, (const uint16_t*)L.w_gate, (const uint16_t*)L.w_up, act, f, T, 2 * f, d, EPI_SWIGLU, err))
+      return rc;
+    if (int rc = gemm(act, f, (const uint16_t*)L.w_down, nullptr, resid, d, T, d, f, EPI_RESID, err)) return rc;
+  }
+  uint16_t* hr = dev<uint16_t>(plan_.off_hr);
+  float* logits = dev<float>(plan_.off_logits);
+  int32_t* samp = dev<int32_t>(plan_.off_sampled);
+  if (R > 0) {
+    HXF_HIP(rmsnorm_launch(resid, dm + o_lrow, (const uint16_t*)b_.final_norm, hr, R, d, m_.rms_eps, st_));
+    if (int rc = gemm(hr, d, (const uint16_t*)b_.lm_head, nullptr, logits, m_.vocab, R, m_.vocab, d, EPI_F32, err))
+      return rc;
+    HXF_HIP(argmax_launch(logits, samp, R, m_.vocab, st_));
+    HXF_HIP(hipMemcpyAsync(host_sampled_, samp, (size_t)R * 4, hipMemcpyDeviceToHost, st_));
+  }
+  HXF_HIP(hipStreamSynchronize(st_));
+  if (prof.on) {
+    for (size_t i = 0; i + 1 < ev_pool_.size(); i += 2) {
+      float ms = 0.f;
+      HXF_HIP(hipEventElapsedTime(&ms, ev_pool_[i], ev_pool_[i + 1]));
+      prof.decode_attn_ms += ms;
+      (void)hipEventDestroy(ev_pool_[i]);
+      (void)hipEventDestroy(ev_pool_[i + 1]);
+    }
+    ev_pool_.clear();
+  }
+  sampled.assign(host_sampled_, host_sampled_ + R);
+  return HXF_OK;
+}
+
+int HipExecutor::last_logits(uint64_t id, float* dst, int32_t cap, std::string& err) {
+  for (size_t i = 0; i < last_rows_.size(); ++i) {
+    if (last_rows_[i] != id) continue;
+    if (cap < m_.vocab) {
+      err = "last_logits: buffer smaller than vocab";
+      return HXF_ENOMEM;
+    }
+    HXF_HIP(hipMemcpyAsync(dst, dev<float>(plan_.off_logits) + i * (size_t)m_.vocab, (size_t)m_.vocab * 4,
+                           hipMemcpyDeviceToHost, st_));
+    HXF_HIP(hipStreamSynchronize(st_));
+    return HXF_OK;
+  }
+  err = "last_logits: request had no logits row in the last iteration";
+  return HXF_ENOTFOUND;
+}
+
+}  // namespace
+
+std::unique_ptr<Executor> make_hip_executor(const hxf_model_cfg& m, const hxf_sched_cfg& s,
+                                            const hxf_device_buffers& b, void* stream, std::string& err, int* rc) {
+  auto ex = std::make_unique<HipExecutor>(m, s, b, stream);
+  *rc = ex->init(err);
+  if (*rc) return nullptr;
+  return ex;
+}
+
+Profile* executor_profile(Executor* e) {
+  auto* h = dynamic_cast<HipExecutor*>(e);
+  return h ? &h->prof : nullptr;
+}
+
+}  // namespace hxf

@@ -1,0 +1,117 @@
+// Host-side launchers of the gfx950 kernels (one translation unit each).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hxf {
+
+// Physical KV layout (per layer; K pool then V pool):
+//   K: [n_blocks][Hkv][16 tokens][dh]   (a token's head vector contiguous)
+//   V: [n_blocks][Hkv][dh][16 tokens]   (a dimension's 16 tokens contiguous)
+// so one (page, kv-head) is one contiguous 16*dh*2-byte tile in each pool.
+constexpr int kPage = 16;
+
+// ------------------------------------------------------------------ GEMM
+enum { EPI_BF16 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3 };
+
+struct GemmArgs {
+  const uint16_t* A;   // bf16 [M, lda]
+  const uint16_t* B;   // bf16 [N, K] (SwiGLU: gate rows [F, K])
+  const uint16_t* B2;  // SwiGLU: up rows [F, K]
+  void* C;             // bf16 / fp32 output or fp32 residual, row stride ldc
+  float* partial;      // split-K partials [splits][M][N] fp32
+  int M, N, K;         // N is logical (2F for SwiGLU); K % 8 == 0
+  int lda, ldc;
+  int k_chunk;
+};
+
+struct GemmPlan {
+  int bm = 128;
+  int splits = 1;
+  int k_chunk = 0;
+};
+
+GemmPlan gemm_plan(int M, int N, int K, int max_splits);
+hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st);
+
+// ------------------------------------------------------------------ norms / embedding
+// out[r] = bf16(rmsnorm(x[rows ? rows[r] : r]) * g); x fp32 [*, d]
+hipError_t rmsnorm_launch(const float* x, const int32_t* rows, const uint16_t* g, uint16_t* out,
+                          int n_rows, int d, float eps, hipStream_t st);
+// resid[t] = E[ids[t]] (fp32); out[t] = bf16(rmsnorm(resid[t]) * g)
+hipError_t embed_rmsnorm_launch(const int32_t* ids, const uint16_t* E, const uint16_t* g, float* resid,
+                                uint16_t* out, int T, int d, float eps, hipStream_t st);
+
+// ------------------------------------------------------------------ RoPE + KV write
+// qkv bf16 [T, (Hq+2Hkv)*dh]: rotates q (in place) and k at pos[t] with the
+// table cs[pos][i] = (cos, sin) of pos * base^(-2i/dh); writes k and v to slot[t].
+hipError_t rope_kv_launch(uint16_t* qkv, const int32_t* pos, const int32_t* slot, const float2* cs,
+                          uint16_t* k_pool, uint16_t* v_pool, int T, int Hq, int Hkv, int dh,
+                          hipStream_t st);
+// Write k, v bf16 [T, Hkv, dh] to slot[t] (no rotation).
+hipError_t kv_scatter_launch(const uint16_t* k, const uint16_t* v, const int32_t* slot, uint16_t* k_pool,
+                             uint16_t* v_pool, int T, int Hkv, int dh, hipStream_t st);
+
+// ------------------------------------------------------------------ attention
+// One decode work item: tokens [t0, t1) of batch entry `entry`, kv-head `kvh`;
+// its partial result goes to slot `part`.
+struct DecodeItem {
+  int32_t entry, kvh, t0, t1, part, pad0, pad1, pad2;
+};
+// One merge job per (entry, kv-head): partials [part0, part0 + n_part).
+struct MergeItem {
+  int32_t entry, kvh, part0, n_part;
+};
+struct DecodeAttnArgs {
+  const uint16_t* q;       // bf16, q of entry e at q + q_row[e]*q_stride (+ head*dh)
+  const int32_t* q_row;    // [entries]
+  int q_stride;
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* bt;       // [entries][bt_stride]
+  int bt_stride;
+  const DecodeItem* items;
+  int n_items;
+  const MergeItem* merges;
+  int n_merges;
+  float* part_o;           // [parts][G][dh]
+  float* part_ml;          // [parts][G][2]  (max in log2 units, sum)
+  uint16_t* out;           // bf16, row q_row[e]*out_stride + head*dh
+  int out_stride;
+  int Hq, Hkv, dh;
+  float scale_log2;        // log2(e) / sqrt(dh)
+};
+hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st);
+
+// One prefill work item: queries [q0, q0 + nq) (chunk-local) of entry `entry`, kv-head `kvh`.
+struct PrefillItem {
+  int32_t entry, kvh, q0, nq;
+};
+struct PrefillAttnArgs {
+  const uint16_t* q;       // bf16 rows; entry e's query i at row row0[e] + i
+  int q_stride;
+  const int32_t* row0;     // [entries]
+  const int32_t* pos0;     // [entries] position of the entry's first query
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* bt;       // [entries][bt_stride]
+  int bt_stride;
+  const PrefillItem* items;
+  int n_items;
+  uint16_t* out;
+  int out_stride;
+  int Hq, Hkv, dh;
+  float scale_log2;
+};
+hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st);
+// Queries covered by one prefill work item for a given GQA group size.
+int prefill_queries_per_item(int group);
+
+// ------------------------------------------------------------------ sampling / misc
+// out[r] = argmax_v logits[r][v], the lowest index among equal maxima.
+hipError_t argmax_launch(const float* logits, int32_t* out, int R, int V, hipStream_t st);
+// dst = src (bytes % 16 == 0); HBM bandwidth probe.
+hipError_t copy_launch(const void* src, void* dst, size_t bytes, hipStream_t st);
+
+}  // namespace hxf

@@ -1,0 +1,77 @@
+// RMSNorm over the fp32 residual stream (one workgroup per row, fp32 math,
+// bf16 output), optionally fused with the token-embedding gather.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace hxf {
+
+namespace {
+
+__device__ __forceinline__ float block_sum_256(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  const float s = red[0] + red[1] + red[2] + red[3];
+  __syncthreads();
+  return s;
+}
+
+__device__ __forceinline__ void norm_store(const float4* x4, const uint16_t* g, uint16_t* out, int d, float eps,
+                                           float* red) {
+  const int n4 = d >> 2;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < n4; i += 256) {
+    const float4 v = x4[i];
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  const float r = rsqrtf(block_sum_256(ss, red) / (float)d + eps);
+  const uint2* g2 = reinterpret_cast<const uint2*>(g);
+  uint2* o2 = reinterpret_cast<uint2*>(out);
+  for (int i = threadIdx.x; i < n4; i += 256) {
+    const float4 v = x4[i];
+    const uint2 gg = g2[i];
+    const float g0 = bf2f(gg.x & 0xFFFF), g1 = bf2f(gg.x >> 16), g2v = bf2f(gg.y & 0xFFFF), g3 = bf2f(gg.y >> 16);
+    o2[i] = make_uint2(pack_bf2(v.x * r * g0, v.y * r * g1), pack_bf2(v.z * r * g2v, v.w * r * g3));
+  }
+}
+
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* x, const int32_t* rows, const uint16_t* g,
+                                                      uint16_t* out, int d, float eps) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const int src = rows ? rows[r] : r;
+  norm_store(reinterpret_cast<const float4*>(x + (size_t)src * d), g, out + (size_t)r * d, d, eps, red);
+}
+
+__global__ __launch_bounds__(256) void embed_rmsnorm_kernel(const int32_t* ids, const uint16_t* E, const uint16_t* g,
+                                                            float* resid, uint16_t* out, int d, float eps) {
+  __shared__ float red[4];
+  const int t = blockIdx.x;
+  const uint2* e2 = reinterpret_cast<const uint2*>(E + (size_t)ids[t] * d);
+  float4* r4 = reinterpret_cast<float4*>(resid + (size_t)t * d);
+  for (int i = threadIdx.x; i < (d >> 2); i += 256) {
+    const uint2 e = e2[i];
+    r4[i] = make_float4(bf2f(e.x & 0xFFFF), bf2f(e.x >> 16), bf2f(e.y & 0xFFFF), bf2f(e.y >> 16));
+  }
+  __syncthreads();
+  norm_store(r4, g, out + (size_t)t * d, d, eps, red);
+}
+
+}  // namespace
+
+hipError_t rmsnorm_launch(const float* x, const int32_t* rows, const uint16_t* g, uint16_t* out, int n_rows, int d,
+                          float eps, hipStream_t st) {
+  if (n_rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(n_rows), dim3(256), 0, st, x, rows, g, out, d, eps);
+  return hipGetLastError();
+}
+
+hipError_t embed_rmsnorm_launch(const int32_t* ids, const uint16_t* E, const uint16_t* g, float* resid,
+                                uint16_t* out, int T, int d, float eps, hipStream_t st) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_rmsnorm_kernel, dim3(T), dim3(256), 0, st, ids, E, g, resid, out, d, eps);
+  return hipGetLastError();
+}
+
+}  // namespace hxf

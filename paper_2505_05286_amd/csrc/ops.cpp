@@ -1,0 +1,234 @@
+// C ABI of the individual kernels (include/hxf_ops.h).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "executor.hpp"
+#include "hxf_ops.h"
+#include "kernels/kernels.hpp"
+
+using namespace hxf;
+
+namespace {
+
+int64_t al(int64_t x) { return (x + 255) & ~int64_t(255); }
+
+int dev_rc(hipError_t e) { return e == hipSuccess ? HXF_OK : HXF_EDEVICE; }
+
+struct DecodeLayout {
+  int64_t items = 0, merges = 0, off_items = 0, off_merges = 0, off_qrow = 0, off_o = 0, off_ml = 0, total = 0;
+};
+
+DecodeLayout decode_layout(int B, int Hq, int Hkv, int dh, const int32_t* ctx) {
+  DecodeLayout L;
+  for (int b = 0; b < B; ++b) L.items += (int64_t)Hkv * ((std::max(ctx[b], 1) + kDecodePartition - 1) / kDecodePartition);
+  L.merges = (int64_t)B * Hkv;
+  const int G = Hq / Hkv;
+  int64_t o = 0;
+  L.off_items = o; o = al(o + L.items * (int64_t)sizeof(DecodeItem));
+  L.off_merges = o; o = al(o + L.merges * (int64_t)sizeof(MergeItem));
+  L.off_qrow = o; o = al(o + (int64_t)B * 4);
+  L.off_o = o; o = al(o + L.items * G * dh * 4);
+  L.off_ml = o; o = al(o + L.items * G * 2 * 4);
+  L.total = o;
+  return L;
+}
+
+bool shapes_ok(int Hq, int Hkv, int dh) {
+  return Hq > 0 && Hkv > 0 && Hq % Hkv == 0 && Hq / Hkv <= 16 && (dh == 64 || dh == 128);
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t hxf_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
+  if (M <= 0 || N <= 0 || K <= 0) return 0;
+  GemmPlan p = gemm_plan(M, N, K, 8);
+  return p.splits > 1 ? (int64_t)p.splits * M * N * 4 : 0;
+}
+
+int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void* C, int32_t ldc, int32_t M, int32_t N,
+                int32_t K, int32_t epi, void* workspace, int64_t ws_bytes, void* stream) {
+  if (!A || !B || !C || M < 0 || N <= 0 || K <= 0 || K % 8 || lda < K || epi < 0 || epi > 3) return HXF_EINVAL;
+  if (epi == HXF_EPI_SWIGLU && (!B2 || N % 32)) return HXF_EINVAL;
+  if (ldc < (epi == HXF_EPI_SWIGLU ? N / 2 : N)) return HXF_EINVAL;
+  if (M == 0) return HXF_OK;
+  GemmPlan p = gemm_plan(M, N, K, 8);
+  if (p.splits > 1 && (!workspace || ws_bytes < (int64_t)p.splits * M * N * 4)) return HXF_ENOMEM;
+  GemmArgs a{};
+  a.A = (const uint16_t*)A;
+  a.B = (const uint16_t*)B;
+  a.B2 = (const uint16_t*)B2;
+  a.C = C;
+  a.partial = (float*)workspace;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.lda = lda;
+  a.ldc = ldc;
+  return dev_rc(gemm_launch(a, epi, p, (hipStream_t)stream));
+}
+
+int hxf_op_rmsnorm(const float* x, const int32_t* rows, const void* g, void* out, int32_t n_rows, int32_t d, float eps,
+                   void* stream) {
+  if (!x || !g || !out || n_rows < 0 || d <= 0 || d % 4) return HXF_EINVAL;
+  return dev_rc(rmsnorm_launch(x, rows, (const uint16_t*)g, (uint16_t*)out, n_rows, d, eps, (hipStream_t)stream));
+}
+
+int hxf_op_embed_rmsnorm(const int32_t* ids, const void* E, const void* g, float* resid, void* out, int32_t T,
+                         int32_t d, float eps, void* stream) {
+  if (!ids || !E || !g || !resid || !out || T < 0 || d <= 0 || d % 4) return HXF_EINVAL;
+  return dev_rc(embed_rmsnorm_launch(ids, (const uint16_t*)E, (const uint16_t*)g, resid, (uint16_t*)out, T, d, eps,
+                                     (hipStream_t)stream));
+}
+
+int hxf_op_rope_table(void* dst, int32_t max_pos, int32_t dh, float base, void* stream) {
+  if (!dst || max_pos <= 0 || dh <= 0 || dh % 2) return HXF_EINVAL;
+  std::vector<float> t;
+  build_rope_table(t, max_pos, dh, base);
+  hipStream_t st = (hipStream_t)stream;
+  if (hipMemcpyAsync(dst, t.data(), t.size() * 4, hipMemcpyHostToDevice, st) != hipSuccess) return HXF_EDEVICE;
+  return dev_rc(hipStreamSynchronize(st));
+}
+
+int hxf_op_rope_kv_write(void* qkv, const int32_t* pos, const int32_t* slot, const void* table, void* k_pool,
+                         void* v_pool, int32_t T, int32_t Hq, int32_t Hkv, int32_t dh, void* stream) {
+  if (!qkv || !pos || !slot || !table || !k_pool || !v_pool || T < 0 || !shapes_ok(Hq, Hkv, dh)) return HXF_EINVAL;
+  return dev_rc(rope_kv_launch((uint16_t*)qkv, pos, slot, (const float2*)table, (uint16_t*)k_pool,
+                               (uint16_t*)v_pool, T, Hq, Hkv, dh, (hipStream_t)stream));
+}
+
+int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k_pool, void* v_pool, int32_t T,
+                      int32_t Hkv, int32_t dh, void* stream) {
+  if (!k || !v || !slot || !k_pool || !v_pool || T < 0 || Hkv <= 0 || dh <= 0) return HXF_EINVAL;
+  return dev_rc(kv_scatter_launch((const uint16_t*)k, (const uint16_t*)v, slot, (uint16_t*)k_pool,
+                                  (uint16_t*)v_pool, T, Hkv, dh, (hipStream_t)stream));
+}
+
+int64_t hxf_op_decode_attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t dh, const int32_t* ctx) {
+  if (B < 0 || !ctx || !shapes_ok(Hq, Hkv, dh)) return -1;
+  return decode_layout(B, Hq, Hkv, dh, ctx).total;
+}
+
+int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_pool, const int32_t* bt,
+                            int32_t bt_stride, const int32_t* ctx, void* out, int32_t B, int32_t Hq, int32_t Hkv,
+                            int32_t dh, void* workspace, int64_t ws_bytes, void* stream) {
+  if (!q || !k_pool || !v_pool || !bt || !ctx || !out || B < 0 || !shapes_ok(Hq, Hkv, dh)) return HXF_EINVAL;
+  if (B == 0) return HXF_OK;
+  for (int b = 0; b < B; ++b)
+    if (ctx[b] <= 0 || (ctx[b] + kPage - 1) / kPage > bt_stride) return HXF_EINVAL;
+  const DecodeLayout L = decode_layout(B, Hq, Hkv, dh, ctx);
+  if (!workspace || ws_bytes < L.total) return HXF_ENOMEM;
+  std::vector<uint8_t> host(L.off_o);
+  auto* items = reinterpret_cast<DecodeItem*>(host.data() + L.off_items);
+  auto* merges = reinterpret_cast<MergeItem*>(host.data() + L.off_merges);
+  auto* qrow = reinterpret_cast<int32_t*>(host.data() + L.off_qrow);
+  int n = 0;
+  for (int b = 0; b < B; ++b) {
+    qrow[b] = b;
+    for (int h = 0; h < Hkv; ++h) {
+      MergeItem mi{b, h, n, 0};
+      for (int t0 = 0; t0 < ctx[b]; t0 += kDecodePartition) {
+        items[n] = DecodeItem{b, h, t0, std::min(ctx[b], t0 + kDecodePartition), n, 0, 0, 0};
+        ++n;
+        ++mi.n_part;
+      }
+      merges[b * Hkv + h] = mi;
+    }
+  }
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t* ws = (uint8_t*)workspace;
+  if (hipMemcpyAsync(ws, host.data(), host.size(), hipMemcpyHostToDevice, st) != hipSuccess) return HXF_EDEVICE;
+  DecodeAttnArgs a{};
+  a.q = (const uint16_t*)q;
+  a.q_row = reinterpret_cast<const int32_t*>(ws + L.off_qrow);
+  a.q_stride = Hq * dh;
+  a.k_pool = (const uint16_t*)k_pool;
+  a.v_pool = (const uint16_t*)v_pool;
+  a.bt = bt;
+  a.bt_stride = bt_stride;
+  a.items = reinterpret_cast<const DecodeItem*>(ws + L.off_items);
+  a.n_items = n;
+  a.merges = reinterpret_cast<const MergeItem*>(ws + L.off_merges);
+  a.n_merges = (int)L.merges;
+  a.part_o = reinterpret_cast<float*>(ws + L.off_o);
+  a.part_ml = reinterpret_cast<float*>(ws + L.off_ml);
+  a.out = (uint16_t*)out;
+  a.out_stride = Hq * dh;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.dh = dh;
+  a.scale_log2 = 1.4426950408889634f / std::sqrt((float)dh);
+  if (decode_attn_launch(a, st) != hipSuccess) return HXF_EDEVICE;
+  return dev_rc(hipStreamSynchronize(st));
+}
+
+int64_t hxf_op_prefill_attention_workspace_bytes(int32_t S, int32_t Hq, int32_t Hkv, const int32_t* n_host) {
+  if (S < 0 || !n_host || Hq <= 0 || Hkv <= 0 || Hq % Hkv) return -1;
+  const int qpi = prefill_queries_per_item(Hq / Hkv);
+  int64_t items = 0;
+  for (int s = 0; s < S; ++s) items += (int64_t)Hkv * ((n_host[s] + qpi - 1) / qpi);
+  return al(items * (int64_t)sizeof(PrefillItem)) + al((int64_t)S * 8);
+}
+
+int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_pool, const int32_t* bt,
+                             int32_t bt_stride, const int32_t* row0, const int32_t* pos0, const int32_t* n_host,
+                             void* out, int32_t S, int32_t Hq, int32_t Hkv, int32_t dh, void* workspace,
+                             int64_t ws_bytes, void* stream) {
+  if (!q || !k_pool || !v_pool || !bt || !row0 || !pos0 || !n_host || !out || S < 0 || !shapes_ok(Hq, Hkv, dh))
+    return HXF_EINVAL;
+  if (S == 0) return HXF_OK;
+  for (int s = 0; s < S; ++s)
+    if (n_host[s] < 0 || pos0[s] < 0 || row0[s] < 0 || (pos0[s] + n_host[s] + kPage - 1) / kPage > bt_stride)
+      return HXF_EINVAL;
+  const int64_t need = hxf_op_prefill_attention_workspace_bytes(S, Hq, Hkv, n_host);
+  if (!workspace || ws_bytes < need) return HXF_ENOMEM;
+  const int qpi = prefill_queries_per_item(Hq / Hkv);
+  std::vector<PrefillItem> items;
+  for (int s = 0; s < S; ++s)
+    for (int h = 0; h < Hkv; ++h)
+      for (int q0 = 0; q0 < n_host[s]; q0 += qpi) items.push_back(PrefillItem{s, h, q0, std::min(qpi, n_host[s] - q0)});
+  const int64_t off_rp = al((int64_t)items.size() * (int64_t)sizeof(PrefillItem));
+  std::vector<uint8_t> host(off_rp + (int64_t)S * 8);
+  std::memcpy(host.data(), items.data(), items.size() * sizeof(PrefillItem));
+  std::memcpy(host.data() + off_rp, row0, (size_t)S * 4);
+  std::memcpy(host.data() + off_rp + S * 4, pos0, (size_t)S * 4);
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t* ws = (uint8_t*)workspace;
+  if (hipMemcpyAsync(ws, host.data(), host.size(), hipMemcpyHostToDevice, st) != hipSuccess) return HXF_EDEVICE;
+  PrefillAttnArgs a{};
+  a.q = (const uint16_t*)q;
+  a.q_stride = Hq * dh;
+  a.row0 = reinterpret_cast<const int32_t*>(ws + off_rp);
+  a.pos0 = reinterpret_cast<const int32_t*>(ws + off_rp + S * 4);
+  a.k_pool = (const uint16_t*)k_pool;
+  a.v_pool = (const uint16_t*)v_pool;
+  a.bt = bt;
+  a.bt_stride = bt_stride;
+  a.items = reinterpret_cast<const PrefillItem*>(ws);
+  a.n_items = (int)items.size();
+  a.out = (uint16_t*)out;
+  a.out_stride = Hq * dh;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.dh = dh;
+  a.scale_log2 = 1.4426950408889634f / std::sqrt((float)dh);
+  if (prefill_attn_launch(a, st) != hipSuccess) return HXF_EDEVICE;
+  return dev_rc(hipStreamSynchronize(st));
+}
+
+int hxf_op_argmax(const float* logits, int32_t* out, int32_t R, int32_t V, void* stream) {
+  if (!logits || !out || R < 0 || V <= 0 || V % 4) return HXF_EINVAL;
+  return dev_rc(argmax_launch(logits, out, R, V, (hipStream_t)stream));
+}
+
+int hxf_op_copy(const void* src, void* dst, int64_t bytes, void* stream) {
+  if (!src || !dst || bytes < 0 || bytes % 16) return HXF_EINVAL;
+  return dev_rc(copy_launch(src, dst, (size_t)bytes, (hipStream_t)stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,382 @@
+"""ctypes binding of libhxf.so (include/hxf.h and include/hxf_ops.h).
+
+Argument marshalling only: every step of the serving iteration runs in the
+library.  Device buffers are passed as integer addresses (e.g.
+``tensor.data_ptr()``) and the stream as a ``hipStream_t`` address.
+"""
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhxf.so")
+
+OK, IDLE = 0, 1
+EINVAL, ENOMEM, ENOTFOUND, ESTATE, EDEVICE = -1, -2, -3, -4, -5
+POLICY_PQ, POLICY_FCFS, POLICY_LLF = 0, 1, 2
+CLOCK_VIRTUAL, CLOCK_MEASURED = 0, 1
+EXEC_HIP, EXEC_NULL = 0, 1
+EPI_BF16, EPI_RESID, EPI_SWIGLU, EPI_F32 = 0, 1, 2, 3
+
+
+class HxfError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"hxf error {code}: {msg}")
+        self.code = code
+
+
+class ModelCfg(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_q_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32),
+                ("vocab", C.c_int32), ("page_size", C.c_int32), ("max_context", C.c_int32),
+                ("rms_eps", C.c_float), ("rope_base", C.c_float)]
+
+
+class SchedCfg(C.Structure):
+    _fields_ = [("n_blocks", C.c_int64), ("max_seqs", C.c_int32), ("chunk_tokens", C.c_int32),
+                ("policy", C.c_int32), ("clock", C.c_int32), ("executor", C.c_int32), ("reserved", C.c_int32),
+                ("cost_ps", C.c_int64 * 4), ("iter_ps", C.c_int64 * 4)]
+
+
+class StageShape(C.Structure):
+    _fields_ = [("l_in", C.c_int32), ("l_out", C.c_int32)]
+
+
+class StageReq(C.Structure):
+    _fields_ = [("workflow_id", C.c_uint64), ("stage_index", C.c_int32), ("prompt_len", C.c_int32),
+                ("workflow_arrival_us", C.c_int64), ("workflow_slo_us", C.c_int64),
+                ("prompt_ids", C.POINTER(C.c_int32)), ("max_new_tokens", C.c_int32), ("retain_kv", C.c_uint8),
+                ("pad_", C.c_uint8 * 3), ("parent_id", C.c_uint64), ("rest", C.POINTER(StageShape)),
+                ("n_rest", C.c_int32), ("n_forced", C.c_int32), ("forced_ids", C.POINTER(C.c_int32))]
+
+
+class LayerWeights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("attn_norm", "wqkv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")]
+
+
+class DeviceBuffers(C.Structure):
+    _fields_ = [("embed", C.c_void_p), ("final_norm", C.c_void_p), ("lm_head", C.c_void_p),
+                ("layers", C.POINTER(LayerWeights)), ("kv_pool", C.c_void_p), ("kv_pool_bytes", C.c_int64),
+                ("workspace", C.c_void_p), ("workspace_bytes", C.c_int64)]
+
+
+class StepInfo(C.Structure):
+    _fields_ = [("n_tokens", C.c_int32), ("n_decode", C.c_int32), ("n_prefill_tokens", C.c_int32),
+                ("n_logit_rows", C.c_int32), ("n_admitted", C.c_int32), ("n_finished", C.c_int32),
+                ("t_iter_us", C.c_int64), ("free_blocks", C.c_int64), ("iteration", C.c_int64)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+class Completion(C.Structure):
+    _fields_ = [("id", C.c_uint64), ("workflow_id", C.c_uint64), ("stage_index", C.c_int32),
+                ("n_generated", C.c_int32), ("t_submit_us", C.c_int64), ("t_first_sched_us", C.c_int64),
+                ("t_first_token_us", C.c_int64), ("t_finish_us", C.c_int64), ("t_slo_us", C.c_int64),
+                ("t_comp_us", C.c_int64), ("met_slo", C.c_int32), ("pad_", C.c_int32)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_ if k != "pad_"}
+
+
+class RequestState(C.Structure):
+    _fields_ = [("state", C.c_int32), ("n_generated", C.c_int32), ("n_kv", C.c_int32), ("n_blocks", C.c_int32),
+                ("t_comp_us", C.c_int64), ("t_slo_us", C.c_int64), ("key_us", C.c_int64),
+                ("t_submit_us", C.c_int64)]
+
+
+class Profile(C.Structure):
+    _fields_ = [("decode_attn_launches", C.c_int64), ("decode_attn_bytes", C.c_int64),
+                ("decode_attn_ms", C.c_double)]
+
+
+_lib = None
+
+# name -> (restype, argtypes)
+_SIGS = {
+    "hxf_create": (C.c_int, [C.POINTER(ModelCfg), C.POINTER(SchedCfg), C.POINTER(C.c_void_p)]),
+    "hxf_destroy": (None, [C.c_void_p]),
+    "hxf_last_error": (C.c_char_p, [C.c_void_p]),
+    "hxf_kv_pool_bytes": (C.c_int64, [C.POINTER(ModelCfg), C.c_int64]),
+    "hxf_workspace_bytes": (C.c_int64, [C.POINTER(ModelCfg), C.POINTER(SchedCfg)]),
+    "hxf_bind": (C.c_int, [C.c_void_p, C.POINTER(DeviceBuffers), C.c_void_p]),
+    "hxf_submit": (C.c_int, [C.c_void_p, C.POINTER(StageReq), C.c_int64, C.POINTER(C.c_uint64)]),
+    "hxf_step": (C.c_int, [C.c_void_p, C.c_int64, C.POINTER(StepInfo)]),
+    "hxf_drain": (C.c_int, [C.c_void_p, C.POINTER(Completion), C.c_int32, C.POINTER(C.c_int32)]),
+    "hxf_completion_tokens": (C.c_int, [C.c_void_p, C.c_uint64, C.POINTER(C.c_int32), C.c_int32,
+                                        C.POINTER(C.c_int32)]),
+    "hxf_release": (C.c_int, [C.c_void_p, C.c_uint64]),
+    "hxf_cancel": (C.c_int, [C.c_void_p, C.c_uint64]),
+    "hxf_queue_order": (C.c_int, [C.c_void_p, C.POINTER(C.c_uint64), C.c_int32, C.POINTER(C.c_int32)]),
+    "hxf_block_table": (C.c_int, [C.c_void_p, C.c_uint64, C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32)]),
+    "hxf_request_state_get": (C.c_int, [C.c_void_p, C.c_uint64, C.POINTER(RequestState)]),
+    "hxf_last_batch": (C.c_int, [C.c_void_p, C.POINTER(C.c_uint64), C.c_int32, C.POINTER(C.c_int32),
+                                 C.POINTER(C.c_uint64), C.c_int32, C.POINTER(C.c_int32)]),
+    "hxf_last_logits": (C.c_int, [C.c_void_p, C.c_uint64, C.POINTER(C.c_float), C.c_int32]),
+    "hxf_profile_enable": (C.c_int, [C.c_void_p, C.c_int32]),
+    "hxf_profile_get": (C.c_int, [C.c_void_p, C.POINTER(Profile)]),
+    # ops
+    "hxf_op_gemm_workspace_bytes": (C.c_int64, [C.c_int32, C.c_int32, C.c_int32]),
+    "hxf_op_gemm": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32,
+                              C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p]),
+    "hxf_op_rmsnorm": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_float,
+                                 C.c_void_p]),
+    "hxf_op_embed_rmsnorm": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                       C.c_int32, C.c_float, C.c_void_p]),
+    "hxf_op_rope_table": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_float, C.c_void_p]),
+    "hxf_op_rope_kv_write": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                       C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_void_p]),
+    "hxf_op_kv_scatter": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                    C.c_int32, C.c_int32, C.c_void_p]),
+    "hxf_op_decode_attention_workspace_bytes": (C.c_int64, [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                                            C.POINTER(C.c_int32)]),
+    "hxf_op_decode_attention": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                          C.POINTER(C.c_int32), C.c_void_p, C.c_int32, C.c_int32, C.c_int32,
+                                          C.c_int32, C.c_void_p, C.c_int64, C.c_void_p]),
+    "hxf_op_prefill_attention_workspace_bytes": (C.c_int64, [C.c_int32, C.c_int32, C.c_int32,
+                                                             C.POINTER(C.c_int32)]),
+    "hxf_op_prefill_attention": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                           C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32),
+                                           C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
+                                           C.c_int64, C.c_void_p]),
+    "hxf_op_argmax": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p]),
+    "hxf_op_copy": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p]),
+}
+
+EXPORTED = tuple(_SIGS)
+
+
+def lib():
+    """Load libhxf.so; raises if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2505_05286_amd.build`")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _i32(a):
+    a = np.ascontiguousarray(a, dtype=np.int32)
+    return a, a.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+def model_cfg(shape, max_context):
+    return ModelCfg(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                    shape.ffn_dim, shape.vocab, shape.page_size, int(max_context), shape.rms_eps, shape.rope_base)
+
+
+def sched_cfg(n_blocks, max_seqs, chunk_tokens, cost_ps, iter_ps, policy=POLICY_PQ, clock=CLOCK_VIRTUAL,
+              executor=EXEC_HIP):
+    s = SchedCfg()
+    s.n_blocks, s.max_seqs, s.chunk_tokens = int(n_blocks), int(max_seqs), int(chunk_tokens)
+    s.policy, s.clock, s.executor = policy, clock, executor
+    for i in range(4):
+        s.cost_ps[i] = int(cost_ps[i])
+        s.iter_ps[i] = int(iter_ps[i])
+    return s
+
+
+def kv_pool_bytes(mcfg, n_blocks):
+    return lib().hxf_kv_pool_bytes(C.byref(mcfg), int(n_blocks))
+
+
+def workspace_bytes(mcfg, scfg):
+    n = lib().hxf_workspace_bytes(C.byref(mcfg), C.byref(scfg))
+    if n < 0:
+        raise HxfError(EINVAL, "invalid configuration")
+    return n
+
+
+class Instance:
+    """One serving instance (hxf_instance*)."""
+
+    def __init__(self, mcfg, scfg):
+        self.L = lib()
+        self.mcfg, self.scfg = mcfg, scfg
+        h = C.c_void_p()
+        rc = self.L.hxf_create(C.byref(mcfg), C.byref(scfg), C.byref(h))
+        if rc != OK:
+            raise HxfError(rc, "hxf_create rejected the configuration")
+        self.h = h
+        self._keep = []
+
+    def close(self):
+        if self.h:
+            self.L.hxf_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, rc, what):
+        if rc < 0:
+            raise HxfError(rc, f"{what}: {self.L.hxf_last_error(self.h).decode()}")
+        return rc
+
+    def bind(self, embed, final_norm, lm_head, layers, kv_pool, kv_pool_bytes, workspace, workspace_bytes, stream=0):
+        arr = (LayerWeights * len(layers))()
+        for i, lw in enumerate(layers):
+            for k in ("attn_norm", "wqkv", "wo", "ffn_norm", "w_gate", "w_up", "w_down"):
+                setattr(arr[i], k, int(lw[k]))
+        b = DeviceBuffers(int(embed), int(final_norm), int(lm_head), arr, int(kv_pool), int(kv_pool_bytes),
+                          int(workspace), int(workspace_bytes))
+        self._check(self.L.hxf_bind(self.h, C.byref(b), C.c_void_p(int(stream))), "hxf_bind")
+
+    def submit(self, now, workflow_id, stage_index, wf_arrival, wf_slo, prompt, max_new, parent=0, retain=False,
+               rest=(), forced=None):
+        p, pp = _i32(prompt)
+        rs = (StageShape * max(1, len(rest)))()
+        for i, (li, lo) in enumerate(rest):
+            rs[i].l_in, rs[i].l_out = int(li), int(lo)
+        q = StageReq()
+        q.workflow_id, q.stage_index, q.prompt_len = int(workflow_id), int(stage_index), len(p)
+        q.workflow_arrival_us, q.workflow_slo_us = int(wf_arrival), int(wf_slo)
+        q.prompt_ids, q.max_new_tokens, q.retain_kv = pp, int(max_new), 1 if retain else 0
+        q.parent_id, q.rest, q.n_rest = int(parent), rs, len(rest)
+        if forced is not None:
+            f, fp = _i32(forced)
+            q.n_forced, q.forced_ids = len(f), fp
+        out = C.c_uint64()
+        self._check(self.L.hxf_submit(self.h, C.byref(q), int(now), C.byref(out)), "hxf_submit")
+        return out.value
+
+    def step(self, now):
+        info = StepInfo()
+        rc = self._check(self.L.hxf_step(self.h, int(now), C.byref(info)), "hxf_step")
+        return rc, info.as_dict()
+
+    def drain(self, cap=4096):
+        buf = (Completion * cap)()
+        n = C.c_int32()
+        self._check(self.L.hxf_drain(self.h, buf, cap, C.byref(n)), "hxf_drain")
+        return [buf[i].as_dict() for i in range(n.value)]
+
+    def tokens(self, rid, cap=1 << 16):
+        buf = (C.c_int32 * cap)()
+        n = C.c_int32()
+        self._check(self.L.hxf_completion_tokens(self.h, int(rid), buf, cap, C.byref(n)), "hxf_completion_tokens")
+        return list(buf[:n.value])
+
+    def release(self, rid):
+        self._check(self.L.hxf_release(self.h, int(rid)), "hxf_release")
+
+    def cancel(self, rid):
+        self._check(self.L.hxf_cancel(self.h, int(rid)), "hxf_cancel")
+
+    def queue_order(self, cap=1 << 16):
+        buf = (C.c_uint64 * cap)()
+        n = C.c_int32()
+        self._check(self.L.hxf_queue_order(self.h, buf, cap, C.byref(n)), "hxf_queue_order")
+        return list(buf[:n.value])
+
+    def block_table(self, rid, cap=1 << 16):
+        buf = (C.c_int32 * cap)()
+        n = C.c_int32()
+        self._check(self.L.hxf_block_table(self.h, int(rid), buf, cap, C.byref(n)), "hxf_block_table")
+        return list(buf[:n.value])
+
+    def request_state(self, rid):
+        s = RequestState()
+        self._check(self.L.hxf_request_state_get(self.h, int(rid), C.byref(s)), "hxf_request_state_get")
+        return {k: getattr(s, k) for k, _ in s._fields_}
+
+    def last_batch(self, cap=4096):
+        ids = (C.c_uint64 * cap)()
+        adm = (C.c_uint64 * cap)()
+        n, na = C.c_int32(), C.c_int32()
+        self._check(self.L.hxf_last_batch(self.h, ids, cap, C.byref(n), adm, cap, C.byref(na)), "hxf_last_batch")
+        return list(ids[:n.value]), list(adm[:na.value])
+
+    def last_logits(self, rid):
+        v = self.mcfg.vocab
+        out = np.empty(v, np.float32)
+        self._check(self.L.hxf_last_logits(self.h, int(rid), out.ctypes.data_as(C.POINTER(C.c_float)), v),
+                    "hxf_last_logits")
+        return out
+
+    def profile_enable(self, on=True):
+        self._check(self.L.hxf_profile_enable(self.h, 1 if on else 0), "hxf_profile_enable")
+
+    def profile(self):
+        p = Profile()
+        self._check(self.L.hxf_profile_get(self.h, C.byref(p)), "hxf_profile_get")
+        return {k: getattr(p, k) for k, _ in p._fields_}
+
+
+# ------------------------------------------------------------------ ops
+def _op(rc, what):
+    if rc != OK:
+        raise HxfError(rc, what)
+
+
+def op_gemm_workspace_bytes(M, N, K):
+    return lib().hxf_op_gemm_workspace_bytes(M, N, K)
+
+
+def op_gemm(A, lda, B, B2, Cp, ldc, M, N, K, epi, ws=0, ws_bytes=0, stream=0):
+    _op(lib().hxf_op_gemm(A, lda, B, B2 or None, Cp, ldc, M, N, K, epi, ws or None, ws_bytes, stream or None),
+        "hxf_op_gemm")
+
+
+def op_rmsnorm(x, rows, g, out, n_rows, d, eps, stream=0):
+    _op(lib().hxf_op_rmsnorm(x, rows or None, g, out, n_rows, d, eps, stream or None), "hxf_op_rmsnorm")
+
+
+def op_embed_rmsnorm(ids, E, g, resid, out, T, d, eps, stream=0):
+    _op(lib().hxf_op_embed_rmsnorm(ids, E, g, resid, out, T, d, eps, stream or None), "hxf_op_embed_rmsnorm")
+
+
+def op_rope_table(dst, max_pos, dh, base, stream=0):
+    _op(lib().hxf_op_rope_table(dst, max_pos, dh, base, stream or None), "hxf_op_rope_table")
+
+
+def op_rope_kv_write(qkv, pos, slot, table, k_pool, v_pool, T, Hq, Hkv, dh, stream=0):
+    _op(lib().hxf_op_rope_kv_write(qkv, pos, slot, table, k_pool, v_pool, T, Hq, Hkv, dh, stream or None),
+        "hxf_op_rope_kv_write")
+
+
+def op_kv_scatter(k, v, slot, k_pool, v_pool, T, Hkv, dh, stream=0):
+    _op(lib().hxf_op_kv_scatter(k, v, slot, k_pool, v_pool, T, Hkv, dh, stream or None), "hxf_op_kv_scatter")
+
+
+def op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, ctx):
+    c, cp = _i32(ctx)
+    return lib().hxf_op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, cp)
+
+
+def op_decode_attention(q, k_pool, v_pool, bt, bt_stride, ctx, out, B, Hq, Hkv, dh, ws, ws_bytes, stream=0):
+    c, cp = _i32(ctx)
+    _op(lib().hxf_op_decode_attention(q, k_pool, v_pool, bt, bt_stride, cp, out, B, Hq, Hkv, dh, ws, ws_bytes,
+                                      stream or None), "hxf_op_decode_attention")
+
+
+def op_prefill_attention_workspace_bytes(S, Hq, Hkv, n):
+    a, ap = _i32(n)
+    return lib().hxf_op_prefill_attention_workspace_bytes(S, Hq, Hkv, ap)
+
+
+def op_prefill_attention(q, k_pool, v_pool, bt, bt_stride, row0, pos0, n, out, S, Hq, Hkv, dh, ws, ws_bytes,
+                         stream=0):
+    r, rp = _i32(row0)
+    p, pp = _i32(pos0)
+    m, mp = _i32(n)
+    _op(lib().hxf_op_prefill_attention(q, k_pool, v_pool, bt, bt_stride, rp, pp, mp, out, S, Hq, Hkv, dh, ws,
+                                       ws_bytes, stream or None), "hxf_op_prefill_attention")
+
+
+def op_argmax(logits, out, R, V, stream=0):
+    _op(lib().hxf_op_argmax(logits, out, R, V, stream or None), "hxf_op_argmax")
+
+
+def op_copy(src, dst, nbytes, stream=0):
+    _op(lib().hxf_op_copy(src, dst, nbytes, stream or None), "hxf_op_copy")

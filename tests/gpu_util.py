@@ -1,0 +1,53 @@
+"""Helpers shared by the GPU tests: bf16 tensors in HBM, read-back, tolerances."""
+import sys
+
+import numpy as np
+
+import synth
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def torch():
+    import torch as t
+    return t
+
+
+def dev_bits(bits):
+    """uint16 bf16 bits (numpy) -> int16 tensor on cuda:0."""
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(bits, np.uint16).view(np.int16)).to("cuda:0")
+
+
+def host_f64(tensor_i16):
+    """int16 bf16-bit tensor -> float64 numpy."""
+    b = tensor_i16.detach().cpu().numpy().view(np.uint16)
+    return synth.bf16_bits_to_f32(b).astype(np.float64)
+
+
+def rand_bf16(rng, shape, scale=1.0):
+    """Random bf16 bits and their exact float64 values."""
+    x = (rng.standard_normal(shape) * scale).astype(np.float32)
+    b = synth.f32_to_bf16_bits(x)
+    return b.reshape(shape), synth.bf16_bits_to_f32(b).astype(np.float64).reshape(shape)
+
+
+def empty_i16(n):
+    t = torch()
+    return t.empty(n, dtype=t.int16, device="cuda:0")
+
+
+def i32(a):
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(a, np.int32)).to("cuda:0")
+
+
+def rel_max_err(got, ref):
+    """max |got - ref| / max |ref| (the logits metric, per row when 2-D)."""
+    got, ref = np.asarray(got, np.float64), np.asarray(ref, np.float64)
+    if got.ndim == 1:
+        return float(np.max(np.abs(got - ref)) / max(np.max(np.abs(ref)), 1e-30))
+    return max(rel_max_err(g, r) for g, r in zip(got, ref))

@@ -1,0 +1,266 @@
+"""Kernel-level parity through the C ABI (include/hxf_ops.h) against the oracle.
+
+Inputs are seeded bf16 values; references are float64 (oracle functions, or a
+plain matmul for the GEMM).  Tolerances follow from bf16 storage of the
+outputs (relative rounding 2^-9) and of the attention probabilities fed to
+the PV product.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import model as M
+from oracle import paged as P
+from paper_2505_05286_amd import hxf
+
+from .gpu_util import dev_bits, empty_i16, host_f64, i32, log, rand_bf16, torch
+
+pytestmark = pytest.mark.gpu
+
+
+def _gemm_case(M_, N, K, epi, seed):
+    t = torch()
+    rng = np.random.default_rng(seed)
+    ab, af = rand_bf16(rng, (M_, K))
+    bb, bf = rand_bf16(rng, (N if epi != hxf.EPI_SWIGLU else N // 2, K), 0.05)
+    A, B = dev_bits(ab), dev_bits(bb)
+    B2 = None
+    if epi == hxf.EPI_SWIGLU:
+        b2b, b2f = rand_bf16(rng, (N // 2, K), 0.05)
+        B2 = dev_bits(b2b)
+    ws_n = hxf.op_gemm_workspace_bytes(M_, N, K)
+    ws = t.empty(max(ws_n, 256), dtype=t.uint8, device="cuda:0")
+    n_out = N // 2 if epi == hxf.EPI_SWIGLU else N
+    if epi in (hxf.EPI_BF16, hxf.EPI_SWIGLU):
+        C = empty_i16(M_ * n_out)
+    else:
+        base = rng.standard_normal((M_, n_out)).astype(np.float32)
+        C = t.from_numpy(base.copy()).to("cuda:0") if epi == hxf.EPI_RESID else t.empty(M_ * n_out, dtype=t.float32,
+                                                                                         device="cuda:0")
+    log(f"gemm M={M_} N={N} K={K} epi={epi} ws={ws_n}")
+    hxf.op_gemm(A.data_ptr(), K, B.data_ptr(), B2.data_ptr() if B2 is not None else 0, C.data_ptr(), n_out, M_, N, K,
+                epi, ws.data_ptr(), ws.numel())
+    t.cuda.synchronize()
+    if epi == hxf.EPI_SWIGLU:
+        ref = M.silu(af @ bf.T) * (af @ b2f.T)
+        got = host_f64(C).reshape(M_, n_out)
+    elif epi == hxf.EPI_BF16:
+        ref = af @ bf.T
+        got = host_f64(C).reshape(M_, n_out)
+    else:
+        ref = af @ bf.T + (base.astype(np.float64) if epi == hxf.EPI_RESID else 0.0)
+        got = C.cpu().numpy().astype(np.float64).reshape(M_, n_out)
+    scale = np.max(np.abs(ref))
+    rtol = 2 ** -7 if epi in (hxf.EPI_BF16, hxf.EPI_SWIGLU) else 1e-5
+    np.testing.assert_allclose(got, ref, rtol=rtol, atol=2e-4 * scale)
+
+
+@pytest.mark.parametrize("M_,N,K", [(1, 64, 64), (37, 200, 136), (64, 6144, 4096), (256, 1024, 688),
+                                    (300, 1000, 688), (2080, 384, 512)])
+@pytest.mark.parametrize("epi", [hxf.EPI_BF16, hxf.EPI_RESID, hxf.EPI_F32])
+def test_gemm(M_, N, K, epi):
+    _gemm_case(M_, N, K, epi, seed=M_ * 7 + N + K + epi)
+
+
+@pytest.mark.parametrize("M_,N,K", [(5, 64, 256), (64, 2 * 688, 256), (300, 2 * 1376, 512), (128, 2 * 14336, 4096)])
+def test_gemm_swiglu(M_, N, K):
+    _gemm_case(M_, N, K, hxf.EPI_SWIGLU, seed=M_ + N + K)
+
+
+@pytest.mark.parametrize("d,rows", [(256, 7), (4096, 64), (5120, 33)])
+def test_rmsnorm_and_embed(d, rows):
+    t = torch()
+    rng = np.random.default_rng(d + rows)
+    x = (rng.standard_normal((rows, d)) * 3).astype(np.float32)
+    gb, gf = rand_bf16(rng, d)
+    xs = t.from_numpy(x).to("cuda:0")
+    G = dev_bits(gb)
+    sel = rng.permutation(rows)[: rows // 2 + 1].astype(np.int32)
+    out = empty_i16(len(sel) * d)
+    hxf.op_rmsnorm(xs.data_ptr(), i32(sel).data_ptr(), G.data_ptr(), out.data_ptr(), len(sel), d, 1e-5)
+    t.cuda.synchronize()
+    ref = M.rmsnorm(x[sel].astype(np.float64), gf, 1e-5)
+    np.testing.assert_allclose(host_f64(out).reshape(len(sel), d), ref, rtol=2 ** -7, atol=1e-6)
+    # embedding gather + norm
+    V = 300
+    eb, ef = rand_bf16(rng, (V, d), 0.02)
+    ids = rng.integers(0, V, rows).astype(np.int32)
+    resid = t.empty(rows * d, dtype=t.float32, device="cuda:0")
+    out2 = empty_i16(rows * d)
+    hxf.op_embed_rmsnorm(i32(ids).data_ptr(), dev_bits(eb).data_ptr(), G.data_ptr(), resid.data_ptr(),
+                         out2.data_ptr(), rows, d, 1e-5)
+    t.cuda.synchronize()
+    np.testing.assert_array_equal(resid.cpu().numpy().reshape(rows, d), ef[ids].astype(np.float32))
+    np.testing.assert_allclose(host_f64(out2).reshape(rows, d), M.rmsnorm(ef[ids], gf, 1e-5), rtol=2 ** -7,
+                               atol=1e-6)
+
+
+def _make_pools(nb, hkv, dh):
+    t = torch()
+    kp = t.zeros(nb * hkv * 16 * dh, dtype=t.int16, device="cuda:0")
+    vp = t.zeros(nb * hkv * 16 * dh, dtype=t.int16, device="cuda:0")
+    return kp, vp
+
+
+def _logical_pool(kp, vp, nb, hkv, dh):
+    """Read the physical pools back into the oracle's logical [nb, 16, Hkv, dh] layout."""
+    k = host_f64(kp).reshape(nb, hkv, 16, dh).transpose(0, 2, 1, 3)
+    v = host_f64(vp).reshape(nb, hkv, dh, 16).transpose(0, 3, 1, 2)
+    return k, v
+
+
+@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128)])
+def test_rope_kv_write(hq, hkv, dh):
+    t = torch()
+    rng = np.random.default_rng(hq + dh)
+    T, nb, maxpos = 50, 20, 9000
+    qkvb, qkvf = rand_bf16(rng, (T, (hq + 2 * hkv) * dh))
+    pos = rng.integers(0, maxpos, T).astype(np.int32)
+    slots = rng.permutation(nb * 16)[:T].astype(np.int32)
+    table = t.empty(maxpos * dh // 2 * 2, dtype=t.float32, device="cuda:0")
+    hxf.op_rope_table(table.data_ptr(), maxpos, dh, 10000.0)
+    qkv = dev_bits(qkvb)
+    kp, vp = _make_pools(nb, hkv, dh)
+    hxf.op_rope_kv_write(qkv.data_ptr(), i32(pos).data_ptr(), i32(slots).data_ptr(), table.data_ptr(), kp.data_ptr(),
+                         vp.data_ptr(), T, hq, hkv, dh)
+    t.cuda.synchronize()
+    q = qkvf[:, : hq * dh].reshape(T, hq, dh)
+    k = qkvf[:, hq * dh:(hq + hkv) * dh].reshape(T, hkv, dh)
+    v = qkvf[:, (hq + hkv) * dh:].reshape(T, hkv, dh)
+    got_q = host_f64(qkv).reshape(T, -1)[:, : hq * dh].reshape(T, hq, dh)
+    np.testing.assert_allclose(got_q, M.apply_rope(q, pos, 1e4), rtol=2 ** -7, atol=2e-3)
+    K, V = _logical_pool(kp, vp, nb, hkv, dh)
+    flatk = K.reshape(nb * 16, hkv, dh)
+    flatv = V.reshape(nb * 16, hkv, dh)
+    np.testing.assert_allclose(flatk[slots], M.apply_rope(k, pos, 1e4), rtol=2 ** -7, atol=2e-3)
+    np.testing.assert_array_equal(flatv[slots], v)
+
+
+def _fill_paged(rng, ctxs, hkv, dh, extra_blocks=3):
+    """Random K/V for sequences of the given lengths written through the library's
+    scatter op into randomly permuted pages.  Returns pools, block tables and the
+    logical copies the oracle reads."""
+    t = torch()
+    pages = [P.pages_for(c) for c in ctxs]
+    nb = sum(pages) + extra_blocks
+    perm = rng.permutation(nb)
+    bts, o = [], 0
+    for n in pages:
+        bts.append(list(perm[o:o + n]))
+        o += n
+    width = max(pages)
+    bt = np.zeros((len(ctxs), width), np.int32)
+    for i, b in enumerate(bts):
+        bt[i, : len(b)] = b
+    kp, vp = _make_pools(nb, hkv, dh)
+    # poison the unused tail of every last page with NaN bit patterns
+    kp.fill_(0x7FC0)
+    vp.fill_(0x7FC0)
+    tot = sum(ctxs)
+    kb, kf = rand_bf16(rng, (tot, hkv, dh))
+    vb, vf = rand_bf16(rng, (tot, hkv, dh))
+    slots = np.concatenate([[P.slot(b, p) for p in range(c)] for b, c in zip(bts, ctxs)]).astype(np.int32)
+    hxf.op_kv_scatter(dev_bits(kb).data_ptr(), dev_bits(vb).data_ptr(), i32(slots).data_ptr(), kp.data_ptr(),
+                      vp.data_ptr(), tot, hkv, dh)
+    t.cuda.synchronize()
+    Kl = np.zeros((nb, 16, hkv, dh))
+    Vl = np.zeros((nb, 16, hkv, dh))
+    o = 0
+    for b, c in zip(bts, ctxs):
+        P.scatter(Kl, b, 0, kf[o:o + c])
+        P.scatter(Vl, b, 0, vf[o:o + c])
+        o += c
+    return kp, vp, bt, bts, Kl, Vl
+
+
+def _decode_case(ctxs, hq, hkv, dh, seed, sample=None):
+    t = torch()
+    rng = np.random.default_rng(seed)
+    B = len(ctxs)
+    log(f"decode attention B={B} hq={hq} hkv={hkv} dh={dh} sum_ctx={sum(ctxs)}")
+    kp, vp, bt, bts, Kl, Vl = _fill_paged(rng, ctxs, hkv, dh)
+    qb, qf = rand_bf16(rng, (B, hq, dh))
+    out = empty_i16(B * hq * dh)
+    wsn = hxf.op_decode_attention_workspace_bytes(B, hq, hkv, dh, ctxs)
+    ws = t.empty(wsn, dtype=t.uint8, device="cuda:0")
+    hxf.op_decode_attention(dev_bits(qb).data_ptr(), kp.data_ptr(), vp.data_ptr(), i32(bt).data_ptr(), bt.shape[1],
+                            ctxs, out.data_ptr(), B, hq, hkv, dh, ws.data_ptr(), wsn)
+    t.cuda.synchronize()
+    got = host_f64(out).reshape(B, hq, dh)
+    seqs = range(B) if sample is None else sample
+    for b in seqs:
+        c = ctxs[b]
+        ref = P.paged_attention(qf[b:b + 1], np.array([c - 1]), Kl, Vl, bts[b], c)[0]
+        np.testing.assert_allclose(got[b], ref, rtol=1e-2, atol=1e-2, err_msg=f"seq {b} ctx {c}")
+
+
+@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128)])
+def test_decode_attention_ragged(hq, hkv, dh):
+    ctxs = [1, 15, 16, 17, 31, 32, 33, 255, 256, 257, 511, 700, 1500]
+    _decode_case(ctxs, hq, hkv, dh, seed=hq)
+
+
+def test_decode_attention_cfg2_full_size_sampled():
+    """Config-2 shape: 64 sequences with lognormal contexts (median 3000, clipped to
+    [1024, 8192]), 32 q-heads / 8 kv-heads of 128; oracle on 12 sampled sequences."""
+    ctxs, _ = synth.workloads.cfg2_contexts()
+    ctxs = [int(c) for c in ctxs]
+    order = np.argsort(ctxs)
+    sample = sorted(set(list(order[:4]) + list(order[-4:]) + list(order[30:34])))
+    _decode_case(ctxs, 32, 8, 128, seed=2, sample=sample)
+
+
+def _prefill_case(chunks, hq, hkv, dh, seed):
+    """chunks: list of (pos0, n): n new queries at positions pos0.. over a context of pos0+n."""
+    t = torch()
+    rng = np.random.default_rng(seed)
+    ctxs = [p0 + n for p0, n in chunks]
+    log(f"prefill attention chunks={chunks} hq={hq} hkv={hkv} dh={dh}")
+    kp, vp, bt, bts, Kl, Vl = _fill_paged(rng, ctxs, hkv, dh)
+    ns = [n for _, n in chunks]
+    row0 = np.concatenate([[0], np.cumsum(ns)[:-1]]).astype(np.int32)
+    T = sum(ns)
+    qb, qf = rand_bf16(rng, (T, hq, dh))
+    out = empty_i16(T * hq * dh)
+    S = len(chunks)
+    wsn = hxf.op_prefill_attention_workspace_bytes(S, hq, hkv, ns)
+    ws = t.empty(max(wsn, 256), dtype=t.uint8, device="cuda:0")
+    hxf.op_prefill_attention(dev_bits(qb).data_ptr(), kp.data_ptr(), vp.data_ptr(), i32(bt).data_ptr(), bt.shape[1],
+                             row0, [p for p, _ in chunks], ns, out.data_ptr(), S, hq, hkv, dh, ws.data_ptr(),
+                             ws.numel())
+    t.cuda.synchronize()
+    got = host_f64(out).reshape(T, hq, dh)
+    for s, (p0, n) in enumerate(chunks):
+        ref = P.paged_attention(qf[row0[s]:row0[s] + n], np.arange(p0, p0 + n), Kl, Vl, bts[s], p0 + n)
+        np.testing.assert_allclose(got[row0[s]:row0[s] + n], ref, rtol=1e-2, atol=1e-2, err_msg=f"chunk {s}")
+
+
+@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128)])
+def test_prefill_attention_chunks(hq, hkv, dh):
+    chunks = [(0, 1), (0, 17), (0, 64), (16, 16), (40, 9), (100, 77), (0, 300), (513, 130)]
+    _prefill_case(chunks, hq, hkv, dh, seed=dh + hq)
+
+
+def test_argmax_ties_and_lowest_index():
+    t = torch()
+    rng = np.random.default_rng(5)
+    R, V = 9, 128256
+    x = rng.standard_normal((R, V)).astype(np.float32)
+    x[0, [5, 77, 100000]] = 50.0          # tie: lowest index 5
+    x[1, :] = 1.0                          # all equal: index 0
+    x[2, V - 1] = 99.0                     # last element
+    x[3, [7, 8]] = -np.inf
+    out = t.empty(R, dtype=t.int32, device="cuda:0")
+    xs = t.from_numpy(x).to("cuda:0")
+    hxf.op_argmax(xs.data_ptr(), out.data_ptr(), R, V)
+    t.cuda.synchronize()
+    np.testing.assert_array_equal(out.cpu().numpy(), M.argmax_lowest(x))
+
+
+def test_copy_probe():
+    t = torch()
+    a = t.arange(1 << 20, dtype=t.int32, device="cuda:0")
+    b = t.zeros_like(a)
+    hxf.op_copy(a.data_ptr(), b.data_ptr(), a.numel() * 4)
+    t.cuda.synchronize()
+    assert t.equal(a, b)
