@@ -77,7 +77,8 @@ def test_rmsnorm_and_embed(d, rows):
     G = dev_bits(gb)
     sel = rng.permutation(rows)[: rows // 2 + 1].astype(np.int32)
     out = empty_i16(len(sel) * d)
-    hxf.op_rmsnorm(xs.data_ptr(), i32(sel).data_ptr(), G.data_ptr(), out.data_ptr(), len(sel), d, 1e-5)
+    sel_d = i32(sel)
+    hxf.op_rmsnorm(xs.data_ptr(), sel_d.data_ptr(), G.data_ptr(), out.data_ptr(), len(sel), d, 1e-5)
     t.cuda.synchronize()
     ref = M.rmsnorm(x[sel].astype(np.float64), gf, 1e-5)
     np.testing.assert_allclose(host_f64(out).reshape(len(sel), d), ref, rtol=2 ** -7, atol=1e-6)
@@ -87,8 +88,9 @@ def test_rmsnorm_and_embed(d, rows):
     ids = rng.integers(0, V, rows).astype(np.int32)
     resid = t.empty(rows * d, dtype=t.float32, device="cuda:0")
     out2 = empty_i16(rows * d)
-    hxf.op_embed_rmsnorm(i32(ids).data_ptr(), dev_bits(eb).data_ptr(), G.data_ptr(), resid.data_ptr(),
-                         out2.data_ptr(), rows, d, 1e-5)
+    ids_d, E = i32(ids), dev_bits(eb)
+    hxf.op_embed_rmsnorm(ids_d.data_ptr(), E.data_ptr(), G.data_ptr(), resid.data_ptr(), out2.data_ptr(), rows, d,
+                         1e-5)
     t.cuda.synchronize()
     np.testing.assert_array_equal(resid.cpu().numpy().reshape(rows, d), ef[ids].astype(np.float32))
     np.testing.assert_allclose(host_f64(out2).reshape(rows, d), M.rmsnorm(ef[ids], gf, 1e-5), rtol=2 ** -7,
@@ -121,7 +123,8 @@ def test_rope_kv_write(hq, hkv, dh):
     hxf.op_rope_table(table.data_ptr(), maxpos, dh, 10000.0)
     qkv = dev_bits(qkvb)
     kp, vp = _make_pools(nb, hkv, dh)
-    hxf.op_rope_kv_write(qkv.data_ptr(), i32(pos).data_ptr(), i32(slots).data_ptr(), table.data_ptr(), kp.data_ptr(),
+    pos_d, slots_d = i32(pos), i32(slots)
+    hxf.op_rope_kv_write(qkv.data_ptr(), pos_d.data_ptr(), slots_d.data_ptr(), table.data_ptr(), kp.data_ptr(),
                          vp.data_ptr(), T, hq, hkv, dh)
     t.cuda.synchronize()
     q = qkvf[:, : hq * dh].reshape(T, hq, dh)
@@ -160,8 +163,8 @@ def _fill_paged(rng, ctxs, hkv, dh, extra_blocks=3):
     kb, kf = rand_bf16(rng, (tot, hkv, dh))
     vb, vf = rand_bf16(rng, (tot, hkv, dh))
     slots = np.concatenate([[P.slot(b, p) for p in range(c)] for b, c in zip(bts, ctxs)]).astype(np.int32)
-    hxf.op_kv_scatter(dev_bits(kb).data_ptr(), dev_bits(vb).data_ptr(), i32(slots).data_ptr(), kp.data_ptr(),
-                      vp.data_ptr(), tot, hkv, dh)
+    k_d, v_d, slots_d = dev_bits(kb), dev_bits(vb), i32(slots)
+    hxf.op_kv_scatter(k_d.data_ptr(), v_d.data_ptr(), slots_d.data_ptr(), kp.data_ptr(), vp.data_ptr(), tot, hkv, dh)
     t.cuda.synchronize()
     Kl = np.zeros((nb, 16, hkv, dh))
     Vl = np.zeros((nb, 16, hkv, dh))
@@ -183,8 +186,9 @@ def _decode_case(ctxs, hq, hkv, dh, seed, sample=None):
     out = empty_i16(B * hq * dh)
     wsn = hxf.op_decode_attention_workspace_bytes(B, hq, hkv, dh, ctxs)
     ws = t.empty(wsn, dtype=t.uint8, device="cuda:0")
-    hxf.op_decode_attention(dev_bits(qb).data_ptr(), kp.data_ptr(), vp.data_ptr(), i32(bt).data_ptr(), bt.shape[1],
-                            ctxs, out.data_ptr(), B, hq, hkv, dh, ws.data_ptr(), wsn)
+    q_d, bt_d = dev_bits(qb), i32(bt)
+    hxf.op_decode_attention(q_d.data_ptr(), kp.data_ptr(), vp.data_ptr(), bt_d.data_ptr(), bt.shape[1], ctxs,
+                            out.data_ptr(), B, hq, hkv, dh, ws.data_ptr(), wsn)
     t.cuda.synchronize()
     got = host_f64(out).reshape(B, hq, dh)
     seqs = range(B) if sample is None else sample
@@ -225,9 +229,9 @@ def _prefill_case(chunks, hq, hkv, dh, seed):
     S = len(chunks)
     wsn = hxf.op_prefill_attention_workspace_bytes(S, hq, hkv, ns)
     ws = t.empty(max(wsn, 256), dtype=t.uint8, device="cuda:0")
-    hxf.op_prefill_attention(dev_bits(qb).data_ptr(), kp.data_ptr(), vp.data_ptr(), i32(bt).data_ptr(), bt.shape[1],
-                             row0, [p for p, _ in chunks], ns, out.data_ptr(), S, hq, hkv, dh, ws.data_ptr(),
-                             ws.numel())
+    q_d, bt_d = dev_bits(qb), i32(bt)
+    hxf.op_prefill_attention(q_d.data_ptr(), kp.data_ptr(), vp.data_ptr(), bt_d.data_ptr(), bt.shape[1], row0,
+                             [p for p, _ in chunks], ns, out.data_ptr(), S, hq, hkv, dh, ws.data_ptr(), ws.numel())
     t.cuda.synchronize()
     got = host_f64(out).reshape(T, hq, dh)
     for s, (p0, n) in enumerate(chunks):
