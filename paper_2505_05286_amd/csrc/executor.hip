@@ -344,6 +344,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
         prof.decode_attn_launches += 1;
         prof.decode_attn_bytes += kv_tokens * 2 * dh * 2;
       }
+      HXF_HIP(decode_merge_launch(da, st_));
     }
     HXF_HIP(prefill_attn_launch(pa, st_));
     if (int rc = gemm(attn, hq * dh, (const uint16_t*)L.wo, nullptr, resid, d, T, d, hq * dh, EPI_RESID, err))

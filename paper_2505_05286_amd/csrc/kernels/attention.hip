@@ -247,16 +247,18 @@ int prefill_queries_per_item(int group) { return 4 * (16 / group); }
 
 hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st) {
   if (a.n_items <= 0) return hipSuccess;
-  const int G = a.Hq / a.Hkv;
-  if (a.dh == 128) {
-    hipLaunchKernelGGL(decode_attn_kernel<128>, dim3((a.n_items + 3) / 4), dim3(256), 0, st, a);
-    hipLaunchKernelGGL(decode_merge_kernel<128>, dim3((a.n_merges * G + 3) / 4), dim3(256), 0, st, a);
-  } else if (a.dh == 64) {
-    hipLaunchKernelGGL(decode_attn_kernel<64>, dim3((a.n_items + 3) / 4), dim3(256), 0, st, a);
-    hipLaunchKernelGGL(decode_merge_kernel<64>, dim3((a.n_merges * G + 3) / 4), dim3(256), 0, st, a);
-  } else {
-    return hipErrorInvalidValue;
-  }
+  if (a.dh == 128) hipLaunchKernelGGL(decode_attn_kernel<128>, dim3((a.n_items + 3) / 4), dim3(256), 0, st, a);
+  else if (a.dh == 64) hipLaunchKernelGGL(decode_attn_kernel<64>, dim3((a.n_items + 3) / 4), dim3(256), 0, st, a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st) {
+  if (a.n_merges <= 0) return hipSuccess;
+  const int jobs = a.n_merges * (a.Hq / a.Hkv);
+  if (a.dh == 128) hipLaunchKernelGGL(decode_merge_kernel<128>, dim3((jobs + 3) / 4), dim3(256), 0, st, a);
+  else if (a.dh == 64) hipLaunchKernelGGL(decode_merge_kernel<64>, dim3((jobs + 3) / 4), dim3(256), 0, st, a);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

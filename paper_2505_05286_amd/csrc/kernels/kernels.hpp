@@ -82,7 +82,9 @@ struct DecodeAttnArgs {
   int Hq, Hkv, dh;
   float scale_log2;        // log2(e) / sqrt(dh)
 };
+// Split-K partials of every work item, then the log-sum-exp merge into `out`.
 hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st);
+hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st);
 
 // One prefill work item: queries [q0, q0 + nq) (chunk-local) of entry `entry`, kv-head `kvh`.
 struct PrefillItem {

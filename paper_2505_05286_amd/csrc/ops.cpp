@@ -163,7 +163,7 @@ int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_poo
   a.Hkv = Hkv;
   a.dh = dh;
   a.scale_log2 = 1.4426950408889634f / std::sqrt((float)dh);
-  if (decode_attn_launch(a, st) != hipSuccess) return HXF_EDEVICE;
+  if (decode_attn_launch(a, st) != hipSuccess || decode_merge_launch(a, st) != hipSuccess) return HXF_EDEVICE;
   return dev_rc(hipStreamSynchronize(st));
 }
 
