@@ -11,10 +11,11 @@
  * `workspace` with an asynchronous host-to-device copy and synchronise the
  * stream before returning, so their host arguments may be freed afterwards.
  *
- * Physical KV layout (one layer): K pool [n_blocks][Hkv][16][dh] then a
- * separate V pool [n_blocks][Hkv][dh][16] (V transposed inside a page); the
- * token at position p of a sequence with block table bt lives in slot
- * bt[p/16]*16 + p%16.
+ * Physical KV layout (one layer), kv-head major: K pool [Hkv][n_blocks][dh/8][16][8]
+ * (element (token t, dim d) of a page at ((d/8)*16 + t)*8 + d%8), then a separate
+ * V pool [Hkv][n_blocks][dh][16] (V transposed inside a page); the token at
+ * position p of a sequence with block table bt lives in slot bt[p/16]*16 + p%16.
+ * `n_blocks` is the number of pages of the pool (its kv-head stride).
  */
 #ifndef HXF_OPS_H
 #define HXF_OPS_H
@@ -58,11 +59,12 @@ int hxf_op_rope_table(void* dst, int32_t max_pos, int32_t head_dim, float base, 
 /* qkv bf16 [T, (Hq+2Hkv)*dh] rows (q heads, k heads, v heads): rotate-half RoPE of q (in place)
  * and k at pos[t]; write rotated k and v to slot[t] of the K and V pools. */
 int hxf_op_rope_kv_write(void* qkv, const int32_t* pos, const int32_t* slot, const void* rope_table, void* k_pool,
-                         void* v_pool, int32_t T, int32_t Hq, int32_t Hkv, int32_t head_dim, void* stream);
+                         void* v_pool, int64_t n_blocks, int32_t T, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                         void* stream);
 
 /* Write k, v bf16 [T, Hkv, dh] to slot[t] of the pools (no rotation). */
-int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k_pool, void* v_pool, int32_t T,
-                      int32_t Hkv, int32_t head_dim, void* stream);
+int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k_pool, void* v_pool, int64_t n_blocks,
+                      int32_t T, int32_t Hkv, int32_t head_dim, void* stream);
 
 /* Decode attention, one query token per sequence: q bf16 [B, Hq, dh] (rotated), attends to positions
  * [0, ctx_host[b]) of sequence b through block table bt [B, bt_stride] (device); out bf16 [B, Hq, dh].
@@ -70,7 +72,7 @@ int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k
  * workspace: hxf_op_decode_attention_workspace_bytes(...) bytes. */
 int64_t hxf_op_decode_attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
                                                 const int32_t* ctx_host);
-int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_pool, const int32_t* bt,
+int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_pool, int64_t n_blocks, const int32_t* bt,
                             int32_t bt_stride, const int32_t* ctx_host, void* out, int32_t B, int32_t Hq, int32_t Hkv,
                             int32_t head_dim, void* workspace, int64_t workspace_bytes, void* stream);
 
@@ -78,7 +80,7 @@ int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_poo
  * pos0_host[s] .. pos0_host[s]+n-1, stored at rows row0_host[s].. of q bf16 [*, Hq, dh];
  * it attends to positions [0, pos0+i] of its block table row bt[s] (device).  out rows as q. */
 int64_t hxf_op_prefill_attention_workspace_bytes(int32_t S, int32_t Hq, int32_t Hkv, const int32_t* n_host);
-int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_pool, const int32_t* bt,
+int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_pool, int64_t n_blocks, const int32_t* bt,
                              int32_t bt_stride, const int32_t* row0_host, const int32_t* pos0_host,
                              const int32_t* n_host, void* out, int32_t S, int32_t Hq, int32_t Hkv, int32_t head_dim,
                              void* workspace, int64_t workspace_bytes, void* stream);

@@ -285,6 +285,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   da.q = qkv;
   da.q_row = dm + o_row0;
   da.q_stride = qkv_w;
+  da.n_blocks = s_.n_blocks;
   da.bt = dm + o_bt;
   da.bt_stride = bt_w;
   da.items = reinterpret_cast<const DecodeItem*>(dm + o_ditems);
@@ -302,6 +303,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   PrefillAttnArgs pa{};
   pa.q = qkv;
   pa.q_stride = qkv_w;
+  pa.n_blocks = s_.n_blocks;
   pa.row0 = dm + o_row0;
   pa.pos0 = dm + o_pos0;
   pa.bt = dm + o_bt;
@@ -326,7 +328,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     uint16_t* vp = kp + layer_pool;
     if (l > 0) HXF_HIP(rmsnorm_launch(resid, nullptr, (const uint16_t*)L.attn_norm, h, T, d, m_.rms_eps, st_));
     if (int rc = gemm(h, d, (const uint16_t*)L.wqkv, nullptr, qkv, qkv_w, T, qkv_w, d, EPI_BF16, err)) return rc;
-    HXF_HIP(rope_kv_launch(qkv, dm + o_pos, dm + o_slot, rope, kp, vp, T, hq, hkv, dh, st_));
+    HXF_HIP(rope_kv_launch(qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq, hkv, dh, st_));
     da.k_pool = pa.k_pool = kp;
     da.v_pool = pa.v_pool = vp;
     if (da.n_items) {

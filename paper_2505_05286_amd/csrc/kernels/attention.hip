@@ -13,8 +13,10 @@
 // column l%16), the score tile that QK^T leaves in a lane is exactly the P^T
 // operand the PV product needs from that lane, so softmax runs in registers
 // with only two cross-lane exchanges per page pair (xor 16, xor 32).
-// K pages are read as [token][dh] rows, V pages as [dh][token] rows (the pool
-// stores V transposed within a page), both as 16-byte / 8-byte vector loads.
+// K pages are stored in MFMA operand order (see kernels.hpp), so each K load
+// instruction of a wavefront reads 1 KiB of contiguous memory; V pages are
+// stored transposed ([dh][token]) and read as 8-byte vectors, 512 contiguous
+// bytes per instruction.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -38,26 +40,22 @@ struct AttnState {
 };
 
 template <int DH>
+__device__ __forceinline__ void load_page(uint4* k, uint2* v, const uint16_t* k_pool, const uint16_t* v_pool,
+                                          size_t tile, int lane) {
+  const uint16_t* kp = k_pool + tile + lane * 8;
+  const uint16_t* vp = v_pool + tile + (lane & 15) * kPage + (lane >> 4) * 4;
+#pragma unroll
+  for (int s = 0; s < DH / 32; ++s) k[s] = load_stream16(kp + s * 512);
+#pragma unroll
+  for (int n = 0; n < DH / 16; ++n) v[n] = load_stream8(vp + n * 16 * kPage);
+}
+
+template <int DH>
 __device__ __forceinline__ void load_pair(PairRegs<DH>& R, const uint16_t* k_pool, const uint16_t* v_pool,
-                                          const int32_t* bt, int Hkv, int kvh, int page, int t_end, int lane) {
-  const int tok = lane & 15, rq = lane >> 4;
-  {
-    const size_t tile = ((size_t)bt[page] * Hkv + kvh) * kPage * DH;
-    const uint16_t* kp = k_pool + tile + tok * DH + rq * 8;
-    const uint16_t* vp = v_pool + tile + (lane & 15) * kPage + rq * 4;
-#pragma unroll
-    for (int s = 0; s < DH / 32; ++s) R.ka[s] = *reinterpret_cast<const uint4*>(kp + s * 32);
-#pragma unroll
-    for (int n = 0; n < DH / 16; ++n) R.va[n] = *reinterpret_cast<const uint2*>(vp + n * 16 * kPage);
-  }
+                                          const int32_t* bt, int64_t nb, int kvh, int page, int t_end, int lane) {
+  load_page<DH>(R.ka, R.va, k_pool, v_pool, kv_tile(kvh, nb, bt[page], DH), lane);
   if ((page + 1) * kPage < t_end) {
-    const size_t tile = ((size_t)bt[page + 1] * Hkv + kvh) * kPage * DH;
-    const uint16_t* kp = k_pool + tile + tok * DH + rq * 8;
-    const uint16_t* vp = v_pool + tile + (lane & 15) * kPage + rq * 4;
-#pragma unroll
-    for (int s = 0; s < DH / 32; ++s) R.kb[s] = *reinterpret_cast<const uint4*>(kp + s * 32);
-#pragma unroll
-    for (int n = 0; n < DH / 16; ++n) R.vb[n] = *reinterpret_cast<const uint2*>(vp + n * 16 * kPage);
+    load_page<DH>(R.kb, R.vb, k_pool, v_pool, kv_tile(kvh, nb, bt[page + 1], DH), lane);
   } else {
 #pragma unroll
     for (int s = 0; s < DH / 32; ++s) R.kb[s] = make_uint4(0, 0, 0, 0);
@@ -66,18 +64,15 @@ __device__ __forceinline__ void load_pair(PairRegs<DH>& R, const uint16_t* k_poo
   }
 }
 
-// Zero the bf16 V entries of tokens at or beyond t_end (their memory may hold
-// anything; a zero probability times a NaN would still be NaN).
-__device__ __forceinline__ uint2 mask_v(uint2 v, int first_tok, int t_end) {
-  const int n_ok = t_end - first_tok;   // valid tokens among the 4 held
-  if (n_ok >= 4) return v;
-  if (n_ok <= 0) return make_uint2(0, 0);
-  if (n_ok == 1) return make_uint2(v.x & 0xFFFFu, 0);
-  if (n_ok == 2) return make_uint2(v.x, 0);
-  return make_uint2(v.x, v.y & 0xFFFFu);
+// Mask keeping the first n (0..4) of the 4 bf16 V entries a lane holds for one
+// page: tokens at or beyond the context end may hold anything, and a zero
+// probability times a NaN would still be NaN.
+__device__ __forceinline__ uint2 keep_mask(int n) {
+  const uint64_t m = n >= 4 ? ~0ull : (n <= 0 ? 0ull : ((1ull << (16 * n)) - 1));
+  return make_uint2((uint32_t)m, (uint32_t)(m >> 32));
 }
 
-template <int DH>
+template <int DH, bool CAUSAL>
 __device__ __forceinline__ void compute_pair(AttnState<DH>& S, const PairRegs<DH>& R, const bf16x8* qf, int page,
                                              int t_end, int lim, float scale_log2, int lane) {
   const int rq = lane >> 4;
@@ -89,22 +84,34 @@ __device__ __forceinline__ void compute_pair(AttnState<DH>& S, const PairRegs<DH
   }
   const int ta = page * kPage + rq * 4;   // first token of this lane's rows in page a
   const int tb = ta + kPage;
+  const bool full = (page + 2) * kPage <= t_end;   // wavefront-uniform
   float x[8];
-  float mx = kNegInf;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const bool oka = (ta + e) < t_end && (ta + e) <= lim;
-    const bool okb = (tb + e) < t_end && (tb + e) <= lim;
-    x[e] = oka ? sa[e] * scale_log2 : kNegInf;
-    x[4 + e] = okb ? sb[e] * scale_log2 : kNegInf;
-    mx = fmaxf(mx, fmaxf(x[e], x[4 + e]));
+    x[e] = sa[e] * scale_log2;
+    x[4 + e] = sb[e] * scale_log2;
   }
+  if (!full) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (ta + e >= t_end) x[e] = kNegInf;
+      if (tb + e >= t_end) x[4 + e] = kNegInf;
+    }
+  }
+  if (CAUSAL) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (ta + e > lim) x[e] = kNegInf;
+      if (tb + e > lim) x[4 + e] = kNegInf;
+    }
+  }
+  float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
   mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
   mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
   const float m_new = fmaxf(S.m, mx);
   const float alpha = exp2f(S.m - m_new);
-  float psum = 0.f;
   float p[8];
+  float psum = 0.f;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     p[e] = exp2f(x[e] - m_new);
@@ -112,22 +119,26 @@ __device__ __forceinline__ void compute_pair(AttnState<DH>& S, const PairRegs<DH
   }
   S.l = S.l * alpha + psum;
   S.m = m_new;
-  const uint4 pw = make_uint4(pack_bf2(p[0], p[1]), pack_bf2(p[2], p[3]), pack_bf2(p[4], p[5]), pack_bf2(p[6], p[7]));
-  const bf16x8 pf = as_bf16x8(pw);
+  const bf16x8 pf = as_bf16x8(make_uint4(pack_bf2(p[0], p[1]), pack_bf2(p[2], p[3]), pack_bf2(p[4], p[5]),
+                                         pack_bf2(p[6], p[7])));
+  uint2 ma = make_uint2(~0u, ~0u), mb = make_uint2(~0u, ~0u);
+  if (!full) {
+    ma = keep_mask(t_end - ta);
+    mb = keep_mask(t_end - tb);
+  }
 #pragma unroll
   for (int n = 0; n < DH / 16; ++n) {
     S.acc[n] *= alpha;
-    const uint2 a = mask_v(R.va[n], ta, t_end);
-    const uint2 b = mask_v(R.vb[n], tb, t_end);
-    S.acc[n] = mfma16x16x32(as_bf16x8(make_uint4(a.x, a.y, b.x, b.y)), pf, S.acc[n]);
+    const uint4 v = make_uint4(R.va[n].x & ma.x, R.va[n].y & ma.y, R.vb[n].x & mb.x, R.vb[n].y & mb.y);
+    S.acc[n] = mfma16x16x32(as_bf16x8(v), pf, S.acc[n]);
   }
 }
 
 // Attend the lane's column to tokens [t_begin, t_end) (t_begin page aligned);
 // tokens beyond `lim` are masked for this column.
-template <int DH>
+template <int DH, bool CAUSAL>
 __device__ __forceinline__ void attn_range(AttnState<DH>& S, const bf16x8* qf, const uint16_t* k_pool,
-                                           const uint16_t* v_pool, const int32_t* bt, int Hkv, int kvh, int t_begin,
+                                           const uint16_t* v_pool, const int32_t* bt, int64_t nb, int kvh, int t_begin,
                                            int t_end, int lim, float scale_log2, int lane) {
 #pragma unroll
   for (int n = 0; n < DH / 16; ++n) S.acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -135,10 +146,10 @@ __device__ __forceinline__ void attn_range(AttnState<DH>& S, const bf16x8* qf, c
   S.l = 0.f;
   const int p0 = t_begin / kPage, p_end = (t_end + kPage - 1) / kPage;
   PairRegs<DH> cur, nxt;
-  load_pair<DH>(cur, k_pool, v_pool, bt, Hkv, kvh, p0, t_end, lane);
+  load_pair<DH>(cur, k_pool, v_pool, bt, nb, kvh, p0, t_end, lane);
   for (int p = p0; p < p_end; p += 2) {
-    if (p + 2 < p_end) load_pair<DH>(nxt, k_pool, v_pool, bt, Hkv, kvh, p + 2, t_end, lane);
-    compute_pair<DH>(S, cur, qf, p, t_end, lim, scale_log2, lane);
+    if (p + 2 < p_end) load_pair<DH>(nxt, k_pool, v_pool, bt, nb, kvh, p + 2, t_end, lane);
+    compute_pair<DH, CAUSAL>(S, cur, qf, p, t_end, lim, scale_log2, lane);
     cur = nxt;
   }
   S.l += __shfl_xor(S.l, 16, kWave);
@@ -166,8 +177,8 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(DecodeAttnArgs a) {
   bf16x8 qf[DH / 32];
   load_q<DH>(qf, a.q + (size_t)a.q_row[it.entry] * a.q_stride + head * DH, ok, lane);
   AttnState<DH> S;
-  attn_range<DH>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)it.entry * a.bt_stride, a.Hkv, it.kvh, it.t0, it.t1,
-                 0x7FFFFFFF, a.scale_log2, lane);
+  attn_range<DH, false>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)it.entry * a.bt_stride, a.n_blocks, it.kvh, it.t0,
+                        it.t1, 0x7FFFFFFF, a.scale_log2, lane);
   if (!ok) return;
   const int rq = lane >> 4;
   float* o = a.part_o + ((size_t)it.part * G + col) * DH;
@@ -178,6 +189,8 @@ __global__ __launch_bounds__(256) void decode_attn_kernel(DecodeAttnArgs a) {
 }
 
 // Log-sum-exp merge of the split-K partials; one wavefront per (entry, q-head).
+// The partials' maxima are reduced across lanes first, then the weighted sums
+// are accumulated with independent (unrolled) loads.
 template <int DH>
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeAttnArgs a) {
   const int G = a.Hq / a.Hkv;
@@ -186,24 +199,34 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeAttnArgs a) {
   const int lane = threadIdx.x & 63;
   const MergeItem mi = a.merges[job / G];
   const int g = job % G;
+  const float2* ml = reinterpret_cast<const float2*>(a.part_ml);
   float M = kNegInf;
-  for (int p = 0; p < mi.n_part; ++p) M = fmaxf(M, a.part_ml[((size_t)(mi.part0 + p) * G + g) * 2]);
-  float L = 0.f;
-  float acc[DH / 64];
+  for (int p = lane; p < mi.n_part; p += kWave) M = fmaxf(M, ml[(size_t)(mi.part0 + p) * G + g].x);
+  M = wave_max(M);
+  constexpr int PER = DH / 64;   // dims per lane
+  float acc[PER];
 #pragma unroll
-  for (int k = 0; k < DH / 64; ++k) acc[k] = 0.f;
+  for (int k = 0; k < PER; ++k) acc[k] = 0.f;
+  float L = 0.f;
+#pragma unroll 4
   for (int p = 0; p < mi.n_part; ++p) {
     const size_t b = (size_t)(mi.part0 + p) * G + g;
-    const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + b * 2);
-    const float wgt = exp2f(ml.x - M);
-    L += wgt * ml.y;
-#pragma unroll
-    for (int k = 0; k < DH / 64; ++k) acc[k] += wgt * a.part_o[b * DH + lane + 64 * k];
+    const float2 v = ml[b];
+    const float w = exp2f(v.x - M);
+    L += w * v.y;
+    const float* o = a.part_o + b * DH + lane * PER;
+    if (PER == 2) {
+      const float2 x = *reinterpret_cast<const float2*>(o);
+      acc[0] += w * x.x;
+      acc[PER - 1] += w * x.y;
+    } else {
+      acc[0] += w * o[0];
+    }
   }
   const float inv = 1.f / L;
-  uint16_t* out = a.out + (size_t)a.q_row[mi.entry] * a.out_stride + (mi.kvh * G + g) * DH;
-#pragma unroll
-  for (int k = 0; k < DH / 64; ++k) out[lane + 64 * k] = f2bf(acc[k] * inv);
+  uint16_t* out = a.out + (size_t)a.q_row[mi.entry] * a.out_stride + (mi.kvh * G + g) * DH + lane * PER;
+  if (PER == 2) *reinterpret_cast<uint32_t*>(out) = pack_bf2(acc[0] * inv, acc[PER - 1] * inv);
+  else out[0] = f2bf(acc[0] * inv);
 }
 
 template <int DH>
@@ -227,8 +250,8 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillAttnArgs a) {
   const int lim = pos0 + (ok ? qloc : wq0);
   const int t_end = pos0 + wq_end;              // last query position + 1
   AttnState<DH> S;
-  attn_range<DH>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)it.entry * a.bt_stride, a.Hkv, it.kvh, 0, t_end, lim,
-                 a.scale_log2, lane);
+  attn_range<DH, true>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)it.entry * a.bt_stride, a.n_blocks, it.kvh, 0, t_end,
+                       lim, a.scale_log2, lane);
   if (!ok) return;
   const float inv = 1.f / S.l;
   const int rq = lane >> 4;

@@ -6,11 +6,16 @@
 
 namespace hxf {
 
-// Physical KV layout (per layer; K pool then V pool):
-//   K: [n_blocks][Hkv][16 tokens][dh]   (a token's head vector contiguous)
-//   V: [n_blocks][Hkv][dh][16 tokens]   (a dimension's 16 tokens contiguous)
-// so one (page, kv-head) is one contiguous 16*dh*2-byte tile in each pool.
+// Physical KV layout (per layer; K pool then V pool), kv-head major:
+//   K: [Hkv][n_blocks][dh/8][16 tokens][8]  (8-dimension chunks of the 16 tokens
+//      side by side: the order in which a wavefront feeds them to the MFMA)
+//   V: [Hkv][n_blocks][dh][16 tokens]       (a dimension's 16 tokens contiguous)
+// so one (page, kv-head) is one contiguous 16*dh*2-byte tile in each pool, and
+// the pages of one kv-head of a sequence allocated together are contiguous.
 constexpr int kPage = 16;
+__host__ __device__ inline size_t kv_tile(int kvh, int64_t n_blocks, int blk, int dh) {
+  return ((size_t)kvh * n_blocks + blk) * kPage * dh;
+}
 
 // ------------------------------------------------------------------ GEMM
 enum { EPI_BF16 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3 };
@@ -47,11 +52,11 @@ hipError_t embed_rmsnorm_launch(const int32_t* ids, const uint16_t* E, const uin
 // qkv bf16 [T, (Hq+2Hkv)*dh]: rotates q (in place) and k at pos[t] with the
 // table cs[pos][i] = (cos, sin) of pos * base^(-2i/dh); writes k and v to slot[t].
 hipError_t rope_kv_launch(uint16_t* qkv, const int32_t* pos, const int32_t* slot, const float2* cs,
-                          uint16_t* k_pool, uint16_t* v_pool, int T, int Hq, int Hkv, int dh,
+                          uint16_t* k_pool, uint16_t* v_pool, int64_t n_blocks, int T, int Hq, int Hkv, int dh,
                           hipStream_t st);
 // Write k, v bf16 [T, Hkv, dh] to slot[t] (no rotation).
 hipError_t kv_scatter_launch(const uint16_t* k, const uint16_t* v, const int32_t* slot, uint16_t* k_pool,
-                             uint16_t* v_pool, int T, int Hkv, int dh, hipStream_t st);
+                             uint16_t* v_pool, int64_t n_blocks, int T, int Hkv, int dh, hipStream_t st);
 
 // ------------------------------------------------------------------ attention
 // One decode work item: tokens [t0, t1) of batch entry `entry`, kv-head `kvh`;
@@ -69,6 +74,7 @@ struct DecodeAttnArgs {
   int q_stride;
   const uint16_t* k_pool;
   const uint16_t* v_pool;
+  int64_t n_blocks;
   const int32_t* bt;       // [entries][bt_stride]
   int bt_stride;
   const DecodeItem* items;
@@ -97,6 +103,7 @@ struct PrefillAttnArgs {
   const int32_t* pos0;     // [entries] position of the entry's first query
   const uint16_t* k_pool;
   const uint16_t* v_pool;
+  int64_t n_blocks;
   const int32_t* bt;       // [entries][bt_stride]
   int bt_stride;
   const PrefillItem* items;

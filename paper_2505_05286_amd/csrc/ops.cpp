@@ -96,17 +96,18 @@ int hxf_op_rope_table(void* dst, int32_t max_pos, int32_t dh, float base, void* 
 }
 
 int hxf_op_rope_kv_write(void* qkv, const int32_t* pos, const int32_t* slot, const void* table, void* k_pool,
-                         void* v_pool, int32_t T, int32_t Hq, int32_t Hkv, int32_t dh, void* stream) {
-  if (!qkv || !pos || !slot || !table || !k_pool || !v_pool || T < 0 || !shapes_ok(Hq, Hkv, dh)) return HXF_EINVAL;
+                         void* v_pool, int64_t n_blocks, int32_t T, int32_t Hq, int32_t Hkv, int32_t dh, void* stream) {
+  if (!qkv || !pos || !slot || !table || !k_pool || !v_pool || n_blocks <= 0 || T < 0 || !shapes_ok(Hq, Hkv, dh))
+    return HXF_EINVAL;
   return dev_rc(rope_kv_launch((uint16_t*)qkv, pos, slot, (const float2*)table, (uint16_t*)k_pool,
-                               (uint16_t*)v_pool, T, Hq, Hkv, dh, (hipStream_t)stream));
+                               (uint16_t*)v_pool, n_blocks, T, Hq, Hkv, dh, (hipStream_t)stream));
 }
 
-int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k_pool, void* v_pool, int32_t T,
-                      int32_t Hkv, int32_t dh, void* stream) {
-  if (!k || !v || !slot || !k_pool || !v_pool || T < 0 || Hkv <= 0 || dh <= 0) return HXF_EINVAL;
+int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k_pool, void* v_pool, int64_t n_blocks,
+                      int32_t T, int32_t Hkv, int32_t dh, void* stream) {
+  if (!k || !v || !slot || !k_pool || !v_pool || n_blocks <= 0 || T < 0 || Hkv <= 0 || dh <= 0) return HXF_EINVAL;
   return dev_rc(kv_scatter_launch((const uint16_t*)k, (const uint16_t*)v, slot, (uint16_t*)k_pool,
-                                  (uint16_t*)v_pool, T, Hkv, dh, (hipStream_t)stream));
+                                  (uint16_t*)v_pool, n_blocks, T, Hkv, dh, (hipStream_t)stream));
 }
 
 int64_t hxf_op_decode_attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t dh, const int32_t* ctx) {
@@ -114,10 +115,11 @@ int64_t hxf_op_decode_attention_workspace_bytes(int32_t B, int32_t Hq, int32_t H
   return decode_layout(B, Hq, Hkv, dh, ctx).total;
 }
 
-int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_pool, const int32_t* bt,
+int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_pool, int64_t n_blocks, const int32_t* bt,
                             int32_t bt_stride, const int32_t* ctx, void* out, int32_t B, int32_t Hq, int32_t Hkv,
                             int32_t dh, void* workspace, int64_t ws_bytes, void* stream) {
-  if (!q || !k_pool || !v_pool || !bt || !ctx || !out || B < 0 || !shapes_ok(Hq, Hkv, dh)) return HXF_EINVAL;
+  if (!q || !k_pool || !v_pool || n_blocks <= 0 || !bt || !ctx || !out || B < 0 || !shapes_ok(Hq, Hkv, dh))
+    return HXF_EINVAL;
   if (B == 0) return HXF_OK;
   for (int b = 0; b < B; ++b)
     if (ctx[b] <= 0 || (ctx[b] + kPage - 1) / kPage > bt_stride) return HXF_EINVAL;
@@ -149,6 +151,7 @@ int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_poo
   a.q_stride = Hq * dh;
   a.k_pool = (const uint16_t*)k_pool;
   a.v_pool = (const uint16_t*)v_pool;
+  a.n_blocks = n_blocks;
   a.bt = bt;
   a.bt_stride = bt_stride;
   a.items = reinterpret_cast<const DecodeItem*>(ws + L.off_items);
@@ -175,11 +178,12 @@ int64_t hxf_op_prefill_attention_workspace_bytes(int32_t S, int32_t Hq, int32_t 
   return al(items * (int64_t)sizeof(PrefillItem)) + al((int64_t)S * 8);
 }
 
-int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_pool, const int32_t* bt,
+int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_pool, int64_t n_blocks, const int32_t* bt,
                              int32_t bt_stride, const int32_t* row0, const int32_t* pos0, const int32_t* n_host,
                              void* out, int32_t S, int32_t Hq, int32_t Hkv, int32_t dh, void* workspace,
                              int64_t ws_bytes, void* stream) {
-  if (!q || !k_pool || !v_pool || !bt || !row0 || !pos0 || !n_host || !out || S < 0 || !shapes_ok(Hq, Hkv, dh))
+  if (!q || !k_pool || !v_pool || n_blocks <= 0 || !bt || !row0 || !pos0 || !n_host || !out || S < 0 ||
+      !shapes_ok(Hq, Hkv, dh))
     return HXF_EINVAL;
   if (S == 0) return HXF_OK;
   for (int s = 0; s < S; ++s)
@@ -207,6 +211,7 @@ int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_po
   a.pos0 = reinterpret_cast<const int32_t*>(ws + off_rp + S * 4);
   a.k_pool = (const uint16_t*)k_pool;
   a.v_pool = (const uint16_t*)v_pool;
+  a.n_blocks = n_blocks;
   a.bt = bt;
   a.bt_stride = bt_stride;
   a.items = reinterpret_cast<const PrefillItem*>(ws);

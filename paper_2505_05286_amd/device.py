@@ -59,11 +59,11 @@ class Engine:
                        self.kv_pool.data_ptr(), kvb, self.workspace.data_ptr(), wsb, self.stream.cuda_stream)
 
     def layer_kv(self, layer):
-        """(K pool, V pool) views of one layer: [n_blocks, Hkv, 16, dh] and [n_blocks, Hkv, dh, 16] (int16 bits)."""
+        """(K pool, V pool) views of one layer: [Hkv, n_blocks, dh/8, 16, 8] and [Hkv, n_blocks, dh, 16] (int16 bits)."""
         sh = self.model.shape
         nb = self.scfg.n_blocks
         per = nb * sh.n_kv_heads * 16 * sh.head_dim
         flat = self.kv_pool.view(torch.int16)
-        k = flat[(2 * layer) * per:(2 * layer + 1) * per].view(nb, sh.n_kv_heads, 16, sh.head_dim)
-        v = flat[(2 * layer + 1) * per:(2 * layer + 2) * per].view(nb, sh.n_kv_heads, sh.head_dim, 16)
+        k = flat[(2 * layer) * per:(2 * layer + 1) * per].view(sh.n_kv_heads, nb, sh.head_dim // 8, 16, 8)
+        v = flat[(2 * layer + 1) * per:(2 * layer + 2) * per].view(sh.n_kv_heads, nb, sh.head_dim, 16)
         return k, v

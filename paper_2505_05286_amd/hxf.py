@@ -126,17 +126,17 @@ _SIGS = {
                                        C.c_int32, C.c_float, C.c_void_p]),
     "hxf_op_rope_table": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_float, C.c_void_p]),
     "hxf_op_rope_kv_write": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
-                                       C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_void_p]),
-    "hxf_op_kv_scatter": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
-                                    C.c_int32, C.c_int32, C.c_void_p]),
+                                       C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_void_p]),
+    "hxf_op_kv_scatter": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
+                                    C.c_int32, C.c_int32, C.c_int32, C.c_void_p]),
     "hxf_op_decode_attention_workspace_bytes": (C.c_int64, [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                                             C.POINTER(C.c_int32)]),
-    "hxf_op_decode_attention": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+    "hxf_op_decode_attention": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p, C.c_int32,
                                           C.POINTER(C.c_int32), C.c_void_p, C.c_int32, C.c_int32, C.c_int32,
                                           C.c_int32, C.c_void_p, C.c_int64, C.c_void_p]),
     "hxf_op_prefill_attention_workspace_bytes": (C.c_int64, [C.c_int32, C.c_int32, C.c_int32,
                                                              C.POINTER(C.c_int32)]),
-    "hxf_op_prefill_attention": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+    "hxf_op_prefill_attention": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p, C.c_int32,
                                            C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32),
                                            C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
                                            C.c_int64, C.c_void_p]),
@@ -340,13 +340,14 @@ def op_rope_table(dst, max_pos, dh, base, stream=0):
     _op(lib().hxf_op_rope_table(dst, max_pos, dh, base, stream or None), "hxf_op_rope_table")
 
 
-def op_rope_kv_write(qkv, pos, slot, table, k_pool, v_pool, T, Hq, Hkv, dh, stream=0):
-    _op(lib().hxf_op_rope_kv_write(qkv, pos, slot, table, k_pool, v_pool, T, Hq, Hkv, dh, stream or None),
+def op_rope_kv_write(qkv, pos, slot, table, k_pool, v_pool, n_blocks, T, Hq, Hkv, dh, stream=0):
+    _op(lib().hxf_op_rope_kv_write(qkv, pos, slot, table, k_pool, v_pool, n_blocks, T, Hq, Hkv, dh, stream or None),
         "hxf_op_rope_kv_write")
 
 
-def op_kv_scatter(k, v, slot, k_pool, v_pool, T, Hkv, dh, stream=0):
-    _op(lib().hxf_op_kv_scatter(k, v, slot, k_pool, v_pool, T, Hkv, dh, stream or None), "hxf_op_kv_scatter")
+def op_kv_scatter(k, v, slot, k_pool, v_pool, n_blocks, T, Hkv, dh, stream=0):
+    _op(lib().hxf_op_kv_scatter(k, v, slot, k_pool, v_pool, n_blocks, T, Hkv, dh, stream or None),
+        "hxf_op_kv_scatter")
 
 
 def op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, ctx):
@@ -354,10 +355,10 @@ def op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, ctx):
     return lib().hxf_op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, cp)
 
 
-def op_decode_attention(q, k_pool, v_pool, bt, bt_stride, ctx, out, B, Hq, Hkv, dh, ws, ws_bytes, stream=0):
+def op_decode_attention(q, k_pool, v_pool, n_blocks, bt, bt_stride, ctx, out, B, Hq, Hkv, dh, ws, ws_bytes, stream=0):
     c, cp = _i32(ctx)
-    _op(lib().hxf_op_decode_attention(q, k_pool, v_pool, bt, bt_stride, cp, out, B, Hq, Hkv, dh, ws, ws_bytes,
-                                      stream or None), "hxf_op_decode_attention")
+    _op(lib().hxf_op_decode_attention(q, k_pool, v_pool, n_blocks, bt, bt_stride, cp, out, B, Hq, Hkv, dh, ws,
+                                      ws_bytes, stream or None), "hxf_op_decode_attention")
 
 
 def op_prefill_attention_workspace_bytes(S, Hq, Hkv, n):
@@ -365,13 +366,13 @@ def op_prefill_attention_workspace_bytes(S, Hq, Hkv, n):
     return lib().hxf_op_prefill_attention_workspace_bytes(S, Hq, Hkv, ap)
 
 
-def op_prefill_attention(q, k_pool, v_pool, bt, bt_stride, row0, pos0, n, out, S, Hq, Hkv, dh, ws, ws_bytes,
-                         stream=0):
+def op_prefill_attention(q, k_pool, v_pool, n_blocks, bt, bt_stride, row0, pos0, n, out, S, Hq, Hkv, dh, ws,
+                         ws_bytes, stream=0):
     r, rp = _i32(row0)
     p, pp = _i32(pos0)
     m, mp = _i32(n)
-    _op(lib().hxf_op_prefill_attention(q, k_pool, v_pool, bt, bt_stride, rp, pp, mp, out, S, Hq, Hkv, dh, ws,
-                                       ws_bytes, stream or None), "hxf_op_prefill_attention")
+    _op(lib().hxf_op_prefill_attention(q, k_pool, v_pool, n_blocks, bt, bt_stride, rp, pp, mp, out, S, Hq, Hkv, dh,
+                                       ws, ws_bytes, stream or None), "hxf_op_prefill_attention")
 
 
 def op_argmax(logits, out, R, V, stream=0):

@@ -59,4 +59,4 @@ def test_ops_reject_bad_arguments_without_launching():
         hxf.op_gemm(1, 7, 1, 0, 1, 8, 8, 8, 7, hxf.EPI_BF16)    # K % 8 != 0
     assert e.value.code == hxf.EINVAL
     with pytest.raises(hxf.HxfError):
-        hxf.op_decode_attention(1, 1, 1, 1, 1, [0], 1, 1, 4, 3, 128, 1, 1)   # Hq % Hkv
+        hxf.op_decode_attention(1, 1, 1, 8, 1, 1, [0], 1, 1, 4, 3, 128, 1, 1)   # Hq % Hkv

@@ -106,8 +106,8 @@ def _make_pools(nb, hkv, dh):
 
 def _logical_pool(kp, vp, nb, hkv, dh):
     """Read the physical pools back into the oracle's logical [nb, 16, Hkv, dh] layout."""
-    k = host_f64(kp).reshape(nb, hkv, 16, dh).transpose(0, 2, 1, 3)
-    v = host_f64(vp).reshape(nb, hkv, dh, 16).transpose(0, 3, 1, 2)
+    k = host_f64(kp).reshape(hkv, nb, dh // 8, 16, 8).transpose(1, 3, 0, 2, 4).reshape(nb, 16, hkv, dh)
+    v = host_f64(vp).reshape(hkv, nb, dh, 16).transpose(1, 3, 0, 2)
     return k, v
 
 
@@ -125,7 +125,7 @@ def test_rope_kv_write(hq, hkv, dh):
     kp, vp = _make_pools(nb, hkv, dh)
     pos_d, slots_d = i32(pos), i32(slots)
     hxf.op_rope_kv_write(qkv.data_ptr(), pos_d.data_ptr(), slots_d.data_ptr(), table.data_ptr(), kp.data_ptr(),
-                         vp.data_ptr(), T, hq, hkv, dh)
+                         vp.data_ptr(), nb, T, hq, hkv, dh)
     t.cuda.synchronize()
     q = qkvf[:, : hq * dh].reshape(T, hq, dh)
     k = qkvf[:, hq * dh:(hq + hkv) * dh].reshape(T, hkv, dh)
@@ -164,7 +164,8 @@ def _fill_paged(rng, ctxs, hkv, dh, extra_blocks=3):
     vb, vf = rand_bf16(rng, (tot, hkv, dh))
     slots = np.concatenate([[P.slot(b, p) for p in range(c)] for b, c in zip(bts, ctxs)]).astype(np.int32)
     k_d, v_d, slots_d = dev_bits(kb), dev_bits(vb), i32(slots)
-    hxf.op_kv_scatter(k_d.data_ptr(), v_d.data_ptr(), slots_d.data_ptr(), kp.data_ptr(), vp.data_ptr(), tot, hkv, dh)
+    hxf.op_kv_scatter(k_d.data_ptr(), v_d.data_ptr(), slots_d.data_ptr(), kp.data_ptr(), vp.data_ptr(), nb, tot, hkv,
+                      dh)
     t.cuda.synchronize()
     Kl = np.zeros((nb, 16, hkv, dh))
     Vl = np.zeros((nb, 16, hkv, dh))
@@ -173,7 +174,7 @@ def _fill_paged(rng, ctxs, hkv, dh, extra_blocks=3):
         P.scatter(Kl, b, 0, kf[o:o + c])
         P.scatter(Vl, b, 0, vf[o:o + c])
         o += c
-    return kp, vp, bt, bts, Kl, Vl
+    return kp, vp, nb, bt, bts, Kl, Vl
 
 
 def _decode_case(ctxs, hq, hkv, dh, seed, sample=None):
@@ -181,13 +182,13 @@ def _decode_case(ctxs, hq, hkv, dh, seed, sample=None):
     rng = np.random.default_rng(seed)
     B = len(ctxs)
     log(f"decode attention B={B} hq={hq} hkv={hkv} dh={dh} sum_ctx={sum(ctxs)}")
-    kp, vp, bt, bts, Kl, Vl = _fill_paged(rng, ctxs, hkv, dh)
+    kp, vp, nb, bt, bts, Kl, Vl = _fill_paged(rng, ctxs, hkv, dh)
     qb, qf = rand_bf16(rng, (B, hq, dh))
     out = empty_i16(B * hq * dh)
     wsn = hxf.op_decode_attention_workspace_bytes(B, hq, hkv, dh, ctxs)
     ws = t.empty(wsn, dtype=t.uint8, device="cuda:0")
     q_d, bt_d = dev_bits(qb), i32(bt)
-    hxf.op_decode_attention(q_d.data_ptr(), kp.data_ptr(), vp.data_ptr(), bt_d.data_ptr(), bt.shape[1], ctxs,
+    hxf.op_decode_attention(q_d.data_ptr(), kp.data_ptr(), vp.data_ptr(), nb, bt_d.data_ptr(), bt.shape[1], ctxs,
                             out.data_ptr(), B, hq, hkv, dh, ws.data_ptr(), wsn)
     t.cuda.synchronize()
     got = host_f64(out).reshape(B, hq, dh)
@@ -220,7 +221,7 @@ def _prefill_case(chunks, hq, hkv, dh, seed):
     rng = np.random.default_rng(seed)
     ctxs = [p0 + n for p0, n in chunks]
     log(f"prefill attention chunks={chunks} hq={hq} hkv={hkv} dh={dh}")
-    kp, vp, bt, bts, Kl, Vl = _fill_paged(rng, ctxs, hkv, dh)
+    kp, vp, nb, bt, bts, Kl, Vl = _fill_paged(rng, ctxs, hkv, dh)
     ns = [n for _, n in chunks]
     row0 = np.concatenate([[0], np.cumsum(ns)[:-1]]).astype(np.int32)
     T = sum(ns)
@@ -230,7 +231,7 @@ def _prefill_case(chunks, hq, hkv, dh, seed):
     wsn = hxf.op_prefill_attention_workspace_bytes(S, hq, hkv, ns)
     ws = t.empty(max(wsn, 256), dtype=t.uint8, device="cuda:0")
     q_d, bt_d = dev_bits(qb), i32(bt)
-    hxf.op_prefill_attention(q_d.data_ptr(), kp.data_ptr(), vp.data_ptr(), bt_d.data_ptr(), bt.shape[1], row0,
+    hxf.op_prefill_attention(q_d.data_ptr(), kp.data_ptr(), vp.data_ptr(), nb, bt_d.data_ptr(), bt.shape[1], row0,
                              [p for p, _ in chunks], ns, out.data_ptr(), S, hq, hkv, dh, ws.data_ptr(), ws.numel())
     t.cuda.synchronize()
     got = host_f64(out).reshape(T, hq, dh)
