@@ -145,12 +145,16 @@ __device__ __forceinline__ void attn_range(AttnState<DH>& S, const bf16x8* qf, c
   S.m = kNegInf;
   S.l = 0.f;
   const int p0 = t_begin / kPage, p_end = (t_end + kPage - 1) / kPage;
-  PairRegs<DH> cur, nxt;
-  load_pair<DH>(cur, k_pool, v_pool, bt, nb, kvh, p0, t_end, lane);
-  for (int p = p0; p < p_end; p += 2) {
-    if (p + 2 < p_end) load_pair<DH>(nxt, k_pool, v_pool, bt, nb, kvh, p + 2, t_end, lane);
-    compute_pair<DH, CAUSAL>(S, cur, qf, p, t_end, lim, scale_log2, lane);
-    cur = nxt;
+  // two register buffers used in turn: the loads of the next page pair are in
+  // flight while the current one is multiplied
+  PairRegs<DH> ra, rb;
+  load_pair<DH>(ra, k_pool, v_pool, bt, nb, kvh, p0, t_end, lane);
+  for (int p = p0; p < p_end; p += 4) {
+    if (p + 2 < p_end) load_pair<DH>(rb, k_pool, v_pool, bt, nb, kvh, p + 2, t_end, lane);
+    compute_pair<DH, CAUSAL>(S, ra, qf, p, t_end, lim, scale_log2, lane);
+    if (p + 2 >= p_end) break;
+    if (p + 4 < p_end) load_pair<DH>(ra, k_pool, v_pool, bt, nb, kvh, p + 4, t_end, lane);
+    compute_pair<DH, CAUSAL>(S, rb, qf, p + 2, t_end, lim, scale_log2, lane);
   }
   S.l += __shfl_xor(S.l, 16, kWave);
   S.l += __shfl_xor(S.l, 32, kWave);
@@ -165,9 +169,9 @@ __device__ __forceinline__ void load_q(bf16x8* qf, const uint16_t* qrow, bool ok
 }
 
 template <int DH>
-__global__ __launch_bounds__(256) void decode_attn_kernel(DecodeAttnArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+__global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
+  const int lane = threadIdx.x;
+  const int w = blockIdx.x;
   if (w >= a.n_items) return;
   const DecodeItem it = a.items[w];
   const int G = a.Hq / a.Hkv;
@@ -270,8 +274,8 @@ int prefill_queries_per_item(int group) { return 4 * (16 / group); }
 
 hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st) {
   if (a.n_items <= 0) return hipSuccess;
-  if (a.dh == 128) hipLaunchKernelGGL(decode_attn_kernel<128>, dim3((a.n_items + 3) / 4), dim3(256), 0, st, a);
-  else if (a.dh == 64) hipLaunchKernelGGL(decode_attn_kernel<64>, dim3((a.n_items + 3) / 4), dim3(256), 0, st, a);
+  if (a.dh == 128) hipLaunchKernelGGL(decode_attn_kernel<128>, dim3(a.n_items), dim3(64), 0, st, a);
+  else if (a.dh == 64) hipLaunchKernelGGL(decode_attn_kernel<64>, dim3(a.n_items), dim3(64), 0, st, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
