@@ -4,8 +4,8 @@
 //
 // Tiling: 256 threads = 4 wavefronts in a 2x2 arrangement; each wave owns a
 // (BM/2)x(BN/2) sub-tile made of 16x16 v_mfma_f32_16x16x32_bf16 tiles.  K is
-// staged through LDS 64 at a time; the next K tile is fetched into registers
-// while the current one is multiplied.  Workgroups are renumbered so that
+// staged through LDS (64 or 128 at a time); the next NS-1 K tiles are fetched
+// into registers while the current one is multiplied.  Workgroups are renumbered so that
 // consecutive output tiles (which share a weight slice) land on the same XCD
 // and its L2.
 #include "common.hpp"
@@ -15,8 +15,7 @@ namespace hxf {
 
 namespace {
 
-constexpr int BK = 64;
-constexpr int LDS_ROW = BK + 8;   // bf16 elements per LDS row (16-byte pad)
+constexpr int BK_MAX = 128;
 
 // Logical column c of a SwiGLU GEMM: groups of 32 = 16 gate rows then 16 up rows.
 __device__ __forceinline__ const bf16_t* b_row(const GemmArgs& a, int c, bool swiglu) {
@@ -25,14 +24,21 @@ __device__ __forceinline__ const bf16_t* b_row(const GemmArgs& a, int c, bool sw
   return ((w < 16) ? a.B : a.B2) + (size_t)(g * 16 + (w & 15)) * a.K;
 }
 
+// 16-byte load from a 16-byte aligned address (one global_load_dwordx4).
+__device__ __forceinline__ uint4 load16(const bf16_t* p) {
+  const u32x4_t v = *reinterpret_cast<const u32x4_t*>(__builtin_assume_aligned(p, 16));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __device__ __forceinline__ int xcd_remap(int i, int nb) {
   const int xcd = i & 7, local = i >> 3;
   const int per = nb >> 3, rem = nb & 7;
   return (xcd < rem) ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
-template <int BM, int BN, int EPI, bool SPLIT>
+template <int BM, int BN, int BK, int NS, int EPI, bool SPLIT>
 __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
+  constexpr int LDS_ROW = BK + 8;                   // bf16 elements per LDS row (16-byte pad)
   constexpr int TM = BM / 32, TN = BN / 32;         // MFMA tiles per wave
   constexpr int A_CH = BM * (BK / 8) / 256;         // 16-byte chunks per thread
   constexpr int B_CH = BN * (BK / 8) / 256;
@@ -51,32 +57,47 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int wm = wid >> 1, wn = wid & 1;
 
-  // global load bookkeeping: chunk j of this thread = row (tid + j*256) / 8, col16 (tid % 8)
-  const int c16 = tid & 7;
+  // global load bookkeeping: chunk j of this thread = row (tid + j*256) / CPR, col16 (tid % CPR)
+  constexpr int CPR = BK / 8;                       // 16-byte chunks per row of a K tile
+  const int c16 = tid % CPR;
   const bf16_t* a_ptr[A_CH];
   const bf16_t* b_ptr[B_CH];
   bool a_ok[A_CH], b_ok[B_CH];
 #pragma unroll
   for (int j = 0; j < A_CH; ++j) {
-    const int r = (tid + j * 256) >> 3;
+    const int r = (tid + j * 256) / CPR;
     a_ok[j] = (m0 + r) < a.M;
     a_ptr[j] = a.A + (size_t)(a_ok[j] ? m0 + r : 0) * a.lda + c16 * 8;
   }
 #pragma unroll
   for (int j = 0; j < B_CH; ++j) {
-    const int r = (tid + j * 256) >> 3;
+    const int r = (tid + j * 256) / CPR;
     b_ok[j] = (n0 + r) < a.N;
     b_ptr[j] = b_row(a, b_ok[j] ? n0 + r : 0, SW) + c16 * 8;
   }
-  uint4 ra[A_CH], rb[B_CH];
-  auto fetch = [&](int k0) {
+  // NS register stages: the K tiles it+1 .. it+NS-1 are in flight while tile it
+  // is multiplied (one stage is the tile being stored to LDS).
+  uint4 ra[NS][A_CH], rb[NS][B_CH];
+  auto fetch = [&](uint4 (&xa)[A_CH], uint4 (&xb)[B_CH], int k0) {
     const bool kin = (k0 + c16 * 8) < ke;
 #pragma unroll
     for (int j = 0; j < A_CH; ++j)
-      ra[j] = (a_ok[j] && kin) ? *reinterpret_cast<const uint4*>(a_ptr[j] + k0) : make_uint4(0, 0, 0, 0);
+      xa[j] = (a_ok[j] && kin) ? *reinterpret_cast<const uint4*>(a_ptr[j] + k0) : make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int j = 0; j < B_CH; ++j)
-      rb[j] = (b_ok[j] && kin) ? *reinterpret_cast<const uint4*>(b_ptr[j] + k0) : make_uint4(0, 0, 0, 0);
+      xb[j] = (b_ok[j] && kin) ? *reinterpret_cast<const uint4*>(b_ptr[j] + k0) : make_uint4(0, 0, 0, 0);
+  };
+  auto stage_to_lds = [&](const uint4 (&xa)[A_CH], const uint4 (&xb)[B_CH]) {
+#pragma unroll
+    for (int j = 0; j < A_CH; ++j) {
+      const int r = (tid + j * 256) / CPR;
+      *reinterpret_cast<uint4*>(&As[r * LDS_ROW + c16 * 8]) = xa[j];
+    }
+#pragma unroll
+    for (int j = 0; j < B_CH; ++j) {
+      const int r = (tid + j * 256) / CPR;
+      *reinterpret_cast<uint4*>(&Bs[r * LDS_ROW + c16 * 8]) = xb[j];
+    }
   };
 
   f32x4 acc[TM][TN];
@@ -85,21 +106,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  fetch(kb);
-  for (int k0 = kb; k0 < ke; k0 += BK) {
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < A_CH; ++j) {
-      const int r = (tid + j * 256) >> 3;
-      *reinterpret_cast<uint4*>(&As[r * LDS_ROW + c16 * 8]) = ra[j];
-    }
-#pragma unroll
-    for (int j = 0; j < B_CH; ++j) {
-      const int r = (tid + j * 256) >> 3;
-      *reinterpret_cast<uint4*>(&Bs[r * LDS_ROW + c16 * 8]) = rb[j];
-    }
-    __syncthreads();
-    if (k0 + BK < ke) fetch(k0 + BK);
+  auto compute = [&]() {
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ++ks) {
       const int kc = ks * 32 + (lane >> 4) * 8;
@@ -118,6 +125,23 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x32(fa[i], fb[j], acc[i][j]);
+    }
+  };
+
+#pragma unroll
+  for (int st = 0; st < NS; ++st)
+    if (kb + st * BK < ke) fetch(ra[st], rb[st], kb + st * BK);
+  for (int k0 = kb; k0 < ke; k0 += NS * BK) {
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+      const int kt = k0 + st * BK;
+      if (kt < ke) {
+        __syncthreads();
+        stage_to_lds(ra[st], rb[st]);
+        __syncthreads();
+        if (kt + NS * BK < ke) fetch(ra[st], rb[st], kt + NS * BK);
+        compute();
+      }
     }
   }
 
@@ -177,6 +201,155 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
     }
 }
 
+// Large-tile kernel for prefill-sized M, on the 32x32x16 bf16 MFMA (the
+// 16x16x32 shape issues at half the rate on gfx950).  A 256 x BN macro tile
+// per workgroup of 4 wavefronts (2 x 2); each wavefront owns a 128 x BN/2
+// sub-tile of 32x32 MFMA tiles whose accumulators live in the accumulation
+// registers.  K advances 32 at a time through two LDS buffers: while step k is
+// multiplied out of one buffer, step k+1 is fetched into registers and then
+// written to the other buffer (one barrier per step).  Rows of 40 bf16 (80
+// bytes) keep the 16-byte fragment reads of consecutive rows on distinct
+// banks.  SwiGLU uses groups of 64 logical columns (32 gate rows, then the 32
+// matching up rows) so gate and up land in the same lane.
+constexpr int BIG_BK = 64;
+
+template <int BN, int EPI>
+__global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs a) {
+  constexpr int BM = 256, BK = BIG_BK, ROW = BK + 8;
+  constexpr int TM = 4, TN = BN / 64;              // 32x32 tiles per wave
+  constexpr int A_CH = BM * (BK / 8) / 256;        // 16-byte chunks per thread per K step
+  constexpr int B_CH = BN * (BK / 8) / 256;
+  constexpr int STAGE = (BM + BN) * ROW;           // bf16 elements per LDS buffer
+  constexpr bool SW = (EPI == EPI_SWIGLU);
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+
+  const int tiles_m = (a.M + BM - 1) / BM;
+  const int tiles_n = (a.N + BN - 1) / BN;
+  const int L = xcd_remap(blockIdx.x, tiles_m * tiles_n);
+  const int tn = L / tiles_m, tm = L % tiles_m;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid >> 1, wn = wid & 1;
+  constexpr int CPR = BK / 8, RPP = 256 / CPR;     // chunks per row, rows per fetch pass
+  const int c4 = tid % CPR, r4 = tid / CPR;
+
+  // a thread's chunks: rows r4 + RPP*j of the A and B tiles, k offset c4*8
+  const bf16_t* a_base = a.A + c4 * 8;
+  uint4 ra[A_CH], rb[B_CH];
+  auto fetch = [&](int k0) {
+    const bool kin = (k0 + c4 * 8) < a.K;
+#pragma unroll
+    for (int j = 0; j < A_CH; ++j) {
+      const int r = min(m0 + r4 + RPP * j, a.M - 1);         // rows past M repeat row M-1 (outputs dropped)
+      ra[j] = kin ? load16(a_base + (size_t)r * a.lda + k0) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < B_CH; ++j) {
+      const int c = min(n0 + r4 + RPP * j, a.N - 1);          // logical column; past N repeats N-1 (dropped)
+      const bf16_t* p;
+      if (SW) {   // groups of 64 logical columns: 32 gate rows, then the 32 matching up rows
+        const int w = c & 63;
+        p = ((w < 32) ? a.B : a.B2) + (size_t)((c >> 6) * 32 + (w & 31)) * a.K + c4 * 8;
+      } else {
+        p = a.B + (size_t)c * a.K + c4 * 8;
+      }
+      rb[j] = kin ? load16(p + k0) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store = [&](int buf) {
+    bf16_t* As = smem + buf * STAGE;
+    bf16_t* Bs = As + BM * ROW;
+#pragma unroll
+    for (int j = 0; j < A_CH; ++j) *reinterpret_cast<uint4*>(&As[(r4 + RPP * j) * ROW + c4 * 8]) = ra[j];
+#pragma unroll
+    for (int j = 0; j < B_CH; ++j) *reinterpret_cast<uint4*>(&Bs[(r4 + RPP * j) * ROW + c4 * 8]) = rb[j];
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int nk = (a.K + BK - 1) / BK;
+  const int l32 = lane & 31, kh = (lane >> 5) * 8;
+  fetch(0);
+  store(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) fetch((kt + 1) * BK);
+    const bf16_t* As = smem + cur * STAGE;
+    const bf16_t* Bs = As + BM * ROW;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int kc = ks * 16 + kh;
+      bf16x8 fb[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        fb[j] = as_bf16x8(*reinterpret_cast<const uint4*>(&Bs[(wn * (BN / 2) + j * 32 + l32) * ROW + kc]));
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const bf16x8 fa = as_bf16x8(*reinterpret_cast<const uint4*>(&As[(wm * 128 + i * 32 + l32) * ROW + kc]));
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(fa, fb[j], acc[i][j]);
+      }
+    }
+    if (kt + 1 < nk) store(cur ^ 1);
+    __syncthreads();
+  }
+
+  // lane holds column l32 and rows 8*(r/4) + 4*(lane/32) + r%4 of each 32x32 tile
+  const int rq = (lane >> 5) * 4;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m0 + wm * 128 + i * 32 + (r >> 2) * 8 + rq + (r & 3);
+      if (row >= a.M) continue;
+      if (SW) {
+#pragma unroll
+        for (int j = 0; j < TN; j += 2) {
+          const int lc = n0 + wn * (BN / 2) + j * 32;   // first (gate) logical column of the 64-group
+          if (lc >= a.N) continue;
+          const float g = acc[i][j][r], u = acc[i][j + 1][r];
+          reinterpret_cast<bf16_t*>(a.C)[(size_t)row * a.ldc + (lc >> 6) * 32 + l32] =
+              f2bf(g / (1.f + __expf(-g)) * u);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int col = n0 + wn * (BN / 2) + j * 32 + l32;
+          if (col >= a.N) continue;
+          const size_t o = (size_t)row * a.ldc + col;
+          if (EPI == EPI_BF16) reinterpret_cast<bf16_t*>(a.C)[o] = f2bf(acc[i][j][r]);
+          else if (EPI == EPI_RESID) reinterpret_cast<float*>(a.C)[o] += acc[i][j][r];
+          else reinterpret_cast<float*>(a.C)[o] = acc[i][j][r];
+        }
+      }
+    }
+  }
+}
+
+template <int BN>
+constexpr size_t big_lds_bytes() { return (size_t)2 * (256 + BN) * (BIG_BK + 8) * 2; }
+
+template <int BN, int EPI>
+hipError_t launch_big(const GemmArgs& a, hipStream_t st) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_big_kernel<BN, EPI>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)big_lds_bytes<BN>());
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const int nb = ((a.M + 255) / 256) * ((a.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_big_kernel<BN, EPI>), dim3(nb), dim3(256), big_lds_bytes<BN>(), st, a);
+  return hipGetLastError();
+}
+
 // Sum split-K partials in a fixed order and apply the epilogue.
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int S) {
@@ -203,13 +376,13 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int S) {
   else reinterpret_cast<float*>(a.C)[o] = s;
 }
 
-template <int BM, int BN, int EPI>
+template <int BM, int BN, int BK, int NS, int EPI>
 hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st) {
   const int nb = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   if (S <= 1) {
-    hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, EPI, false>), dim3(nb), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, BK, NS, EPI, false>), dim3(nb), dim3(256), 0, st, a);
   } else {
-    hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, EPI, true>), dim3(nb, 1, S), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, BK, NS, EPI, true>), dim3(nb, 1, S), dim3(256), 0, st, a);
     const int n_out = (EPI == EPI_SWIGLU) ? a.N / 2 : a.N;
     const size_t tot = (size_t)a.M * n_out;
     hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((tot + 255) / 256), dim3(256), 0, st, a, S);
@@ -220,17 +393,31 @@ hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st) {
 template <int EPI>
 hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st) {
   a.k_chunk = p.k_chunk;
-  if (p.bm == 128) return launch_tile<128, 128, EPI>(a, p.splits, st);
-  return launch_tile<64, 64, EPI>(a, p.splits, st);
+  if (p.bm == 256) {
+    // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0
+    if (EPI == EPI_SWIGLU && a.N % 64 != 0) return launch_tile<128, 128, 64, 2, EPI>(a, 1, st);
+    return p.bn == 256 ? launch_big<256, EPI>(a, st) : launch_big<128, EPI>(a, st);
+  }
+  if (p.bm == 128) return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st);
+  return launch_tile<64, 64, 128, 2, EPI>(a, p.splits, st);
 }
 
 }  // namespace
 
-// Tile and split-K choice.  Large M: 128x128 tiles.  Small M (decode): 64x64
+// Tile and split-K choice.  M > 512: 256x256 / 256x128 tiles; 256 < M <= 512:
+// 128x128 tiles.  Small M (decode): 64x64
 // tiles, split along K until the grid has about 1024 workgroups, keeping at
 // least 256 K-elements per split.
 GemmPlan gemm_plan(int M, int N, int K, int max_splits) {
   GemmPlan p;
+  if (M > 512) {
+    // 256-row macro tiles; 256 columns unless that leaves fewer than ~2 tiles per CU
+    p.bm = 256;
+    p.bn = (((M + 255) / 256) * ((N + 255) / 256) >= 512) ? 256 : 128;
+    p.splits = 1;
+    p.k_chunk = K;
+    return p;
+  }
   if (M > 256) {
     p.bm = 128;
     p.splits = 1;
@@ -241,7 +428,7 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits) {
   const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
   int s = 1;
   while (s < max_splits && tiles * s < 1024 && (K / (s * 2)) >= 256) s *= 2;
-  const int kc = (((K + s - 1) / s) + BK - 1) / BK * BK;
+  const int kc = (((K + s - 1) / s) + BK_MAX - 1) / BK_MAX * BK_MAX;
   p.splits = (K + kc - 1) / kc;
   p.k_chunk = kc;
   return p;

@@ -33,6 +33,7 @@ struct GemmArgs {
 
 struct GemmPlan {
   int bm = 128;
+  int bn = 128;
   int splits = 1;
   int k_chunk = 0;
 };

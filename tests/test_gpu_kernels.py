@@ -55,16 +55,38 @@ def _gemm_case(M_, N, K, epi, seed):
     np.testing.assert_allclose(got, ref, rtol=rtol, atol=2e-4 * scale)
 
 
-@pytest.mark.parametrize("M_,N,K", [(1, 64, 64), (37, 200, 136), (64, 6144, 4096), (256, 1024, 688),
-                                    (300, 1000, 688), (2080, 384, 512)])
+@pytest.mark.parametrize("M_,N,K", [(1, 64, 64), (37, 200, 136), (64, 6144, 4096), (48, 1000, 4096),
+                                    (64, 4096, 14336), (3, 520, 1384), (256, 1024, 688), (300, 1000, 688),
+                                    (2080, 384, 512), (600, 1000, 688), (2080, 6144, 1024), (1031, 4096, 1384)])
 @pytest.mark.parametrize("epi", [hxf.EPI_BF16, hxf.EPI_RESID, hxf.EPI_F32])
 def test_gemm(M_, N, K, epi):
     _gemm_case(M_, N, K, epi, seed=M_ * 7 + N + K + epi)
 
 
-@pytest.mark.parametrize("M_,N,K", [(5, 64, 256), (64, 2 * 688, 256), (300, 2 * 1376, 512), (128, 2 * 14336, 4096)])
+@pytest.mark.parametrize("M_,N,K", [(5, 64, 256), (64, 2 * 688, 256), (33, 2 * 688, 2048), (64, 2 * 14336, 4096),
+                                    (300, 2 * 1376, 512), (128, 2 * 14336, 4096), (700, 2 * 688, 256),
+                                    (2080, 2 * 2080, 512)])
 def test_gemm_swiglu(M_, N, K):
     _gemm_case(M_, N, K, hxf.EPI_SWIGLU, seed=M_ + N + K)
+
+
+def test_gemm_split_counters_reset_between_calls():
+    """Repeated split-K calls on one workspace give identical results (arrival
+    counters return to zero)."""
+    t = torch()
+    rng = np.random.default_rng(77)
+    M_, N, K = 64, 6144, 4096
+    ab, _ = rand_bf16(rng, (M_, K))
+    bb, _ = rand_bf16(rng, (N, K), 0.05)
+    A, B = dev_bits(ab), dev_bits(bb)
+    ws = t.empty(hxf.op_gemm_workspace_bytes(M_, N, K), dtype=t.uint8, device="cuda:0")
+    outs = []
+    for _ in range(3):
+        C = t.empty(M_ * N, dtype=t.float32, device="cuda:0")
+        hxf.op_gemm(A.data_ptr(), K, B.data_ptr(), 0, C.data_ptr(), N, M_, N, K, hxf.EPI_F32, ws.data_ptr(), ws.numel())
+        outs.append(C)
+    t.cuda.synchronize()
+    assert t.equal(outs[0], outs[1]) and t.equal(outs[0], outs[2])
 
 
 @pytest.mark.parametrize("d,rows", [(256, 7), (4096, 64), (5120, 33)])
