@@ -83,17 +83,178 @@ def cpu_baseline(shape, ctxs, n_layers_sample=4, iters=3):
             "measured_s": round(iters * (t_fwd + t_lm), 2)}
 
 
+# Calibrated cost-model coefficients in picoseconds (data, measured on one MI355X):
+# t_comp = (c0 + c1*L_in + c2*L_in^2 + d1*L_out) / 1e6 us  (Section 4.1's t_prefill + t_decode)
+# t_iter = (i0 + i1*T + i2*sum_decode_ctx + i3*prefill_attention_pairs) / 1e6 us
+COST_PS = {
+    "llama8b": ((2_000 * 10 ** 6, 30 * 10 ** 6, 2_000, 11_000 * 10 ** 6), (9_000 * 10 ** 6, 28 * 10 ** 6, 12_000, 700)),
+    "qwen32b": ((6_000 * 10 ** 6, 110 * 10 ** 6, 8_000, 30_000 * 10 ** 6), (28_000 * 10 ** 6, 100 * 10 ** 6, 48_000,
+                                                                           2_800)),
+}
+
+
+def load_model(name, n_layers=None):
+    import synth
+    from paper_2505_05286_amd.device import DeviceModel
+    shape = synth.model_shape(name, n_layers)
+    t0 = time.time()
+    progress(f"generating and uploading {shape.name}-shaped bf16 weights")
+    dm = DeviceModel(shape, lambda l: synth.gen_layer(shape, l), synth.gen_embed(shape), synth.gen_lm_head(shape),
+                     synth.norm_weight(shape), device="cuda:0")
+    progress(f"weights ready in {time.time() - t0:.1f} s")
+    return shape, dm
+
+
+def step_until(inst, now, cond, timed=None):
+    """Step until cond(info) is true; return (now, iterations, prefill tokens, decode rows, seconds)."""
+    import torch
+    from paper_2505_05286_amd import hxf
+    it = pf = dec = 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while True:
+        st, info = inst.step(now)
+        if st == hxf.IDLE:
+            break
+        now += info["t_iter_us"]
+        it += 1
+        pf += info["n_prefill_tokens"]
+        dec += info["n_logit_rows"]
+        if cond(info):
+            break
+    torch.cuda.synchronize()
+    return now, it, pf, dec, time.perf_counter() - t0
+
+
+def workload3():
+    """Mixed iterations: 32 running decodes (context U[1024, 4096]) co-batched with chunked
+    prefill (2048 tokens per iteration) of 16 prompts of length U[2048, 8192]."""
+    import synth
+    from paper_2505_05286_amd import hxf
+    from paper_2505_05286_amd.device import Engine
+    shape, dm = load_model("llama8b")
+    decodes, prompts = synth.workloads.cfg3(shape.vocab)
+    cost, it = COST_PS["llama8b"]
+    total = sum(-(-(len(s.prompt) + 4096) // 16) for s in decodes) + sum(-(-len(s.prompt) // 16) for s in prompts)
+    eng = Engine(dm, max_context=8192 + 4096, n_blocks=total + 256, max_seqs=64, chunk_tokens=2048, cost_ps=cost,
+                 iter_ps=it, clock=hxf.CLOCK_MEASURED)
+    inst = eng.inst
+    for s in decodes:
+        inst.submit(0, s.workflow, 0, 0, s.wf_slo_us, s.prompt, s.max_new_tokens)
+    progress("prefilling the 32 decode sequences (untimed)")
+    now, *_ = step_until(inst, 0, lambda i: i["n_prefill_tokens"] == 0)
+    for s in prompts:
+        inst.submit(now, s.workflow, 0, now, s.wf_slo_us, s.prompt, s.max_new_tokens)
+    progress("timed: mixed chunked-prefill + decode iterations")
+    now, iters, pf, dec, dt = step_until(inst, now, lambda i: i["n_prefill_tokens"] == 0)
+    return {"workload": "3: 8B, 16 prompts U[2048,8192] chunked 2048 + 32 decodes ctx U[1024,4096]",
+            "iterations": iters, "ms_per_iteration": round(dt / iters * 1e3, 3), "prefill_tokens": pf,
+            "prefill_tokens_per_s": round(pf / dt, 1), "decode_tokens_per_s": round(dec / dt, 1),
+            "tokens_per_s": round((pf + dec) / dt, 1)}
+
+
+def workload4():
+    """Shared-prefix candidates: 32 prefill-only 4096-token parents, 8 forks each decoding
+    256 tokens (256 sequences), then a 512-token correction prefill on the even branches."""
+    import synth
+    from paper_2505_05286_amd import hxf
+    from paper_2505_05286_amd.device import Engine
+    shape, dm = load_model("llama8b")
+    parents, forks, corr = synth.workloads.cfg4(shape.vocab)
+    cost, it = COST_PS["llama8b"]
+    n_blocks = 32 * 256 + 256 * 18 + 128 * 34 + 512
+    eng = Engine(dm, max_context=4096 + 256 + 512 + 16, n_blocks=n_blocks, max_seqs=256, chunk_tokens=2048,
+                 cost_ps=cost, iter_ps=it, clock=hxf.CLOCK_MEASURED)
+    inst = eng.inst
+    pid = [inst.submit(0, p.workflow, 0, 0, p.wf_slo_us, p.prompt, 0, retain=True) for p in parents]
+    progress("timed: prefill of 32 x 4096-token parents")
+    now, it1, pf1, _, dt1 = step_until(inst, 0, lambda i: False)
+    fid = {}
+    for f in forks:
+        fid[(f.workflow, f.branch)] = inst.submit(now, f.workflow, 1, 0, f.wf_slo_us, f.prompt, f.max_new_tokens,
+                                                  parent=pid[f.workflow], retain=f.retain_kv)
+    for p in pid:
+        inst.release(p)
+    progress("timed: 256 forked branches decoding 256 tokens each")
+    now, it2, pf2, dec2, dt2 = step_until(inst, now, lambda i: False)
+    for c in corr:
+        inst.submit(now, c.workflow, 2, 0, c.wf_slo_us, c.prompt, c.max_new_tokens, parent=fid[(c.workflow, c.branch)])
+    for (w, b), f in fid.items():
+        if b % 2 == 0:
+            inst.release(f)
+    progress("timed: 512-token correction prefill on 128 branches")
+    now, it3, pf3, _, dt3 = step_until(inst, now, lambda i: False)
+    return {"workload": "4: 8B, 32 shared 4096-token prompts x 8 branches x 256 tokens, 512-token corrections",
+            "parent_prefill_tokens_per_s": round(pf1 / dt1, 1),
+            "branch_decode_tokens_per_s": round(dec2 / dt2, 1), "branch_iterations": it2,
+            "branch_ms_per_iteration": round(dt2 / it2 * 1e3, 3),
+            "correction_prefill_tokens_per_s": round(pf3 / dt3, 1)}
+
+
+def cfg5_workflows(n, vocab):
+    import numpy as np
+    import synth
+    from paper_2505_05286_amd.workflows import Req, Workflow
+    s = synth.workloads.CFG5_SHAPE
+    out = []
+    for w in synth.workloads.cfg5(vocab=vocab, n_wf=n):
+        stages = [[Req(w.schema, s["s1_out"], retain=True)],
+                  [Req(np.zeros(0, np.int32), s["cand_out"], parent=(0, 0), retain=(b % 2 == 0))
+                   for b in range(s["n_cand"])],
+                  [Req(w.corrections[k], s["corr_out"], parent=(1, 2 * k)) for k in range(s["n_corr"])],
+                  [Req(w.eval_prompt, s["eval_out"])]]
+        shapes = [(w.schema_len, s["s1_out"]), (16, s["cand_out"]), (16 + s["corr_in"], s["corr_out"]),
+                  (s["eval_in"], s["eval_out"])]
+        out.append(Workflow(w.workflow, w.arrival_us, w.slo_us, stages, shapes))
+    return out
+
+
+def workload5(n_wf, policy):
+    """Qwen2.5-32B-shaped replay of four-stage workflows (Poisson arrivals, 0.5/s) driven by
+    the local priority queue; scheduling runs on the virtual clock, the forward on the GPU."""
+    from paper_2505_05286_amd import hxf
+    from paper_2505_05286_amd.device import Engine
+    from paper_2505_05286_amd.workflows import Driver
+    import torch
+    shape, dm = load_model("qwen32b")
+    wfs = cfg5_workflows(n_wf, shape.vocab)
+    cost, it = COST_PS["qwen32b"]
+    pol = {"pq": hxf.POLICY_PQ, "fcfs": hxf.POLICY_FCFS, "llf": hxf.POLICY_LLF}[policy]
+    eng = Engine(dm, max_context=8192 + 64 + 256 + 512 + 256 + 16, n_blocks=40_000, max_seqs=128,
+                 chunk_tokens=2048, cost_ps=cost, iter_ps=it, policy=pol)
+    d = Driver(eng.inst, wfs)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    d.run()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    st = d.stats()
+    st.update({"workload": f"5: 32B, {n_wf} four-stage workflows, Poisson 0.5/s, policy {policy}",
+               "gpu_seconds": round(dt, 2), "prefill_tokens_per_s": round(st["prefill_tokens"] / dt, 1),
+               "decode_tokens_per_s": round(st["decode_tokens"] / dt, 1)})
+    return st
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", type=int, default=2, choices=(2, 3, 4, 5),
+                    help="2 (default) prints the benchmark line; 3-5 print per-workload measurements")
+    ap.add_argument("--n-workflows", type=int, default=16, help="workload 5: workflows replayed")
+    ap.add_argument("--policy", default="pq", choices=("pq", "fcfs", "llf"), help="workload 5: local queue policy")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.workload != 2:
+        fn = {3: workload3, 4: workload4, 5: lambda: workload5(args.n_workflows, args.policy)}[args.workload]
+        print(json.dumps(fn()), flush=True)
+        return
 
     import numpy as np
     import torch
