@@ -109,20 +109,24 @@ typedef struct hxf_stage_req {
 
 /* Device pointers of one decoder layer.  Every matrix is bf16, row-major
  * [out_features, in_features]. */
+/* The projection matrices and the LM head are PACKED (hxf_op_pack_weight in
+ * hxf_ops.h: 16x32 tiles in MFMA operand order); shapes below are the logical
+ * row-major [rows, columns] before packing.  Norm gains and the embedding table
+ * are plain row-major bf16. */
 typedef struct hxf_layer_weights {
   const void* attn_norm;  /* bf16 [d] */
-  const void* wqkv;       /* bf16 [(Hq + 2*Hkv)*dh, d]: rows of Wq, then Wk, then Wv */
-  const void* wo;         /* bf16 [d, Hq*dh] */
+  const void* wqkv;       /* packed bf16 [(Hq + 2*Hkv)*dh, d]: rows of Wq, then Wk, then Wv */
+  const void* wo;         /* packed bf16 [d, Hq*dh] */
   const void* ffn_norm;   /* bf16 [d] */
-  const void* w_gate;     /* bf16 [F, d] */
-  const void* w_up;       /* bf16 [F, d] */
-  const void* w_down;     /* bf16 [d, F] */
+  const void* w_gate;     /* packed bf16 [F, d] */
+  const void* w_up;       /* packed bf16 [F, d] */
+  const void* w_down;     /* packed bf16 [d, F] */
 } hxf_layer_weights;
 
 typedef struct hxf_device_buffers {
   const void* embed;                 /* bf16 [V, d] */
   const void* final_norm;            /* bf16 [d] */
-  const void* lm_head;               /* bf16 [V, d] */
+  const void* lm_head;               /* packed bf16 [V, d] */
   const hxf_layer_weights* layers;   /* host array of n_layers entries (copied by hxf_bind) */
   void* kv_pool;                     /* hxf_kv_pool_bytes(cfg, n_blocks) bytes, 256-byte aligned */
   int64_t kv_pool_bytes;

@@ -31,7 +31,9 @@ extern "C" {
 /* GEMM epilogues */
 enum { HXF_EPI_BF16 = 0, HXF_EPI_RESID = 1, HXF_EPI_SWIGLU = 2, HXF_EPI_F32 = 3 };
 
-/* C = A[M,K] . B[N,K]^T, bf16 inputs, fp32 accumulation.
+/* C = A[M,K] . B[N,K]^T, bf16 inputs, fp32 accumulation.  A is row-major with row
+ * stride lda; B (and B2) are PACKED weights (hxf_op_pack_weight of the row-major
+ * [N,K] matrix, or [F,K] for SwiGLU).
  *   HXF_EPI_BF16:   C bf16 [M, ldc]            C = bf16(acc)
  *   HXF_EPI_RESID:  C fp32 [M, ldc]            C += acc          (residual stream)
  *   HXF_EPI_SWIGLU: B = W_gate [F,K], B2 = W_up [F,K], N = 2F; C bf16 [M, ldc],
@@ -42,6 +44,17 @@ enum { HXF_EPI_BF16 = 0, HXF_EPI_RESID = 1, HXF_EPI_SWIGLU = 2, HXF_EPI_F32 = 3 
 int64_t hxf_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
 int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void* C, int32_t ldc, int32_t M, int32_t N,
                 int32_t K, int32_t epilogue, void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Packed weight layout, used for every GEMM weight: W [N,K] bf16 row-major becomes
+ * tiles of 16 rows x 32 columns (1 KB), row-tiles outermost, zero padded to
+ * ceil(N/16)*16 rows and ceil(K/32)*32 columns; inside a tile the 8-element chunks
+ * are in the order [k%32 / 8][n%16], i.e. element (n, k) is at
+ *   ((n/16) * ceil(K/32) + k/32) * 512 + ((k%32)/8) * 128 + (n%16) * 8 + k%8.
+ * This is the operand order of the 16x16x32 bf16 MFMA, so a wavefront reads a tile
+ * as one contiguous kilobyte.  hxf_op_pack_weight converts W (device, K % 8 == 0)
+ * into out (device, hxf_packed_weight_bytes(N, K) bytes); W and out must not overlap. */
+int64_t hxf_packed_weight_bytes(int32_t N, int32_t K);
+int hxf_op_pack_weight(const void* W, int32_t N, int32_t K, void* out, void* stream);
 
 /* out[r] = bf16(x[rows[r]] / sqrt(mean(x[rows[r]]^2) + eps) * g); rows may be NULL (identity).
  * x fp32 [*, d], g bf16 [d], out bf16 [n_rows, d]; d % 4 == 0. */

@@ -8,6 +8,8 @@
 // into registers while the current one is multiplied.  Workgroups are renumbered so that
 // consecutive output tiles (which share a weight slice) land on the same XCD
 // and its L2.
+#include <utility>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -17,11 +19,23 @@ namespace {
 
 constexpr int BK_MAX = 128;
 
-// Logical column c of a SwiGLU GEMM: groups of 32 = 16 gate rows then 16 up rows.
+// B operands are packed weights: 16-row x 32-column tiles of 1 KB, row-tiles
+// outermost, and inside a tile the 8-element chunks in MFMA operand order
+// [k/8][row][8] (element (n, k) at ((n/16)*kt + k/32)*512 + ((k%32)/8)*128 +
+// (n%16)*8 + k%8, kt = ceil(K/32), zero padding).  One wavefront-wide 16-byte
+// load of a tile is 1 KB of contiguous memory.
+__device__ __forceinline__ size_t b_koff(int k) { return (size_t)(k >> 5) * 512 + ((k >> 3) & 3) * 128; }
+
+// Start of weight row n (k = 0) of a packed matrix.
+__device__ __forceinline__ const bf16_t* b_packed_row(const bf16_t* W, int kt, int n) {
+  return W + (size_t)(n >> 4) * kt * 512 + (n & 15) * 8;
+}
+
+// Logical column c of a GEMM; SwiGLU interleaves groups of 32 = 16 gate rows then 16 up rows.
 __device__ __forceinline__ const bf16_t* b_row(const GemmArgs& a, int c, bool swiglu) {
-  if (!swiglu) return a.B + (size_t)c * a.K;
+  if (!swiglu) return b_packed_row(a.B, a.kt, c);
   const int g = c >> 5, w = c & 31;
-  return ((w < 16) ? a.B : a.B2) + (size_t)(g * 16 + (w & 15)) * a.K;
+  return b_packed_row((w < 16) ? a.B : a.B2, a.kt, g * 16 + (w & 15));
 }
 
 // 16-byte load from a 16-byte aligned address (one global_load_dwordx4).
@@ -73,7 +87,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
   for (int j = 0; j < B_CH; ++j) {
     const int r = (tid + j * 256) / CPR;
     b_ok[j] = (n0 + r) < a.N;
-    b_ptr[j] = b_row(a, b_ok[j] ? n0 + r : 0, SW) + c16 * 8;
+    b_ptr[j] = b_row(a, b_ok[j] ? n0 + r : 0, SW) + b_koff(c16 * 8);
   }
   // NS register stages: the K tiles it+1 .. it+NS-1 are in flight while tile it
   // is multiplied (one stage is the tile being stored to LDS).
@@ -85,7 +99,7 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
       xa[j] = (a_ok[j] && kin) ? *reinterpret_cast<const uint4*>(a_ptr[j] + k0) : make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int j = 0; j < B_CH; ++j)
-      xb[j] = (b_ok[j] && kin) ? *reinterpret_cast<const uint4*>(b_ptr[j] + k0) : make_uint4(0, 0, 0, 0);
+      xb[j] = (b_ok[j] && kin) ? *reinterpret_cast<const uint4*>(b_ptr[j] + (size_t)k0 * 16) : make_uint4(0, 0, 0, 0);
   };
   auto stage_to_lds = [&](const uint4 (&xa)[A_CH], const uint4 (&xb)[B_CH]) {
 #pragma unroll
@@ -249,11 +263,11 @@ __global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs a) {
       const bf16_t* p;
       if (SW) {   // groups of 64 logical columns: 32 gate rows, then the 32 matching up rows
         const int w = c & 63;
-        p = ((w < 32) ? a.B : a.B2) + (size_t)((c >> 6) * 32 + (w & 31)) * a.K + c4 * 8;
+        p = b_packed_row((w < 32) ? a.B : a.B2, a.kt, (c >> 6) * 32 + (w & 31));
       } else {
-        p = a.B + (size_t)c * a.K + c4 * 8;
+        p = b_packed_row(a.B, a.kt, c);
       }
-      rb[j] = kin ? load16(p + k0) : make_uint4(0, 0, 0, 0);
+      rb[j] = kin ? load16(p + b_koff(c4 * 8) + (size_t)k0 * 16) : make_uint4(0, 0, 0, 0);
     }
   };
   auto store = [&](int buf) {
@@ -376,6 +390,186 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int S) {
   else reinterpret_cast<float*>(a.C)[o] = s;
 }
 
+// Decode-sized M (at most 16 * MT rows): a weight-streaming kernel fed by the
+// LDS DMA path (global_load_lds, 16 bytes per lane, no registers).  Each of
+// the WV wavefronts owns NTW 16-column tiles; a stage holds 64 K-elements of
+// the A rows (MT x 2 MFMA blocks, loaded by all wavefronts together) and of
+// each wavefront's weight tiles (NTW x 2 blocks), each block 1 KB laid out in
+// MFMA operand order.  NSTG stages are in flight: a wavefront waits for its
+// own DMAs of the oldest stage (vmcnt), one barrier makes everybody's visible
+// and frees the slot consumed one step earlier, which is refilled before the
+// multiplies.  Stages live in distinct LDS arrays and the loop is unrolled by
+// NSTG so the compiler can see that the LDS reads of a stage do not alias the
+// DMAs in flight (otherwise it waits for all of them).  Split K (grid.y)
+// writes fp32 partials; a reduction kernel finishes them.
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* global_ptr_t;
+
+__device__ __forceinline__ void dma16(const void* g, void* lds_block) {
+  __builtin_amdgcn_global_load_lds((global_ptr_t)g, (lds_ptr_t)lds_block, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+template <class F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) { static_for_impl(f, std::make_integer_sequence<int, N>{}); }
+
+constexpr int ST_WV = 4, ST_NTW = 2, ST_NSTG = 3;   // 4 wavefronts x 2 tiles = 128 columns per workgroup
+
+template <int MT, int EPI, bool SPLIT>
+__global__ __launch_bounds__(64 * ST_WV) void gemm_stream_kernel(GemmArgs a) {
+  constexpr int WV = ST_WV, NTW = ST_NTW, NSTG = ST_NSTG;
+  constexpr int A_BLK = MT * 2, B_BLK_W = NTW * 2;
+  constexpr int STAGE = (A_BLK + WV * B_BLK_W) * 512;       // bf16 elements per stage
+  constexpr int A_PER_W = A_BLK / WV;                       // A blocks each wavefront moves
+  constexpr int PER_STAGE = A_PER_W + B_BLK_W;              // DMA instructions per wavefront per stage
+  constexpr bool SW = (EPI == EPI_SWIGLU);
+  static_assert(A_BLK % WV == 0, "A blocks are split evenly over the wavefronts");
+  static_assert(NSTG == 3, "three stage arrays");
+  __shared__ __attribute__((aligned(1024))) bf16_t L0[STAGE], L1[STAGE], L2[STAGE];
+  auto slot = [&](auto ic) -> bf16_t* {
+    constexpr int I = decltype(ic)::value;
+    if constexpr (I == 0) return L0; else if constexpr (I == 1) return L1; else return L2;
+  };
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int c0 = (blockIdx.x * WV + w) * NTW * 16;          // first logical column of this wavefront
+  const int kb = blockIdx.y * a.k_chunk;
+  const int ke = min(a.K, kb + a.k_chunk);
+  const int kend = a.kt * 32;                               // packed K (zero padded past K)
+  const int nst = (ke - kb + 63) / 64;
+
+  // weight tile sources (lane offset included); tiles past the end repeat the last one (dropped)
+  // weight tile sources, lane offset included (tiles past the end repeat the last one; dropped)
+  const bf16_t* bsrc[NTW];
+#pragma unroll
+  for (int j = 0; j < NTW; ++j) bsrc[j] = b_row(a, min(c0 + j * 16, a.N - 1) & ~15, SW) + lane * 8;
+  // A block b = (row tile i, 32-column half kk): lane reads row 16i + r (rows past M repeat M-1)
+  const bf16_t* arow[A_PER_W];
+#pragma unroll
+  for (int u = 0; u < A_PER_W; ++u) arow[u] = a.A + (size_t)min(((w * A_PER_W + u) >> 1) * 16 + r, a.M - 1) * a.lda;
+  auto issue = [&](int s, bf16_t* base) {
+    const int k0 = kb + min(s, nst - 1) * 64;               // past the last stage: reload it (never read)
+#pragma unroll
+    for (int u = 0; u < A_PER_W; ++u) {
+      const int kk = (w * A_PER_W + u) & 1;
+      const int k = min(k0 + kk * 32 + g * 8, a.K - 8);      // stays in the row; the weights are zero past K
+      dma16(arow[u] + k, base + (w * A_PER_W + u) * 512);
+    }
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int t = min(k0 / 32 + kk, a.kt - 1);
+        dma16(bsrc[j] + (size_t)t * 512, base + (A_BLK + w * B_BLK_W + j * 2 + kk) * 512);
+      }
+  };
+  f32x4 acc[MT][NTW];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](const bf16_t* base, int s) {
+    const int k0 = kb + s * 64;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      if (k0 + kk * 32 >= kend) break;                      // a 32-block wholly past the packed K
+      bf16x8 fa[MT], fb[NTW];
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+        fa[i] = as_bf16x8(*reinterpret_cast<const uint4*>(base + (i * 2 + kk) * 512 + lane * 8));
+#pragma unroll
+      for (int j = 0; j < NTW; ++j)
+        fb[j] = as_bf16x8(*reinterpret_cast<const uint4*>(base + (A_BLK + w * B_BLK_W + j * 2 + kk) * 512 + lane * 8));
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) acc[i][j] = mfma16x16x32(fa[i], fb[j], acc[i][j]);
+    }
+  };
+
+  static_for<NSTG - 1>([&](auto ic) { issue(decltype(ic)::value, slot(ic)); });
+  int s0 = 0;
+  for (; s0 + NSTG <= nst; s0 += NSTG) {
+    static_for<NSTG>([&](auto ic) {
+      constexpr int J = decltype(ic)::value;
+      wait_vmcnt<(NSTG - 2) * PER_STAGE>();
+      __builtin_amdgcn_s_barrier();
+      issue(s0 + J + NSTG - 1, slot(std::integral_constant<int, (J + NSTG - 1) % NSTG>{}));
+      compute(slot(ic), s0 + J);
+    });
+  }
+  // the remaining nst - s0 < NSTG stages are already in flight, in slots 0, 1, ..
+  wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  static_for<NSTG - 1>([&](auto ic) {
+    if (s0 + decltype(ic)::value < nst) compute(slot(ic), s0 + decltype(ic)::value);
+  });
+
+  // lane holds rows 16i + 4g + e, column c0 + 16j + r
+  if (SPLIT) {
+    float* P = a.partial + (size_t)blockIdx.y * a.M * a.N;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = i * 16 + g * 4 + e;
+        if (row >= a.M) continue;
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) {
+          const int col = c0 + j * 16 + r;
+          if (col < a.N) P[(size_t)row * a.N + col] = acc[i][j][e];
+        }
+      }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int row = i * 16 + g * 4 + e;
+      if (row >= a.M) continue;
+      if (SW) {
+        if (c0 >= a.N) continue;                             // gate tile j = 0, up tile j = 1 of group c0 / 32
+        const float gt = acc[i][0][e], up = acc[i][1][e];
+        reinterpret_cast<bf16_t*>(a.C)[(size_t)row * a.ldc + (c0 >> 5) * 16 + r] = f2bf(gt / (1.f + __expf(-gt)) * up);
+      } else {
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) {
+          const int col = c0 + j * 16 + r;
+          if (col >= a.N) continue;
+          const size_t o = (size_t)row * a.ldc + col;
+          if (EPI == EPI_BF16) reinterpret_cast<bf16_t*>(a.C)[o] = f2bf(acc[i][j][e]);
+          else if (EPI == EPI_RESID) reinterpret_cast<float*>(a.C)[o] += acc[i][j][e];
+          else reinterpret_cast<float*>(a.C)[o] = acc[i][j][e];
+        }
+      }
+    }
+}
+
+template <int MT, int EPI>
+hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st) {
+  const int nb = (a.N + ST_WV * ST_NTW * 16 - 1) / (ST_WV * ST_NTW * 16);
+  if (S > 1) {
+    hipLaunchKernelGGL((gemm_stream_kernel<MT, EPI, true>), dim3(nb, S), dim3(64 * ST_WV), 0, st, a);
+    const int n_out = (EPI == EPI_SWIGLU) ? a.N / 2 : a.N;
+    const size_t tot = (size_t)a.M * n_out;
+    hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((tot + 255) / 256), dim3(256), 0, st, a, S);
+  } else {
+    hipLaunchKernelGGL((gemm_stream_kernel<MT, EPI, false>), dim3(nb, 1), dim3(64 * ST_WV), 0, st, a);
+  }
+  return hipGetLastError();
+}
+
 template <int BM, int BN, int BK, int NS, int EPI>
 hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st) {
   const int nb = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
@@ -393,6 +587,7 @@ hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st) {
 template <int EPI>
 hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st) {
   a.k_chunk = p.k_chunk;
+  if (p.stream) return p.bm <= 32 ? launch_stream<2, EPI>(a, p.splits, st) : launch_stream<4, EPI>(a, p.splits, st);
   if (p.bm == 256) {
     // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0
     if (EPI == EPI_SWIGLU && a.N % 64 != 0) return launch_tile<128, 128, 64, 2, EPI>(a, 1, st);
@@ -402,14 +597,50 @@ hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st) {
   return launch_tile<64, 64, 128, 2, EPI>(a, p.splits, st);
 }
 
+// One 16-byte chunk of the packed layout per thread: chunk q is tile q / 64 and,
+// inside it, [k/8 = (q % 64) / 16][row = q % 16].
+__global__ __launch_bounds__(256) void pack_weight_kernel(const bf16_t* __restrict__ W, int N, int K, int kt,
+                                                         bf16_t* __restrict__ out, size_t n_chunks) {
+  const size_t q = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= n_chunks) return;
+  const size_t tile = q >> 6;
+  const int c = (int)(q & 63);
+  const int n = (int)(tile / kt) * 16 + (c & 15);
+  const int k = (int)(tile % kt) * 32 + (c >> 4) * 8;
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (n < N && k < K) v = load16(W + (size_t)n * K + k);
+  *reinterpret_cast<uint4*>(out + q * 8) = v;
+}
+
 }  // namespace
 
-// Tile and split-K choice.  M > 512: 256x256 / 256x128 tiles; 256 < M <= 512:
-// 128x128 tiles.  Small M (decode): 64x64
-// tiles, split along K until the grid has about 1024 workgroups, keeping at
-// least 256 K-elements per split.
+size_t packed_weight_elems(int N, int K) { return (size_t)((N + 15) / 16) * 16 * (size_t)((K + 31) / 32) * 32; }
+
+hipError_t pack_weight_launch(const uint16_t* W, int N, int K, uint16_t* out, hipStream_t st) {
+  const size_t n_chunks = packed_weight_elems(N, K) / 8;
+  hipLaunchKernelGGL(pack_weight_kernel, dim3((unsigned)((n_chunks + 255) / 256)), dim3(256), 0, st,
+                     reinterpret_cast<const bf16_t*>(W), N, K, (K + 31) / 32, reinterpret_cast<bf16_t*>(out), n_chunks);
+  return hipGetLastError();
+}
+
+// Kernel, tile and split-K choice.  M <= 64 (decode): the weight-streaming
+// kernel.  64 < M <= 256: 64x64 tiles, split along K until the grid has about
+// 1024 workgroups, keeping at least 256 K-elements per split.  256 < M <= 512:
+// 128x128 tiles.  M > 512: 256x256 / 256x128 tiles.
 GemmPlan gemm_plan(int M, int N, int K, int max_splits) {
   GemmPlan p;
+  if (M <= 64) {
+    // weight streaming: 128 columns per workgroup; split K in powers of two while the
+    // grid stays within one workgroup per CU and every split keeps >= 512 of K
+    p.stream = true;
+    p.bm = M <= 32 ? 32 : 64;
+    const int tiles = (N + 127) / 128;
+    int s = 1;
+    while (s * 2 <= max_splits && tiles * s * 2 <= 256 && K / (s * 2) >= 512) s *= 2;
+    p.k_chunk = (((K + s - 1) / s) + 63) / 64 * 64;
+    p.splits = (K + p.k_chunk - 1) / p.k_chunk;
+    return p;
+  }
   if (M > 512) {
     // 256-row macro tiles; 256 columns unless that leaves fewer than ~2 tiles per CU
     p.bm = 256;

@@ -29,9 +29,11 @@ struct GemmArgs {
   int M, N, K;         // N is logical (2F for SwiGLU); K % 8 == 0
   int lda, ldc;
   int k_chunk;
+  int kt;              // K tiles of the packed weights, ceil(K / 32)
 };
 
 struct GemmPlan {
+  bool stream = false;  // decode-sized M: LDS-DMA weight-streaming kernel
   int bm = 128;
   int bn = 128;
   int splits = 1;
@@ -40,6 +42,10 @@ struct GemmPlan {
 
 GemmPlan gemm_plan(int M, int N, int K, int max_splits);
 hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st);
+// Weight packing: W bf16 [N, K] row-major -> tiles of 16 rows x 32 columns in MFMA
+// operand order, zero padded to ceil(N/16)*16 rows and ceil(K/32)*32 columns.
+size_t packed_weight_elems(int N, int K);
+hipError_t pack_weight_launch(const uint16_t* W, int N, int K, uint16_t* out, hipStream_t st);
 
 // ------------------------------------------------------------------ norms / embedding
 // out[r] = bf16(rmsnorm(x[rows ? rows[r] : r]) * g); x fp32 [*, d]

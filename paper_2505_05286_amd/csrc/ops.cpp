@@ -70,7 +70,18 @@ int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void*
   a.K = K;
   a.lda = lda;
   a.ldc = ldc;
+  a.kt = (K + 31) / 32;
   return dev_rc(gemm_launch(a, epi, p, (hipStream_t)stream));
+}
+
+int64_t hxf_packed_weight_bytes(int32_t N, int32_t K) {
+  if (N <= 0 || K <= 0) return 0;
+  return (int64_t)packed_weight_elems(N, K) * 2;
+}
+
+int hxf_op_pack_weight(const void* W, int32_t N, int32_t K, void* out, void* stream) {
+  if (!W || !out || N <= 0 || K <= 0 || K % 8) return HXF_EINVAL;
+  return dev_rc(pack_weight_launch((const uint16_t*)W, N, K, (uint16_t*)out, (hipStream_t)stream));
 }
 
 int hxf_op_rmsnorm(const float* x, const int32_t* rows, const void* g, void* out, int32_t n_rows, int32_t d, float eps,

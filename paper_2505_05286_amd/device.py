@@ -12,29 +12,41 @@ def _dev_u16(bits, device):
     return torch.from_numpy(a).to(device)
 
 
+def _dev_packed(bits, device):
+    """Upload a row-major bf16 [N, K] weight and repack it on the GPU into the
+    library's MFMA tile layout (the row-major copy is dropped)."""
+    n, k = bits.shape
+    src = _dev_u16(bits, device)
+    out = torch.empty(hxf.packed_weight_bytes(n, k) // 2, dtype=torch.int16, device=device)
+    hxf.op_pack_weight(src.data_ptr(), n, k, out.data_ptr(), torch.cuda.current_stream(device).cuda_stream)
+    return out
+
+
 class DeviceModel:
     """Weights of one decoder in HBM (bf16 bit patterns in int16 tensors).
 
     ``layer_fn(l)`` returns the host bf16 bits of layer l as a dict with keys
     wq, wk, wv, wo, w_gate, w_up, w_down; ``embed``, ``lm_head`` and ``norm``
     are host bf16 bits.  Wq, Wk and Wv are stacked row-wise into one QKV matrix.
+    Projection matrices and the LM head are held packed (hxf_op_pack_weight).
     """
 
     def __init__(self, shape, layer_fn, embed, lm_head, norm, device="cuda"):
         self.shape = shape
         self.device = device
         self.embed = _dev_u16(embed, device)
-        self.lm_head = _dev_u16(lm_head, device)
+        self.lm_head = _dev_packed(lm_head, device)
         self.norm = _dev_u16(norm, device)
         self.layers = []
         for l in range(shape.n_layers):
             w = layer_fn(l)
             qkv = np.concatenate([w["wq"], w["wk"], w["wv"]], axis=0)
             self.layers.append({
-                "wqkv": _dev_u16(qkv, device), "wo": _dev_u16(w["wo"], device),
-                "w_gate": _dev_u16(w["w_gate"], device), "w_up": _dev_u16(w["w_up"], device),
-                "w_down": _dev_u16(w["w_down"], device),
+                "wqkv": _dev_packed(qkv, device), "wo": _dev_packed(w["wo"], device),
+                "w_gate": _dev_packed(w["w_gate"], device), "w_up": _dev_packed(w["w_up"], device),
+                "w_down": _dev_packed(w["w_down"], device),
             })
+        torch.cuda.current_stream(device).synchronize()
 
     def layer_ptrs(self):
         n = self.norm.data_ptr()

@@ -118,6 +118,8 @@ _SIGS = {
     "hxf_profile_get": (C.c_int, [C.c_void_p, C.POINTER(Profile)]),
     # ops
     "hxf_op_gemm_workspace_bytes": (C.c_int64, [C.c_int32, C.c_int32, C.c_int32]),
+    "hxf_packed_weight_bytes": (C.c_int64, [C.c_int32, C.c_int32]),
+    "hxf_op_pack_weight": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]),
     "hxf_op_gemm": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32,
                               C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p]),
     "hxf_op_rmsnorm": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_float,
@@ -326,6 +328,14 @@ def op_gemm_workspace_bytes(M, N, K):
 def op_gemm(A, lda, B, B2, Cp, ldc, M, N, K, epi, ws=0, ws_bytes=0, stream=0):
     _op(lib().hxf_op_gemm(A, lda, B, B2 or None, Cp, ldc, M, N, K, epi, ws or None, ws_bytes, stream or None),
         "hxf_op_gemm")
+
+
+def packed_weight_bytes(N, K):
+    return lib().hxf_packed_weight_bytes(N, K)
+
+
+def op_pack_weight(W, N, K, out, stream=0):
+    _op(lib().hxf_op_pack_weight(W, N, K, out, stream or None), "hxf_op_pack_weight")
 
 
 def op_rmsnorm(x, rows, g, out, n_rows, d, eps, stream=0):

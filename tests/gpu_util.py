@@ -22,6 +22,18 @@ def dev_bits(bits):
     return t.from_numpy(np.ascontiguousarray(bits, np.uint16).view(np.int16)).to("cuda:0")
 
 
+def dev_packed(bits):
+    """uint16 bf16 bits [N, K] (numpy) -> the packed weight layout on cuda:0."""
+    from paper_2505_05286_amd import hxf
+    t = torch()
+    n, k = bits.shape
+    src = dev_bits(bits)
+    out = t.empty(hxf.packed_weight_bytes(n, k) // 2, dtype=t.int16, device="cuda:0")
+    hxf.op_pack_weight(src.data_ptr(), n, k, out.data_ptr())
+    t.cuda.synchronize()
+    return out
+
+
 def host_f64(tensor_i16):
     """int16 bf16-bit tensor -> float64 numpy."""
     b = tensor_i16.detach().cpu().numpy().view(np.uint16)

@@ -13,7 +13,7 @@ from oracle import model as M
 from oracle import paged as P
 from paper_2505_05286_amd import hxf
 
-from .gpu_util import dev_bits, empty_i16, host_f64, i32, log, rand_bf16, torch
+from .gpu_util import dev_bits, dev_packed, empty_i16, host_f64, i32, log, rand_bf16, torch
 
 pytestmark = pytest.mark.gpu
 
@@ -23,11 +23,11 @@ def _gemm_case(M_, N, K, epi, seed):
     rng = np.random.default_rng(seed)
     ab, af = rand_bf16(rng, (M_, K))
     bb, bf = rand_bf16(rng, (N if epi != hxf.EPI_SWIGLU else N // 2, K), 0.05)
-    A, B = dev_bits(ab), dev_bits(bb)
+    A, B = dev_bits(ab), dev_packed(bb)
     B2 = None
     if epi == hxf.EPI_SWIGLU:
         b2b, b2f = rand_bf16(rng, (N // 2, K), 0.05)
-        B2 = dev_bits(b2b)
+        B2 = dev_packed(b2b)
     ws_n = hxf.op_gemm_workspace_bytes(M_, N, K)
     ws = t.empty(max(ws_n, 256), dtype=t.uint8, device="cuda:0")
     n_out = N // 2 if epi == hxf.EPI_SWIGLU else N
@@ -56,7 +56,9 @@ def _gemm_case(M_, N, K, epi, seed):
 
 
 @pytest.mark.parametrize("M_,N,K", [(1, 64, 64), (37, 200, 136), (64, 6144, 4096), (48, 1000, 4096),
-                                    (64, 4096, 14336), (3, 520, 1384), (256, 1024, 688), (300, 1000, 688),
+                                    (64, 4096, 14336), (3, 520, 1384), (16, 4096, 4096), (64, 256, 8192),
+                                    (32, 136, 160), (17, 8192, 1024), (65, 4096, 4096),
+                                    (256, 1024, 688), (300, 1000, 688),
                                     (2080, 384, 512), (600, 1000, 688), (2080, 6144, 1024), (1031, 4096, 1384)])
 @pytest.mark.parametrize("epi", [hxf.EPI_BF16, hxf.EPI_RESID, hxf.EPI_F32])
 def test_gemm(M_, N, K, epi):
@@ -64,21 +66,21 @@ def test_gemm(M_, N, K, epi):
 
 
 @pytest.mark.parametrize("M_,N,K", [(5, 64, 256), (64, 2 * 688, 256), (33, 2 * 688, 2048), (64, 2 * 14336, 4096),
+                                    (20, 2 * 4096, 4096), (64, 2 * 96, 8192),
                                     (300, 2 * 1376, 512), (128, 2 * 14336, 4096), (700, 2 * 688, 256),
                                     (2080, 2 * 2080, 512)])
 def test_gemm_swiglu(M_, N, K):
     _gemm_case(M_, N, K, hxf.EPI_SWIGLU, seed=M_ + N + K)
 
 
-def test_gemm_split_counters_reset_between_calls():
-    """Repeated split-K calls on one workspace give identical results (arrival
-    counters return to zero)."""
+def test_gemm_split_repeatable():
+    """Repeated split-K calls on one workspace give bit-identical results."""
     t = torch()
     rng = np.random.default_rng(77)
     M_, N, K = 64, 6144, 4096
     ab, _ = rand_bf16(rng, (M_, K))
     bb, _ = rand_bf16(rng, (N, K), 0.05)
-    A, B = dev_bits(ab), dev_bits(bb)
+    A, B = dev_bits(ab), dev_packed(bb)
     ws = t.empty(hxf.op_gemm_workspace_bytes(M_, N, K), dtype=t.uint8, device="cuda:0")
     outs = []
     for _ in range(3):
@@ -291,3 +293,17 @@ def test_copy_probe():
     hxf.op_copy(a.data_ptr(), b.data_ptr(), a.numel() * 4)
     t.cuda.synchronize()
     assert t.equal(a, b)
+
+
+@pytest.mark.parametrize("N,K", [(37, 72), (64, 4096), (1, 8), (200, 136)])
+def test_pack_weight_layout(N, K):
+    """The packed weight layout is the row-major matrix, zero padded to 16 x 32
+    multiples, cut into 16 x 32 tiles (row-tiles outermost) stored [k/8][row][8]."""
+    rng = np.random.default_rng(N * 131 + K)
+    bits, _ = rand_bf16(rng, (N, K))
+    got = dev_packed(bits).cpu().numpy().view(np.uint16)
+    np_, kp = -(-N // 16) * 16, -(-K // 32) * 32
+    pad = np.zeros((np_, kp), np.uint16)
+    pad[:N, :K] = bits
+    want = pad.reshape(np_ // 16, 16, kp // 32, 4, 8).transpose(0, 2, 3, 1, 4).reshape(-1)
+    assert got.shape == want.shape and np.array_equal(got, want)
