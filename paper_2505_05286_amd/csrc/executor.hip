@@ -153,8 +153,10 @@ class HipExecutor : public Executor {
  private:
   template <typename T>
   T* dev(int64_t off) { return reinterpret_cast<T*>(ws_ + off); }
+  // With `pending` set, a split-K plan leaves its partials in the workspace and
+  // *pending = its split count (0 when the GEMM finished its own epilogue).
   int gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M, int N, int K,
-           int epi, std::string& err);
+           int epi, std::string& err, int* pending = nullptr);
 
   hxf_model_cfg m_;
   hxf_sched_cfg s_;
@@ -171,7 +173,7 @@ class HipExecutor : public Executor {
 };
 
 int HipExecutor::gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M,
-                      int N, int K, int epi, std::string& err) {
+                      int N, int K, int epi, std::string& err, int* pending) {
   GemmArgs a{};
   a.A = A;
   a.B = B;
@@ -189,7 +191,9 @@ int HipExecutor::gemm(const uint16_t* A, int lda, const uint16_t* B, const uint1
     err = "gemm: split-K partial buffer too small";
     return HXF_EINVAL;
   }
-  HXF_HIP(gemm_launch(a, epi, p, st_));
+  const bool defer = pending && p.splits > 1;
+  HXF_HIP(gemm_launch(a, epi, p, st_, !defer));
+  if (pending) *pending = defer ? p.splits : 0;
   return HXF_OK;
 }
 
@@ -323,13 +327,25 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
 
   HXF_HIP(embed_rmsnorm_launch(dm + o_ids, (const uint16_t*)b_.embed, (const uint16_t*)layers_[0].attn_norm, resid,
                                h, T, d, m_.rms_eps, st_));
+  // Split-K GEMMs of decode-sized batches hand their partials to the next kernel
+  // (RoPE/KV write, residual add + RMSNorm), which sums them in split order.
+  float* part = dev<float>(plan_.off_part);
+  int pend_down = 0;
   for (int l = 0; l < m_.n_layers; ++l) {
     const hxf_layer_weights& L = layers_[l];
     uint16_t* kp = pool + (int64_t)l * 2 * layer_pool;
     uint16_t* vp = kp + layer_pool;
-    if (l > 0) HXF_HIP(rmsnorm_launch(resid, nullptr, (const uint16_t*)L.attn_norm, h, T, d, m_.rms_eps, st_));
-    if (int rc = gemm(h, d, (const uint16_t*)L.wqkv, nullptr, qkv, qkv_w, T, qkv_w, d, EPI_BF16, err)) return rc;
-    HXF_HIP(rope_kv_launch(qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq, hkv, dh, st_));
+    if (l > 0)
+      HXF_HIP(resid_rmsnorm_launch(resid, part, pend_down, T, nullptr, (const uint16_t*)L.attn_norm, h, T, d,
+                                   m_.rms_eps, st_));
+    int pend_qkv = 0;
+    if (int rc = gemm(h, d, (const uint16_t*)L.wqkv, nullptr, qkv, qkv_w, T, qkv_w, d, EPI_BF16, err, &pend_qkv))
+      return rc;
+    if (pend_qkv)
+      HXF_HIP(rope_kv_partials_launch(qkv, part, pend_qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq,
+                                      hkv, dh, st_));
+    else
+      HXF_HIP(rope_kv_launch(qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq, hkv, dh, st_));
     da.k_pool = pa.k_pool = kp;
     da.v_pool = pa.v_pool = vp;
     if (da.n_items) {
@@ -350,18 +366,23 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
       HXF_HIP(decode_merge_launch(da, st_));
     }
     HXF_HIP(prefill_attn_launch(pa, st_));
-    if (int rc = gemm(attn, hq * dh, (const uint16_t*)L.wo, nullptr, resid, d, T, d, hq * dh, EPI_RESID, err))
+    int pend_o = 0;
+    if (int rc = gemm(attn, hq * dh, (const uint16_t*)L.wo, nullptr, resid, d, T, d, hq * dh, EPI_RESID, err, &pend_o))
       return rc;
-    HXF_HIP(rmsnorm_launch(resid, nullptr, (const uint16_t*)L.ffn_norm, h, T, d, m_.rms_eps, st_));
+    HXF_HIP(resid_rmsnorm_launch(resid, part, pend_o, T, nullptr, (const uint16_t*)L.ffn_norm, h, T, d, m_.rms_eps,
+                                 st_));
     if (int rc = gemm(h, d, (const uint16_t*)L.w_gate, (const uint16_t*)L.w_up, act, f, T, 2 * f, d, EPI_SWIGLU, err))
       return rc;
-    if (int rc = gemm(act, f, (const uint16_t*)L.w_down, nullptr, resid, d, T, d, f, EPI_RESID, err)) return rc;
+    if (int rc = gemm(act, f, (const uint16_t*)L.w_down, nullptr, resid, d, T, d, f, EPI_RESID, err, &pend_down))
+      return rc;
   }
   uint16_t* hr = dev<uint16_t>(plan_.off_hr);
   float* logits = dev<float>(plan_.off_logits);
   int32_t* samp = dev<int32_t>(plan_.off_sampled);
   if (R > 0) {
-    HXF_HIP(rmsnorm_launch(resid, dm + o_lrow, (const uint16_t*)b_.final_norm, hr, R, d, m_.rms_eps, st_));
+    // (rows without logits never need the last down projection's partials)
+    HXF_HIP(resid_rmsnorm_launch(resid, part, pend_down, T, dm + o_lrow, (const uint16_t*)b_.final_norm, hr, R, d,
+                                 m_.rms_eps, st_));
     if (int rc = gemm(hr, d, (const uint16_t*)b_.lm_head, nullptr, logits, m_.vocab, R, m_.vocab, d, EPI_F32, err))
       return rc;
     HXF_HIP(argmax_launch(logits, samp, R, m_.vocab, st_));

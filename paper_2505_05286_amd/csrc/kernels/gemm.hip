@@ -557,10 +557,11 @@ __global__ __launch_bounds__(64 * ST_WV) void gemm_stream_kernel(GemmArgs a) {
 }
 
 template <int MT, int EPI>
-hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st) {
+hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st, bool reduce) {
   const int nb = (a.N + ST_WV * ST_NTW * 16 - 1) / (ST_WV * ST_NTW * 16);
   if (S > 1) {
     hipLaunchKernelGGL((gemm_stream_kernel<MT, EPI, true>), dim3(nb, S), dim3(64 * ST_WV), 0, st, a);
+    if (!reduce) return hipGetLastError();
     const int n_out = (EPI == EPI_SWIGLU) ? a.N / 2 : a.N;
     const size_t tot = (size_t)a.M * n_out;
     hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((tot + 255) / 256), dim3(256), 0, st, a, S);
@@ -571,12 +572,13 @@ hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st) {
 }
 
 template <int BM, int BN, int BK, int NS, int EPI>
-hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st) {
+hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st, bool reduce = true) {
   const int nb = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   if (S <= 1) {
     hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, BK, NS, EPI, false>), dim3(nb), dim3(256), 0, st, a);
   } else {
     hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, BK, NS, EPI, true>), dim3(nb, 1, S), dim3(256), 0, st, a);
+    if (!reduce) return hipGetLastError();
     const int n_out = (EPI == EPI_SWIGLU) ? a.N / 2 : a.N;
     const size_t tot = (size_t)a.M * n_out;
     hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((tot + 255) / 256), dim3(256), 0, st, a, S);
@@ -585,16 +587,17 @@ hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st) {
 }
 
 template <int EPI>
-hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st) {
+hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st, bool reduce) {
   a.k_chunk = p.k_chunk;
-  if (p.stream) return p.bm <= 32 ? launch_stream<2, EPI>(a, p.splits, st) : launch_stream<4, EPI>(a, p.splits, st);
+  if (p.stream)
+    return p.bm <= 32 ? launch_stream<2, EPI>(a, p.splits, st, reduce) : launch_stream<4, EPI>(a, p.splits, st, reduce);
   if (p.bm == 256) {
     // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0
     if (EPI == EPI_SWIGLU && a.N % 64 != 0) return launch_tile<128, 128, 64, 2, EPI>(a, 1, st);
     return p.bn == 256 ? launch_big<256, EPI>(a, st) : launch_big<128, EPI>(a, st);
   }
-  if (p.bm == 128) return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st);
-  return launch_tile<64, 64, 128, 2, EPI>(a, p.splits, st);
+  if (p.bm == 128) return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce);
+  return launch_tile<64, 64, 128, 2, EPI>(a, p.splits, st, reduce);
 }
 
 // One 16-byte chunk of the packed layout per thread: chunk q is tile q / 64 and,
@@ -665,12 +668,12 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits) {
   return p;
 }
 
-hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st) {
+hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st, bool reduce) {
   switch (epi) {
-    case EPI_BF16: return launch_epi<EPI_BF16>(a, p, st);
-    case EPI_RESID: return launch_epi<EPI_RESID>(a, p, st);
-    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, p, st);
-    default: return launch_epi<EPI_F32>(a, p, st);
+    case EPI_BF16: return launch_epi<EPI_BF16>(a, p, st, reduce);
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, p, st, reduce);
+    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, p, st, reduce);
+    default: return launch_epi<EPI_F32>(a, p, st, reduce);
   }
 }
 

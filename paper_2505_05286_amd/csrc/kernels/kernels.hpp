@@ -41,7 +41,9 @@ struct GemmPlan {
 };
 
 GemmPlan gemm_plan(int M, int N, int K, int max_splits);
-hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st);
+// With reduce == false a split-K plan leaves its fp32 partials [splits][M][N] in
+// a.partial for the consumer to sum (no reduction launch).
+hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st, bool reduce = true);
 // Weight packing: W bf16 [N, K] row-major -> tiles of 16 rows x 32 columns in MFMA
 // operand order, zero padded to ceil(N/16)*16 rows and ceil(K/32)*32 columns.
 size_t packed_weight_elems(int N, int K);
@@ -51,6 +53,10 @@ hipError_t pack_weight_launch(const uint16_t* W, int N, int K, uint16_t* out, hi
 // out[r] = bf16(rmsnorm(x[rows ? rows[r] : r]) * g); x fp32 [*, d]
 hipError_t rmsnorm_launch(const float* x, const int32_t* rows, const uint16_t* g, uint16_t* out,
                           int n_rows, int d, float eps, hipStream_t st);
+// x[rows[r]] += sum over z < S of part[z][rows[r]] (split-K partials [S][part_rows][d] of a
+// residual GEMM, in split order), then out[r] = bf16(rmsnorm(x[rows[r]]) * g)
+hipError_t resid_rmsnorm_launch(float* x, const float* part, int S, int part_rows, const int32_t* rows,
+                                const uint16_t* g, uint16_t* out, int n_rows, int d, float eps, hipStream_t st);
 // resid[t] = E[ids[t]] (fp32); out[t] = bf16(rmsnorm(resid[t]) * g)
 hipError_t embed_rmsnorm_launch(const int32_t* ids, const uint16_t* E, const uint16_t* g, float* resid,
                                 uint16_t* out, int T, int d, float eps, hipStream_t st);
@@ -61,6 +67,11 @@ hipError_t embed_rmsnorm_launch(const int32_t* ids, const uint16_t* E, const uin
 hipError_t rope_kv_launch(uint16_t* qkv, const int32_t* pos, const int32_t* slot, const float2* cs,
                           uint16_t* k_pool, uint16_t* v_pool, int64_t n_blocks, int T, int Hq, int Hkv, int dh,
                           hipStream_t st);
+// The same with the projection given as S split-K partials part [S][T][(Hq+2Hkv)*dh]
+// (each value = bf16 of their sum in split order); rotated q goes to qkv.
+hipError_t rope_kv_partials_launch(uint16_t* qkv, const float* part, int S, const int32_t* pos, const int32_t* slot,
+                                   const float2* cs, uint16_t* k_pool, uint16_t* v_pool, int64_t n_blocks, int T,
+                                   int Hq, int Hkv, int dh, hipStream_t st);
 // Write k, v bf16 [T, Hkv, dh] to slot[t] (no rotation).
 hipError_t kv_scatter_launch(const uint16_t* k, const uint16_t* v, const int32_t* slot, uint16_t* k_pool,
                              uint16_t* v_pool, int64_t n_blocks, int T, int Hkv, int dh, hipStream_t st);

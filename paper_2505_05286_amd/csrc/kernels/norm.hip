@@ -36,12 +36,35 @@ __device__ __forceinline__ void norm_store(const float4* x4, const uint16_t* g, 
   }
 }
 
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* x, const int32_t* rows, const uint16_t* g,
-                                                      uint16_t* out, int d, float eps) {
+// With S > 0 the row first takes the S split-K partial sums of a residual GEMM
+// (part [S][part_rows][d], summed in split order, then added), exactly as the
+// GEMM's own reduction would have, and the updated row is stored back.  The S
+// partial loads of an element are independent and issued together.
+template <int S>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(float* x, const int32_t* rows, const float* part, int part_rows,
+                                                      const uint16_t* g, uint16_t* out, int d, float eps) {
   __shared__ float red[4];
   const int r = blockIdx.x;
   const int src = rows ? rows[r] : r;
-  norm_store(reinterpret_cast<const float4*>(x + (size_t)src * d), g, out + (size_t)r * d, d, eps, red);
+  float4* x4 = reinterpret_cast<float4*>(x + (size_t)src * d);
+  if constexpr (S > 0) {
+    const float4* p4 = reinterpret_cast<const float4*>(part + (size_t)src * d);
+    const size_t zs = (size_t)part_rows * d / 4;
+    for (int i = threadIdx.x; i < (d >> 2); i += 256) {
+      float4 q[S];
+#pragma unroll
+      for (int z = 0; z < S; ++z) q[z] = p4[z * zs + i];
+      float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int z = 0; z < S; ++z) {
+        s.x += q[z].x; s.y += q[z].y; s.z += q[z].z; s.w += q[z].w;
+      }
+      float4 v = x4[i];
+      v.x += s.x; v.y += s.y; v.z += s.z; v.w += s.w;
+      x4[i] = v;
+    }
+  }
+  norm_store(x4, g, out + (size_t)r * d, d, eps, red);
 }
 
 __global__ __launch_bounds__(256) void embed_rmsnorm_kernel(const int32_t* ids, const uint16_t* E, const uint16_t* g,
@@ -62,8 +85,22 @@ __global__ __launch_bounds__(256) void embed_rmsnorm_kernel(const int32_t* ids, 
 
 hipError_t rmsnorm_launch(const float* x, const int32_t* rows, const uint16_t* g, uint16_t* out, int n_rows, int d,
                           float eps, hipStream_t st) {
+  return resid_rmsnorm_launch(const_cast<float*>(x), nullptr, 0, 0, rows, g, out, n_rows, d, eps, st);
+}
+
+hipError_t resid_rmsnorm_launch(float* x, const float* part, int S, int part_rows, const int32_t* rows,
+                                const uint16_t* g, uint16_t* out, int n_rows, int d, float eps, hipStream_t st) {
   if (n_rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3(n_rows), dim3(256), 0, st, x, rows, g, out, d, eps);
+#define HXF_NORM(SS)                                                                                         \
+  case SS:                                                                                                   \
+    hipLaunchKernelGGL(rmsnorm_kernel<SS>, dim3(n_rows), dim3(256), 0, st, x, rows, part, part_rows, g, out, d, \
+                       eps);                                                                                 \
+    break;
+  switch (S) {
+    HXF_NORM(0) HXF_NORM(1) HXF_NORM(2) HXF_NORM(3) HXF_NORM(4) HXF_NORM(5) HXF_NORM(6) HXF_NORM(7) HXF_NORM(8)
+    default: return hipErrorInvalidValue;
+  }
+#undef HXF_NORM
   return hipGetLastError();
 }
 
