@@ -28,6 +28,12 @@ sys.path.insert(0, ROOT)
 
 METRIC = "prefill+decode tokens/s per MI355X at 8B shape; decode-attn HBM % of peak"
 HBM_PEAK_GBS = 8000.0
+# HBM bytes per launch of decode_attn_kernel<128> from hardware counters
+# (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, over `bench.py --attn-kernel-probe`,
+# each scaled by what the counter reads for a 1 GiB copy: 2.000 and 1.000); valid
+# for the kernel as it stands, to be re-measured whenever it changes.
+DECODE_ATTN_TRAFFIC = {"bytes_per_launch": 843_570_944, "algorithmic_bytes_per_launch": 829_956_096,
+                       "sample": "attention probe, 64 contexts of the benchmark, 202626 tokens"}
 BATCH = 64
 MAX_NEW = 1000
 
@@ -235,6 +241,53 @@ def workload5(n_wf, policy):
     return st
 
 
+def attn_kernel_probe(reps=8):
+    """Only the paged decode-attention kernel (plus its merge) on the benchmark's
+    64 contexts, `reps` times, then one 1 GiB device copy of known size: the short
+    program the hardware-counter runs profile (the copy calibrates FETCH_SIZE and
+    WRITE_SIZE).  KV pages are contiguous per sequence, contents random bf16."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2505_05286_amd import hxf
+
+    hxf.lib()
+    shape = synth.model_shape("llama8b")
+    hq, hkv, dh = shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+    stages = synth.workloads.cfg2(vocab=shape.vocab, n=BATCH, max_new_tokens=MAX_NEW)
+    ctx = np.array([len(s.prompt) + 8 for s in stages], np.int32)
+    pages = -(-ctx // 16)
+    n_blocks = int(pages.sum())
+    bt_w = int(pages.max())
+    bt = np.zeros((BATCH, bt_w), np.int32)
+    off = 0
+    for b, n in enumerate(pages):
+        bt[b, :n] = np.arange(off, off + n)
+        off += n
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(0)
+    per = hkv * n_blocks * 16 * dh
+    kp = (torch.randn(per, device=dev, generator=g) * 0.5).to(torch.bfloat16)
+    vp = (torch.randn(per, device=dev, generator=g) * 0.5).to(torch.bfloat16)
+    q = (torch.randn(BATCH * hq * dh, device=dev, generator=g) * 0.5).to(torch.bfloat16)
+    out = torch.empty_like(q)
+    btd = torch.from_numpy(bt).to(dev)
+    wsb = hxf.op_decode_attention_workspace_bytes(BATCH, hq, hkv, dh, ctx)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    st = torch.cuda.current_stream().cuda_stream
+    for _ in range(reps):
+        hxf.op_decode_attention(q.data_ptr(), kp.data_ptr(), vp.data_ptr(), n_blocks, btd.data_ptr(), bt_w, ctx,
+                                out.data_ptr(), BATCH, hq, hkv, dh, ws.data_ptr(), wsb, st)
+    copy_bytes = 1 << 30
+    src = torch.empty(copy_bytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    hxf.op_copy(src.data_ptr(), dst.data_ptr(), copy_bytes, st)
+    torch.cuda.synchronize()
+    return {"probe": "decode attention kernel", "launches": reps, "sum_context_tokens": int(ctx.sum()),
+            "kv_bytes_per_launch": int(ctx.sum()) * 2 * hkv * dh * 2, "copy_bytes": copy_bytes}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -245,11 +298,17 @@ def main():
                     help="2 (default) prints the benchmark line; 3-5 print per-workload measurements")
     ap.add_argument("--n-workflows", type=int, default=16, help="workload 5: workflows replayed")
     ap.add_argument("--policy", default="pq", choices=("pq", "fcfs", "llf"), help="workload 5: local queue policy")
+    ap.add_argument("--attn-kernel-probe", action="store_true",
+                    help="run only the decode-attention kernel and a calibration copy (for counter runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.attn_kernel_probe:
+        print(json.dumps(attn_kernel_probe()), flush=True)
+        return
 
     if args.workload != 2:
         fn = {3: workload3, 4: workload4, 5: lambda: workload5(args.n_workflows, args.policy)}[args.workload]
@@ -335,7 +394,8 @@ def main():
                    "batch": BATCH, "layers": shape.n_layers, "sum_context_tokens": int(sum_ctx_now)},
         "prefill_tokens_per_s": round(pf_tokens / t_pf, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": DECODE_ATTN_TRAFFIC["bytes_per_launch"],
+                     "traffic_sample": DECODE_ATTN_TRAFFIC,
                      "kernel": "decode_attn_kernel<128>", "avg_launch_us": round(avg_ms * 1e3, 2),
                      "bytes_per_launch": int(bytes_per_launch)},
     }
