@@ -14,7 +14,8 @@ sampled ids back on the host.
 Prints one JSON line.  `value` is decode tokens/s over the K timed steps.
 `roofline` is the paged decode-attention kernel (the largest single kernel of
 the step): algorithmic K+V bytes per launch over its average duration, timed
-with HIP events on the instance's stream.  `cpu_baseline` times the CPU
+with HIP events that the launch itself stamps with the kernel's start and end
+(hipExtLaunchKernel) on the instance's stream.  `cpu_baseline` times the CPU
 oracle on a bounded sample of the same step.
 """
 import argparse

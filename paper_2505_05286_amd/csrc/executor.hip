@@ -353,11 +353,9 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
       if (prof.on) {
         HXF_HIP(hipEventCreate(&e0));
         HXF_HIP(hipEventCreate(&e1));
-        HXF_HIP(hipEventRecord(e0, st_));
       }
-      HXF_HIP(decode_attn_launch(da, st_));
+      HXF_HIP(decode_attn_launch(da, st_, e0, e1));
       if (prof.on) {
-        HXF_HIP(hipEventRecord(e1, st_));
         ev_pool_.push_back(e0);
         ev_pool_.push_back(e1);
         prof.decode_attn_launches += 1;

@@ -17,6 +17,8 @@
 // instruction of a wavefront reads 1 KiB of contiguous memory; V pages are
 // stored transposed ([dh][token]) and read as 8-byte vectors, 512 contiguous
 // bytes per instruction.
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -272,11 +274,15 @@ __global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillAttnArgs a) {
 
 int prefill_queries_per_item(int group) { return 4 * (16 / group); }
 
-hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st) {
+hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (a.n_items <= 0) return hipSuccess;
-  if (a.dh == 128) hipLaunchKernelGGL(decode_attn_kernel<128>, dim3(a.n_items), dim3(64), 0, st, a);
-  else if (a.dh == 64) hipLaunchKernelGGL(decode_attn_kernel<64>, dim3(a.n_items), dim3(64), 0, st, a);
-  else return hipErrorInvalidValue;
+  // with events, they take the kernel's own start and end timestamps
+  if (a.dh == 128)
+    hipExtLaunchKernelGGL(decode_attn_kernel<128>, dim3(a.n_items), dim3(64), 0, st, ev_start, ev_stop, 0, a);
+  else if (a.dh == 64)
+    hipExtLaunchKernelGGL(decode_attn_kernel<64>, dim3(a.n_items), dim3(64), 0, st, ev_start, ev_stop, 0, a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

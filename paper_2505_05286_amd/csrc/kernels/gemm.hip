@@ -1,13 +1,13 @@
-// bf16 "NT" GEMM on CDNA4 matrix cores: C[M,N] = A[M,K] * B[N,K]^T with an
-// fp32 accumulator and fused epilogues (bf16 store, fp32 residual add,
-// SwiGLU gate*up, fp32 store) or fp32 split-K partials.
-//
-// Tiling: 256 threads = 4 wavefronts in a 2x2 arrangement; each wave owns a
-// (BM/2)x(BN/2) sub-tile made of 16x16 v_mfma_f32_16x16x32_bf16 tiles.  K is
-// staged through LDS (64 or 128 at a time); the next NS-1 K tiles are fetched
-// into registers while the current one is multiplied.  Workgroups are renumbered so that
-// consecutive output tiles (which share a weight slice) land on the same XCD
-// and its L2.
+// bf16 "NT" GEMMs on CDNA4 matrix cores: C[M,N] = A[M,K] * B[N,K]^T with an
+// fp32 accumulator and fused epilogues (bf16 store, fp32 residual add, SwiGLU
+// gate*up, fp32 store) or fp32 split-K partials.  A is row-major activations, B
+// the packed weights (see below).  Three kernels by M:
+//   M <= 64      gemm_stream_kernel: weight streaming through LDS DMA, split K;
+//   64 < M <= 512 gemm_nt_kernel: 64x64 / 128x128 tiles of 16x16x32 MFMAs, K
+//                staged through LDS from registers, split K for M <= 256;
+//   M > 512      gemm_big_dma_kernel: 256-row tiles of 32x32x16 MFMAs fed by LDS DMA.
+// Workgroups are renumbered so that consecutive output tiles (which share a
+// weight slice) land on the same XCD and its L2.
 #include <utility>
 
 #include "common.hpp"
@@ -213,155 +213,6 @@ __global__ __launch_bounds__(256) void gemm_nt_kernel(GemmArgs a) {
         else reinterpret_cast<float*>(a.C)[o] = acc[i][j][e];
       }
     }
-}
-
-// Large-tile kernel for prefill-sized M, on the 32x32x16 bf16 MFMA (the
-// 16x16x32 shape issues at half the rate on gfx950).  A 256 x BN macro tile
-// per workgroup of 4 wavefronts (2 x 2); each wavefront owns a 128 x BN/2
-// sub-tile of 32x32 MFMA tiles whose accumulators live in the accumulation
-// registers.  K advances 32 at a time through two LDS buffers: while step k is
-// multiplied out of one buffer, step k+1 is fetched into registers and then
-// written to the other buffer (one barrier per step).  Rows of 40 bf16 (80
-// bytes) keep the 16-byte fragment reads of consecutive rows on distinct
-// banks.  SwiGLU uses groups of 64 logical columns (32 gate rows, then the 32
-// matching up rows) so gate and up land in the same lane.
-constexpr int BIG_BK = 64;
-
-template <int BN, int EPI>
-__global__ __launch_bounds__(256) void gemm_big_kernel(GemmArgs a) {
-  constexpr int BM = 256, BK = BIG_BK, ROW = BK + 8;
-  constexpr int TM = 4, TN = BN / 64;              // 32x32 tiles per wave
-  constexpr int A_CH = BM * (BK / 8) / 256;        // 16-byte chunks per thread per K step
-  constexpr int B_CH = BN * (BK / 8) / 256;
-  constexpr int STAGE = (BM + BN) * ROW;           // bf16 elements per LDS buffer
-  constexpr bool SW = (EPI == EPI_SWIGLU);
-  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
-
-  const int tiles_m = (a.M + BM - 1) / BM;
-  const int tiles_n = (a.N + BN - 1) / BN;
-  const int L = xcd_remap(blockIdx.x, tiles_m * tiles_n);
-  const int tn = L / tiles_m, tm = L % tiles_m;
-  const int m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
-  constexpr int CPR = BK / 8, RPP = 256 / CPR;     // chunks per row, rows per fetch pass
-  const int c4 = tid % CPR, r4 = tid / CPR;
-
-  // a thread's chunks: rows r4 + RPP*j of the A and B tiles, k offset c4*8
-  const bf16_t* a_base = a.A + c4 * 8;
-  uint4 ra[A_CH], rb[B_CH];
-  auto fetch = [&](int k0) {
-    const bool kin = (k0 + c4 * 8) < a.K;
-#pragma unroll
-    for (int j = 0; j < A_CH; ++j) {
-      const int r = min(m0 + r4 + RPP * j, a.M - 1);         // rows past M repeat row M-1 (outputs dropped)
-      ra[j] = kin ? load16(a_base + (size_t)r * a.lda + k0) : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int j = 0; j < B_CH; ++j) {
-      const int c = min(n0 + r4 + RPP * j, a.N - 1);          // logical column; past N repeats N-1 (dropped)
-      const bf16_t* p;
-      if (SW) {   // groups of 64 logical columns: 32 gate rows, then the 32 matching up rows
-        const int w = c & 63;
-        p = b_packed_row((w < 32) ? a.B : a.B2, a.kt, (c >> 6) * 32 + (w & 31));
-      } else {
-        p = b_packed_row(a.B, a.kt, c);
-      }
-      rb[j] = kin ? load16(p + b_koff(c4 * 8) + (size_t)k0 * 16) : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto store = [&](int buf) {
-    bf16_t* As = smem + buf * STAGE;
-    bf16_t* Bs = As + BM * ROW;
-#pragma unroll
-    for (int j = 0; j < A_CH; ++j) *reinterpret_cast<uint4*>(&As[(r4 + RPP * j) * ROW + c4 * 8]) = ra[j];
-#pragma unroll
-    for (int j = 0; j < B_CH; ++j) *reinterpret_cast<uint4*>(&Bs[(r4 + RPP * j) * ROW + c4 * 8]) = rb[j];
-  };
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  const int nk = (a.K + BK - 1) / BK;
-  const int l32 = lane & 31, kh = (lane >> 5) * 8;
-  fetch(0);
-  store(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) fetch((kt + 1) * BK);
-    const bf16_t* As = smem + cur * STAGE;
-    const bf16_t* Bs = As + BM * ROW;
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int kc = ks * 16 + kh;
-      bf16x8 fb[TN];
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        fb[j] = as_bf16x8(*reinterpret_cast<const uint4*>(&Bs[(wn * (BN / 2) + j * 32 + l32) * ROW + kc]));
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const bf16x8 fa = as_bf16x8(*reinterpret_cast<const uint4*>(&As[(wm * 128 + i * 32 + l32) * ROW + kc]));
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(fa, fb[j], acc[i][j]);
-      }
-    }
-    if (kt + 1 < nk) store(cur ^ 1);
-    __syncthreads();
-  }
-
-  // lane holds column l32 and rows 8*(r/4) + 4*(lane/32) + r%4 of each 32x32 tile
-  const int rq = (lane >> 5) * 4;
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = m0 + wm * 128 + i * 32 + (r >> 2) * 8 + rq + (r & 3);
-      if (row >= a.M) continue;
-      if (SW) {
-#pragma unroll
-        for (int j = 0; j < TN; j += 2) {
-          const int lc = n0 + wn * (BN / 2) + j * 32;   // first (gate) logical column of the 64-group
-          if (lc >= a.N) continue;
-          const float g = acc[i][j][r], u = acc[i][j + 1][r];
-          reinterpret_cast<bf16_t*>(a.C)[(size_t)row * a.ldc + (lc >> 6) * 32 + l32] =
-              f2bf(g / (1.f + __expf(-g)) * u);
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int col = n0 + wn * (BN / 2) + j * 32 + l32;
-          if (col >= a.N) continue;
-          const size_t o = (size_t)row * a.ldc + col;
-          if (EPI == EPI_BF16) reinterpret_cast<bf16_t*>(a.C)[o] = f2bf(acc[i][j][r]);
-          else if (EPI == EPI_RESID) reinterpret_cast<float*>(a.C)[o] += acc[i][j][r];
-          else reinterpret_cast<float*>(a.C)[o] = acc[i][j][r];
-        }
-      }
-    }
-  }
-}
-
-template <int BN>
-constexpr size_t big_lds_bytes() { return (size_t)2 * (256 + BN) * (BIG_BK + 8) * 2; }
-
-template <int BN, int EPI>
-hipError_t launch_big(const GemmArgs& a, hipStream_t st) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_big_kernel<BN, EPI>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)big_lds_bytes<BN>());
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  const int nb = ((a.M + 255) / 256) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_big_kernel<BN, EPI>), dim3(nb), dim3(256), big_lds_bytes<BN>(), st, a);
-  return hipGetLastError();
 }
 
 // Sum split-K partials in a fixed order and apply the epilogue.
@@ -571,6 +422,154 @@ hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st, bool reduce) 
   return hipGetLastError();
 }
 
+// Prefill-sized M: 256 x BN macro tiles on the 32x32x16 bf16 MFMA, fed by the
+// LDS DMA path.  A stage is 32 of K: the 16 A blocks (16 rows x 32 columns of
+// the activations, 1 KB each, in the MFMA operand order [k/8][row][8]) and the
+// BN/16 packed weight tiles, DMA'd by the four wavefronts together; NSTG stages
+// in flight in distinct LDS arrays (see the streaming kernel for the wait and
+// barrier discipline).  Wavefront (wm, wn) owns rows wm*128.. and columns
+// wn*BN/2.. as 4 x BN/64 tiles of 32 x 32.  SwiGLU groups logical columns by 64
+// (32 gate rows, then the 32 matching up rows) so one lane holds both.
+template <int BN, int NSTG, int EPI>
+__global__ __launch_bounds__(256) void gemm_big_dma_kernel(GemmArgs a) {
+  constexpr int BM = 256;
+  constexpr int TM = 4, TN = BN / 64;
+  constexpr int AB = BM / 16, BB = BN / 16;                 // 1 KB blocks per stage
+  constexpr int STAGE = (AB + BB) * 512;
+  constexpr int A_W = AB / 4, B_W = BB / 4;                  // blocks each wavefront moves per stage
+  constexpr int PER_W = A_W + B_W;                           // DMA instructions per wavefront per stage
+  constexpr bool SW = (EPI == EPI_SWIGLU);
+  static_assert(AB % 4 == 0 && BB % 4 == 0 && NSTG >= 2 && NSTG <= 4, "stage layout");
+  __shared__ __attribute__((aligned(1024))) bf16_t L0[STAGE], L1[STAGE], L2[NSTG > 2 ? STAGE : 8],
+      L3[NSTG > 3 ? STAGE : 8];
+  auto slot = [&](auto ic) -> bf16_t* {
+    constexpr int I = decltype(ic)::value;
+    if constexpr (I == 0) return L0; else if constexpr (I == 1) return L1; else if constexpr (I == 2) return L2;
+    else return L3;
+  };
+  const int tiles_m = (a.M + BM - 1) / BM;
+  const int tiles_n = (a.N + BN - 1) / BN;
+  const int L = xcd_remap(blockIdx.x, tiles_m * tiles_n);
+  const int tn = L / tiles_m, tm = L % tiles_m;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int nst = (a.K + 31) / 32;
+
+  // this wavefront's DMA sources: A row-blocks w*A_W.. and weight tiles w*B_W.. (no
+  // per-block branches, so the compiler keeps track of which LDS array each DMA writes)
+  const bf16_t* asrc[A_W];
+  const bf16_t* bsrc[B_W];
+#pragma unroll
+  for (int u = 0; u < A_W; ++u) asrc[u] = a.A + (size_t)min(m0 + (w * A_W + u) * 16 + (lane & 15), a.M - 1) * a.lda;
+#pragma unroll
+  for (int v = 0; v < B_W; ++v) {
+    const int c = min(n0 + (w * B_W + v) * 16, a.N - 1) & ~15;  // logical column of the tile (past N: repeat)
+    const bf16_t* mat = a.B;
+    int row = c;
+    if (SW) {
+      const int g = c >> 6, w64 = c & 63;
+      mat = (w64 < 32) ? a.B : a.B2;
+      row = g * 32 + (w64 & 31);
+    }
+    bsrc[v] = mat + (size_t)(row >> 4) * a.kt * 512 + lane * 8;
+  }
+  auto issue = [&](int s, bf16_t* base) {
+    const int st = min(s, nst - 1);                          // past the end: reload the last stage (unused)
+    const int ka = min(st * 32 + (lane >> 4) * 8, a.K - 8);  // stays in the row; the weights are zero past K
+#pragma unroll
+    for (int u = 0; u < A_W; ++u) dma16(asrc[u] + ka, base + (w * A_W + u) * 512);
+#pragma unroll
+    for (int v = 0; v < B_W; ++v) dma16(bsrc[v] + (size_t)st * 512, base + (AB + w * B_W + v) * 512);
+  };
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  // 32x32x16 operand of lane l: row (or column) l % 32 of the tile, k chunk l / 32 of the
+  // 16-wide slice.  The offsets are precomputed so that every LDS read is its array plus
+  // one offset: the compiler must still see which array a read comes from, or it waits
+  // for every DMA in flight.
+  const int lo = ((lane & 31) >> 4) * 512 + (lane >> 5) * 128 + (lane & 15) * 8;
+  int a_off[TM], b_off[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) a_off[i] = (wm * 8 + i * 2) * 512 + lo;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) b_off[j] = (AB + wn * (BN / 32) + j * 2) * 512 + lo;
+  auto compute = [&](const bf16_t* base) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      bf16x8 fb[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) fb[j] = as_bf16x8(*reinterpret_cast<const uint4*>(base + b_off[j] + q * 256));
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const bf16x8 fa = as_bf16x8(*reinterpret_cast<const uint4*>(base + a_off[i] + q * 256));
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(fa, fb[j], acc[i][j]);
+      }
+    }
+  };
+
+  static_for<NSTG - 1>([&](auto ic) { issue(decltype(ic)::value, slot(ic)); });
+  int s0 = 0;
+  for (; s0 + NSTG <= nst; s0 += NSTG) {
+    static_for<NSTG>([&](auto ic) {
+      constexpr int J = decltype(ic)::value;
+      wait_vmcnt<(NSTG - 2) * PER_W>();
+      __builtin_amdgcn_s_barrier();
+      issue(s0 + J + NSTG - 1, slot(std::integral_constant<int, (J + NSTG - 1) % NSTG>{}));
+      compute(slot(ic));
+    });
+  }
+  wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  static_for<NSTG - 1>([&](auto ic) {
+    if (s0 + decltype(ic)::value < nst) compute(slot(ic));
+  });
+
+  // lane holds column l % 32 and rows 8*(r/4) + 4*(lane/32) + r%4 of each 32x32 tile
+  const int l32 = lane & 31, rq = (lane >> 5) * 4;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m0 + wm * 128 + i * 32 + (r >> 2) * 8 + rq + (r & 3);
+      if (row >= a.M) continue;
+      if (SW) {
+#pragma unroll
+        for (int j = 0; j < TN; j += 2) {
+          const int lc = n0 + wn * (BN / 2) + j * 32;   // first (gate) logical column of the 64-group
+          if (lc >= a.N) continue;
+          const float g = acc[i][j][r], u = acc[i][j + 1][r];
+          reinterpret_cast<bf16_t*>(a.C)[(size_t)row * a.ldc + (lc >> 6) * 32 + l32] =
+              f2bf(g / (1.f + __expf(-g)) * u);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int col = n0 + wn * (BN / 2) + j * 32 + l32;
+          if (col >= a.N) continue;
+          const size_t o = (size_t)row * a.ldc + col;
+          if (EPI == EPI_BF16) reinterpret_cast<bf16_t*>(a.C)[o] = f2bf(acc[i][j][r]);
+          else if (EPI == EPI_RESID) reinterpret_cast<float*>(a.C)[o] += acc[i][j][r];
+          else reinterpret_cast<float*>(a.C)[o] = acc[i][j][r];
+        }
+      }
+    }
+  }
+}
+
+template <int BN, int NSTG, int EPI>
+hipError_t launch_big_dma(const GemmArgs& a, hipStream_t st) {
+  const int nb = ((a.M + 255) / 256) * ((a.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_big_dma_kernel<BN, NSTG, EPI>), dim3(nb), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
 template <int BM, int BN, int BK, int NS, int EPI>
 hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st, bool reduce = true) {
   const int nb = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
@@ -592,9 +591,12 @@ hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st, bool reduce
   if (p.stream)
     return p.bm <= 32 ? launch_stream<2, EPI>(a, p.splits, st, reduce) : launch_stream<4, EPI>(a, p.splits, st, reduce);
   if (p.bm == 256) {
-    // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0
+    // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0 and BN % 128 == 0
     if (EPI == EPI_SWIGLU && a.N % 64 != 0) return launch_tile<128, 128, 64, 2, EPI>(a, 1, st);
-    return p.bn == 256 ? launch_big<256, EPI>(a, st) : launch_big<128, EPI>(a, st);
+    if (p.bn == 128) return launch_big_dma<128, 4, EPI>(a, st);
+    if constexpr (EPI != EPI_SWIGLU)
+      if (p.bn == 192) return launch_big_dma<192, 4, EPI>(a, st);
+    return launch_big_dma<256, 4, EPI>(a, st);
   }
   if (p.bm == 128) return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce);
   return launch_tile<64, 64, 128, 2, EPI>(a, p.splits, st, reduce);
@@ -629,7 +631,7 @@ hipError_t pack_weight_launch(const uint16_t* W, int N, int K, uint16_t* out, hi
 // Kernel, tile and split-K choice.  M <= 64 (decode): the weight-streaming
 // kernel.  64 < M <= 256: 64x64 tiles, split along K until the grid has about
 // 1024 workgroups, keeping at least 256 K-elements per split.  256 < M <= 512:
-// 128x128 tiles.  M > 512: 256x256 / 256x128 tiles.
+// 128x128 tiles.  M > 512: the LDS-DMA kernel with 256-row tiles.
 GemmPlan gemm_plan(int M, int N, int K, int max_splits) {
   GemmPlan p;
   if (M <= 64) {
@@ -645,9 +647,20 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits) {
     return p;
   }
   if (M > 512) {
-    // 256-row macro tiles; 256 columns unless that leaves fewer than ~2 tiles per CU
+    // 256-row macro tiles; the column width (128, 192 or 256) that minimises the
+    // rounds of 256 workgroups times the per-tile work, narrower tiles costing
+    // more per flop (measured: x1.2 at 128, x1.05 at 192)
     p.bm = 256;
-    p.bn = (((M + 255) / 256) * ((N + 255) / 256) >= 512) ? 256 : 128;
+    const int tm = (M + 255) / 256;
+    double best = 0;
+    for (int bn : {256, 192, 128}) {
+      const int rounds = (tm * ((N + bn - 1) / bn) + 255) / 256;
+      const double cost = rounds * bn * (bn == 256 ? 1.0 : bn == 192 ? 1.05 : 1.2);
+      if (best == 0 || cost < best - 1e-9) {
+        best = cost;
+        p.bn = bn;
+      }
+    }
     p.splits = 1;
     p.k_chunk = K;
     return p;

@@ -107,7 +107,9 @@ struct DecodeAttnArgs {
   float scale_log2;        // log2(e) / sqrt(dh)
 };
 // Split-K partials of every work item, then the log-sum-exp merge into `out`.
-hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st);
+// ev_start / ev_stop (may be null): events that record the kernel's own start and end.
+hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start = nullptr,
+                              hipEvent_t ev_stop = nullptr);
 hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st);
 
 // One prefill work item: queries [q0, q0 + nq) (chunk-local) of entry `entry`, kv-head `kvh`.

@@ -59,14 +59,15 @@ def _gemm_case(M_, N, K, epi, seed):
                                     (64, 4096, 14336), (3, 520, 1384), (16, 4096, 4096), (64, 256, 8192),
                                     (32, 136, 160), (17, 8192, 1024), (65, 4096, 4096),
                                     (256, 1024, 688), (300, 1000, 688),
-                                    (2080, 384, 512), (600, 1000, 688), (2080, 6144, 1024), (1031, 4096, 1384)])
+                                    (2080, 384, 512), (600, 1000, 688), (2080, 6144, 1024), (1031, 4096, 1384),
+                                    (2048, 4096, 256), (2080, 4096, 264), (2048, 6144, 96)])
 @pytest.mark.parametrize("epi", [hxf.EPI_BF16, hxf.EPI_RESID, hxf.EPI_F32])
 def test_gemm(M_, N, K, epi):
     _gemm_case(M_, N, K, epi, seed=M_ * 7 + N + K + epi)
 
 
 @pytest.mark.parametrize("M_,N,K", [(5, 64, 256), (64, 2 * 688, 256), (33, 2 * 688, 2048), (64, 2 * 14336, 4096),
-                                    (20, 2 * 4096, 4096), (64, 2 * 96, 8192),
+                                    (20, 2 * 4096, 4096), (64, 2 * 96, 8192), (2080, 2 * 4096, 200),
                                     (300, 2 * 1376, 512), (128, 2 * 14336, 4096), (700, 2 * 688, 256),
                                     (2080, 2 * 2080, 512)])
 def test_gemm_swiglu(M_, N, K):
