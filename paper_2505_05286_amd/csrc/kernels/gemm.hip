@@ -8,6 +8,7 @@
 //   M > 512      gemm_big_dma_kernel: 256-row tiles of 32x32x16 MFMAs fed by LDS DMA.
 // Workgroups are renumbered so that consecutive output tiles (which share a
 // weight slice) land on the same XCD and its L2.
+#include <algorithm>
 #include <utility>
 
 #include "common.hpp"
@@ -422,18 +423,17 @@ hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st, bool reduce) 
   return hipGetLastError();
 }
 
-// Prefill-sized M: 256 x BN macro tiles on the 32x32x16 bf16 MFMA, fed by the
-// LDS DMA path.  A stage is 32 of K: the 16 A blocks (16 rows x 32 columns of
-// the activations, 1 KB each, in the MFMA operand order [k/8][row][8]) and the
-// BN/16 packed weight tiles, DMA'd by the four wavefronts together; NSTG stages
-// in flight in distinct LDS arrays (see the streaming kernel for the wait and
-// barrier discipline).  Wavefront (wm, wn) owns rows wm*128.. and columns
-// wn*BN/2.. as 4 x BN/64 tiles of 32 x 32.  SwiGLU groups logical columns by 64
+// Prefill-sized M: BM x BN macro tiles on the 32x32x16 bf16 MFMA, fed by the
+// LDS DMA path.  A stage is 32 of K: the BM/16 A blocks (16 rows x 32 columns
+// of the activations, 1 KB each, in the MFMA operand order [k/8][row][8]) and
+// the BN/16 packed weight tiles, DMA'd by the four wavefronts together; NSTG
+// stages in flight in distinct LDS arrays (see the streaming kernel for the
+// wait and barrier discipline).  Wavefront (wm, wn) owns rows wm*BM/2.. and
+// columns wn*BN/2.. as BM/64 x BN/64 tiles of 32 x 32.  SwiGLU groups logical columns by 64
 // (32 gate rows, then the 32 matching up rows) so one lane holds both.
-template <int BN, int NSTG, int EPI>
-__global__ __launch_bounds__(256) void gemm_big_dma_kernel(GemmArgs a) {
-  constexpr int BM = 256;
-  constexpr int TM = 4, TN = BN / 64;
+template <int BM, int BN, int NSTG, int EPI, int OCC = 1>
+__global__ __launch_bounds__(256, OCC) void gemm_big_dma_kernel(GemmArgs a) {
+  constexpr int TM = BM / 64, TN = BN / 64;
   constexpr int AB = BM / 16, BB = BN / 16;                 // 1 KB blocks per stage
   constexpr int STAGE = (AB + BB) * 512;
   constexpr int A_W = AB / 4, B_W = BB / 4;                  // blocks each wavefront moves per stage
@@ -452,7 +452,7 @@ __global__ __launch_bounds__(256) void gemm_big_dma_kernel(GemmArgs a) {
   const int L = xcd_remap(blockIdx.x, tiles_m * tiles_n);
   const int tn = L / tiles_m, tm = L % tiles_m;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w >> 1, wn = w & 1;
   const int nst = (a.K + 31) / 32;
 
@@ -496,7 +496,7 @@ __global__ __launch_bounds__(256) void gemm_big_dma_kernel(GemmArgs a) {
   const int lo = ((lane & 31) >> 4) * 512 + (lane >> 5) * 128 + (lane & 15) * 8;
   int a_off[TM], b_off[TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) a_off[i] = (wm * 8 + i * 2) * 512 + lo;
+  for (int i = 0; i < TM; ++i) a_off[i] = (wm * (BM / 32) + i * 2) * 512 + lo;
 #pragma unroll
   for (int j = 0; j < TN; ++j) b_off[j] = (AB + wn * (BN / 32) + j * 2) * 512 + lo;
   auto compute = [&](const bf16_t* base) {
@@ -535,9 +535,38 @@ __global__ __launch_bounds__(256) void gemm_big_dma_kernel(GemmArgs a) {
   const int l32 = lane & 31, rq = (lane >> 5) * 4;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
+    if (EPI == EPI_RESID) {
+      // residual loads of RB rows first, then the adds and stores (one wait per RB rows)
+      constexpr int RB = TN > 3 ? 4 : TN > 2 ? 8 : 16;
+      float* C = reinterpret_cast<float*>(a.C);
+#pragma unroll
+      for (int r0 = 0; r0 < 16; r0 += RB) {
+        float old[RB][TN];
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+          const int rr = r0 + r;
+          const int row = min(m0 + wm * (BM / 2) + i * 32 + (rr >> 2) * 8 + rq + (rr & 3), a.M - 1);
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            old[r][j] = C[(size_t)row * a.ldc + min(n0 + wn * (BN / 2) + j * 32 + l32, a.N - 1)];
+        }
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+          const int rr = r0 + r;
+          const int row = m0 + wm * (BM / 2) + i * 32 + (rr >> 2) * 8 + rq + (rr & 3);
+          if (row >= a.M) continue;
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int col = n0 + wn * (BN / 2) + j * 32 + l32;
+            if (col < a.N) C[(size_t)row * a.ldc + col] = old[r][j] + acc[i][j][rr];
+          }
+        }
+      }
+      continue;
+    }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = m0 + wm * 128 + i * 32 + (r >> 2) * 8 + rq + (r & 3);
+      const int row = m0 + wm * (BM / 2) + i * 32 + (r >> 2) * 8 + rq + (r & 3);
       if (row >= a.M) continue;
       if (SW) {
 #pragma unroll
@@ -563,10 +592,10 @@ __global__ __launch_bounds__(256) void gemm_big_dma_kernel(GemmArgs a) {
   }
 }
 
-template <int BN, int NSTG, int EPI>
+template <int BM, int BN, int NSTG, int EPI, int OCC = 1>
 hipError_t launch_big_dma(const GemmArgs& a, hipStream_t st) {
-  const int nb = ((a.M + 255) / 256) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_big_dma_kernel<BN, NSTG, EPI>), dim3(nb), dim3(256), 0, st, a);
+  const int nb = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_big_dma_kernel<BM, BN, NSTG, EPI, OCC>), dim3(nb), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -590,13 +619,14 @@ hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st, bool reduce
   a.k_chunk = p.k_chunk;
   if (p.stream)
     return p.bm <= 32 ? launch_stream<2, EPI>(a, p.splits, st, reduce) : launch_stream<4, EPI>(a, p.splits, st, reduce);
-  if (p.bm == 256) {
-    // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0 and BN % 128 == 0
+  if (p.big) {
+    // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0 (and BN % 128 == 0)
     if (EPI == EPI_SWIGLU && a.N % 64 != 0) return launch_tile<128, 128, 64, 2, EPI>(a, 1, st);
-    if (p.bn == 128) return launch_big_dma<128, 4, EPI>(a, st);
+    if (p.bm == 128) return launch_big_dma<128, 256, 4, EPI>(a, st);
+    if (p.bn == 128) return launch_big_dma<256, 128, 4, EPI>(a, st);
     if constexpr (EPI != EPI_SWIGLU)
-      if (p.bn == 192) return launch_big_dma<192, 4, EPI>(a, st);
-    return launch_big_dma<256, 4, EPI>(a, st);
+      if (p.bn == 192) return launch_big_dma<256, 192, 4, EPI>(a, st);
+    return launch_big_dma<256, 256, 4, EPI>(a, st);
   }
   if (p.bm == 128) return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce);
   return launch_tile<64, 64, 128, 2, EPI>(a, p.splits, st, reduce);
@@ -647,20 +677,22 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits) {
     return p;
   }
   if (M > 512) {
-    // 256-row macro tiles; the column width (128, 192 or 256) that minimises the
-    // rounds of 256 workgroups times the per-tile work, narrower tiles costing
-    // more per flop (measured: x1.2 at 128, x1.05 at 192)
-    p.bm = 256;
-    const int tm = (M + 255) / 256;
+    // the tile (of 256x256, 256x192, 128x256, 256x128) minimising
+    // max(1, tiles / 256 CUs) * tile area * a per-flop factor measured on the
+    // 2048-row projections (narrower wavefront tiles read more LDS per MFMA)
+    struct Cand { int bm, bn; double f; };
+    const Cand cands[4] = {{256, 256, 1.0}, {256, 192, 1.0}, {128, 256, 1.1}, {256, 128, 1.15}};
     double best = 0;
-    for (int bn : {256, 192, 128}) {
-      const int rounds = (tm * ((N + bn - 1) / bn) + 255) / 256;
-      const double cost = rounds * bn * (bn == 256 ? 1.0 : bn == 192 ? 1.05 : 1.2);
-      if (best == 0 || cost < best - 1e-9) {
+    for (const Cand& c : cands) {
+      const double tiles = (double)((M + c.bm - 1) / c.bm) * ((N + c.bn - 1) / c.bn);
+      const double cost = std::max(1.0, tiles / 256.0) * c.bm * c.bn * c.f;
+      if (best == 0 || cost < best - 1e-6) {
         best = cost;
-        p.bn = bn;
+        p.bm = c.bm;
+        p.bn = c.bn;
       }
     }
+    p.big = true;
     p.splits = 1;
     p.k_chunk = K;
     return p;

@@ -34,6 +34,7 @@ struct GemmArgs {
 
 struct GemmPlan {
   bool stream = false;  // decode-sized M: LDS-DMA weight-streaming kernel
+  bool big = false;     // prefill-sized M: LDS-DMA 32x32x16 MFMA kernel
   int bm = 128;
   int bn = 128;
   int splits = 1;
