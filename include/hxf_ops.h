@@ -13,7 +13,9 @@
  *
  * Physical KV layout (one layer), kv-head major: K pool [Hkv][n_blocks][dh/8][16][8]
  * (element (token t, dim d) of a page at ((d/8)*16 + t)*8 + d%8), then a separate
- * V pool [Hkv][n_blocks][dh][16] (V transposed inside a page); the token at
+ * V pool [Hkv][n_blocks][dh][16] (V transposed inside a page: element (t, d) at
+ * d*16 + v_pos(t), v_pos swapping bits 2 and 3 of t, i.e. the page's tokens in
+ * groups of four in the order 0-3, 8-11, 4-7, 12-15); the token at
  * position p of a sequence with block table bt lives in slot bt[p/16]*16 + p%16.
  * `n_blocks` is the number of pages of the pool (its kv-head stride).
  */

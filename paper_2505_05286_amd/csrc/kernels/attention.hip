@@ -45,7 +45,7 @@ template <int DH>
 __device__ __forceinline__ void load_page(uint4* k, uint2* v, const uint16_t* k_pool, const uint16_t* v_pool,
                                           size_t tile, int lane) {
   const uint16_t* kp = k_pool + tile + lane * 8;
-  const uint16_t* vp = v_pool + tile + (lane & 15) * kPage + (lane >> 4) * 4;
+  const uint16_t* vp = v_pool + tile + (lane & 15) * kPage + v_pos((lane >> 4) * 4);   // tokens 4g..4g+3
 #pragma unroll
   for (int s = 0; s < DH / 32; ++s) k[s] = load_stream16(kp + s * 512);
 #pragma unroll
@@ -235,44 +235,210 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeAttnArgs a) {
   else out[0] = f2bf(acc[0] * inv);
 }
 
+// Chunked-prefill causal attention, one workgroup per (chunk, kv-head, block of
+// 256/G queries): the 256 (query, head) pairs of the block are the columns of
+//   S^T[32 keys x 32 pairs] = K[32 x dh] . Q^T[dh x 32]       (v_mfma_f32_32x32x16_bf16)
+//   O^T[32 dims x 32 pairs] += V^T[32 x 32 keys] . P^T[32 x 32]
+// (64 pairs per wavefront, two 32-pair tiles).  Tiles of 32 keys (two pages)
+// of K and V are moved into LDS by the DMA path, four tiles in flight, and
+// shared by the four wavefronts.  A lane of the S^T accumulator holds keys
+// 8m + 4h + i (h = lane / 32) of its pair; taken in the order m = 2s, 2s + 1
+// these are the 8 keys of the P^T operand for the 16-key step s (page s of the
+// tile); the V pool stores each page row with its tokens in that order (see
+// v_pos), so the V^T operand of a lane is one contiguous 16-byte LDS read.  Softmax is
+// online in log2 units, one cross-lane exchange (xor 32) per tile for the max.
 template <int DH>
-__global__ __launch_bounds__(256) void prefill_attn_kernel(PrefillAttnArgs a) {
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+__global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
+  constexpr int KS = DH / 16;                  // 16-dim steps of QK^T
+  constexpr int DT = DH / 32;                  // 32-dim tiles of O^T
+  constexpr int KT = 32 * DH;                  // elements of a K (or V) tile of 32 keys
+  constexpr int STAGE = 2 * KT;                // K tile then V tile
+  constexpr int K_W = KT / 512 / 4;            // 16-byte DMA instructions per wavefront for K
+  constexpr int V_W = KT / 512 / 4;            // and for V
+  constexpr int PER_W = K_W + V_W;
+  __shared__ __attribute__((aligned(1024))) bf16_t L0[STAGE], L1[STAGE], L2[STAGE], L3[STAGE];
+  auto slot = [&](auto ic) -> bf16_t* {
+    constexpr int I = decltype(ic)::value % 4;
+    if constexpr (I == 0) return L0; else if constexpr (I == 1) return L1; else if constexpr (I == 2) return L2;
+    else return L3;
+  };
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const PrefillItem it = a.items[blockIdx.x];
   const int G = a.Hq / a.Hkv;
-  const int qpw = 16 / G;                       // queries per wavefront
-  const int col = lane & 15;
-  const int qi = col / G, j = col % G;
-  const int wq0 = it.q0 + wid * qpw;            // first query of this wave
-  const int wq_end = min(it.q0 + it.nq, wq0 + qpw);
-  if (wq0 >= wq_end) return;
-  const int qloc = wq0 + qi;
-  const bool ok = (col < qpw * G) && (qloc < wq_end);
+  const int npairs = it.nq * G;
   const int pos0 = a.pos0[it.entry];
-  const int row = a.row0[it.entry] + (ok ? qloc : wq0);
-  const int head = it.kvh * G + j;
-  bf16x8 qf[DH / 32];
-  load_q<DH>(qf, a.q + (size_t)row * a.q_stride + head * DH, ok, lane);
-  const int lim = pos0 + (ok ? qloc : wq0);
-  const int t_end = pos0 + wq_end;              // last query position + 1
-  AttnState<DH> S;
-  attn_range<DH, true>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)it.entry * a.bt_stride, a.n_blocks, it.kvh, 0, t_end,
-                       lim, a.scale_log2, lane);
-  if (!ok) return;
-  const float inv = 1.f / S.l;
-  const int rq = lane >> 4;
-  uint16_t* out = a.out + (size_t)row * a.out_stride + head * DH;
+  const int kend = pos0 + it.q0 + it.nq;       // keys [0, kend) are visible to some pair
+  const int ntiles = (kend + 31) / 32;
+  const int last_page = (kend - 1) / kPage;
+  const int32_t* bt = a.bt + (size_t)it.entry * a.bt_stride;
+  const int h = lane >> 5;
+
+  // this lane's two pairs (columns lane % 32 of the wavefront's two pair tiles)
+  int qpos[2];
+  bf16x8 qf[2][KS];
 #pragma unroll
-  for (int n = 0; n < DH / 16; ++n) {
-    const uint2 v = make_uint2(pack_bf2(S.acc[n][0] * inv, S.acc[n][1] * inv),
-                               pack_bf2(S.acc[n][2] * inv, S.acc[n][3] * inv));
-    *reinterpret_cast<uint2*>(out + n * 16 + rq * 4) = v;
+  for (int pt = 0; pt < 2; ++pt) {
+    const int p = w * 64 + pt * 32 + (lane & 31);
+    const bool ok = p < npairs;
+    const int qi = ok ? p / G : 0, hj = ok ? p % G : 0;
+    qpos[pt] = ok ? pos0 + it.q0 + qi : -1;     // -1: every key masked
+    const uint16_t* qrow = a.q + (size_t)(a.row0[it.entry] + it.q0 + qi) * a.q_stride + (it.kvh * G + hj) * DH;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const uint4 v = ok ? *reinterpret_cast<const uint4*>(qrow + ks * 16 + h * 8) : make_uint4(0, 0, 0, 0);
+      qf[pt][ks] = as_bf16x8(v);
+    }
+  }
+
+  // DMA of key tile t into a stage: the two K pages, then the two V pages, as stored
+  auto issue = [&](int t, bf16_t* base) __attribute__((always_inline)) {
+    const int tt = min(t, ntiles - 1);
+#pragma unroll
+    for (int u = 0; u < K_W; ++u) {
+      const int blk = w * K_W + u;               // 1 KB block of the K tile
+      const int pg = blk / (KT / 1024);          // page of the tile (each page is KT / 2 elements)
+      const int page = min(tt * 2 + pg, last_page);
+      const size_t tile = kv_tile(it.kvh, a.n_blocks, bt[page], DH);
+      dma16(a.k_pool + tile + (blk % (KT / 1024)) * 512 + lane * 8, base + blk * 512);
+    }
+#pragma unroll
+    for (int u = 0; u < V_W; ++u) {
+      const int blk = w * V_W + u;               // 1 KB block of the V tile
+      const int pg = blk / (KT / 1024);
+      const int page = min(tt * 2 + pg, last_page);
+      const size_t tile = kv_tile(it.kvh, a.n_blocks, bt[page], DH);
+      dma16(a.v_pool + tile + (blk % (KT / 1024)) * 512 + lane * 8, base + KT + blk * 512);
+    }
+  };
+
+  f32x16 o[2][DT];
+#pragma unroll
+  for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[pt][dt][e] = 0.f;
+  float m[2] = {kNegInf, kNegInf}, l[2] = {0.f, 0.f};
+  // operand offsets inside a stage: K for key lane%32 (page (lane%32)/16), dims chunk ks*2 + h;
+  // V^T for dim dt*32 + lane%32, page s, positions 8h..8h+7
+  const int k_off = ((lane & 31) >> 4) * (KT / 2) + (lane & 15) * 8 + h * 128;
+  const int v_off = KT + (lane & 31) * 16 + h * 8;
+
+  auto compute = [&](const bf16_t* base, int t) __attribute__((always_inline)) {
+    f32x16 s[2];
+#pragma unroll
+    for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[pt][e] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 kf = as_bf16x8(*reinterpret_cast<const uint4*>(base + k_off + ks * 256));
+#pragma unroll
+      for (int pt = 0; pt < 2; ++pt) s[pt] = mfma32x32x16(kf, qf[pt][ks], s[pt]);
+    }
+    const int k0 = t * 32;
+    const bool edge = (k0 + 32 > kend) || (k0 + 31 > pos0 + it.q0);   // wavefront-uniform: a mask is needed
+    bf16x8 pf[2][2];
+#pragma unroll
+    for (int pt = 0; pt < 2; ++pt) {
+      float x[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        x[r] = s[pt][r] * a.scale_log2;
+        if (edge) {
+          const int key = k0 + (r >> 2) * 8 + h * 4 + (r & 3);
+          if (key > qpos[pt] || key >= kend) x[r] = kNegInf;
+        }
+      }
+      float mx = x[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, x[r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      const float m_new = fmaxf(m[pt], mx);
+      const bool live = m_new != kNegInf;
+      const float alpha = live ? exp2f(m[pt] - m_new) : 1.f;
+      float ps = 0.f;
+      float pv[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        pv[r] = live ? exp2f(x[r] - m_new) : 0.f;
+        ps += pv[r];
+      }
+      m[pt] = m_new;
+      l[pt] = l[pt] * alpha + ps;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[pt][dt][e] *= alpha;
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        bf16x8 v;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = (__bf16)pv[st * 8 + j];
+        pf[pt][st] = v;
+      }
+    }
+    // V^T . P^T; past the end of the context the V entries are zeroed (garbage may be NaN)
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      const int tok0 = k0 + st * 16 + h * 4;      // keys of this lane's k slots: tok0 + 0..3, tok0 + 8..11
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        uint4 vv = *reinterpret_cast<const uint4*>(base + v_off + (st * DH + dt * 32) * 16);
+        if (k0 + 32 > kend) {
+          const uint2 lo = keep_mask(kend - tok0), hi = keep_mask(kend - tok0 - 8);
+          vv.x &= lo.x; vv.y &= lo.y; vv.z &= hi.x; vv.w &= hi.y;
+        }
+#pragma unroll
+        for (int pt = 0; pt < 2; ++pt) o[pt][dt] = mfma32x32x16(as_bf16x8(vv), pf[pt][st], o[pt][dt]);
+      }
+    }
+  };
+
+  static_for<3>([&](auto ic) { issue(decltype(ic)::value, slot(ic)); });
+  int t0 = 0;
+  for (; t0 + 4 <= ntiles; t0 += 4) {
+    static_for<4>([&](auto ic) {
+      constexpr int J = decltype(ic)::value;
+      wait_vmcnt<2 * PER_W>();
+      __builtin_amdgcn_s_barrier();
+      issue(t0 + J + 3, slot(std::integral_constant<int, J + 3>{}));
+      compute(slot(ic), t0 + J);
+    });
+  }
+  wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  static_for<3>([&](auto ic) {
+    constexpr int J = decltype(ic)::value;
+    if (t0 + J < ntiles) compute(slot(ic), t0 + J);
+  });
+
+  // O^T lane holds pair lane % 32 and dims dt*32 + 8*(r/4) + 4h + r%4
+  float lt[2];
+#pragma unroll
+  for (int pt = 0; pt < 2; ++pt) lt[pt] = l[pt] + __shfl_xor(l[pt], 32, kWave);
+#pragma unroll
+  for (int pt = 0; pt < 2; ++pt) {
+    const int p = w * 64 + pt * 32 + (lane & 31);
+    if (p >= npairs) continue;
+    const float inv = 1.f / lt[pt];
+    const int qi = p / G, hj = p % G;
+    uint16_t* out = a.out + (size_t)(a.row0[it.entry] + it.q0 + qi) * a.out_stride + (it.kvh * G + hj) * DH;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d = dt * 32 + g4 * 8 + h * 4;
+        *reinterpret_cast<uint2*>(out + d) =
+            make_uint2(pack_bf2(o[pt][dt][g4 * 4] * inv, o[pt][dt][g4 * 4 + 1] * inv),
+                       pack_bf2(o[pt][dt][g4 * 4 + 2] * inv, o[pt][dt][g4 * 4 + 3] * inv));
+      }
   }
 }
 
 }  // namespace
 
-int prefill_queries_per_item(int group) { return 4 * (16 / group); }
+int prefill_queries_per_item(int group) { return 256 / group; }
 
 hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (a.n_items <= 0) return hipSuccess;
@@ -297,8 +463,8 @@ hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st) {
 
 hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st) {
   if (a.n_items <= 0) return hipSuccess;
-  if (a.dh == 128) hipLaunchKernelGGL(prefill_attn_kernel<128>, dim3(a.n_items), dim3(256), 0, st, a);
-  else if (a.dh == 64) hipLaunchKernelGGL(prefill_attn_kernel<64>, dim3(a.n_items), dim3(256), 0, st, a);
+  if (a.dh == 128) hipLaunchKernelGGL(prefill_flash_kernel<128>, dim3(a.n_items), dim3(256), 0, st, a);
+  else if (a.dh == 64) hipLaunchKernelGGL(prefill_flash_kernel<64>, dim3(a.n_items), dim3(256), 0, st, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

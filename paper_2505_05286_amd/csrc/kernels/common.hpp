@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 namespace hxf {
 
 typedef uint16_t bf16_t;   // bf16 storage (upper half of an IEEE float)
@@ -66,5 +68,29 @@ __device__ __forceinline__ T wave_max(T v) {
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
   return v;
 }
+
+// ---- LDS DMA (global_load_lds_dwordx4): each lane moves 16 bytes from its own
+// global address to lds_block + 16 * lane, without passing through registers;
+// completion is counted by vmcnt.
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* global_ptr_t;
+
+__device__ __forceinline__ void dma16(const void* g, void* lds_block) {
+  __builtin_amdgcn_global_load_lds((global_ptr_t)g, (lds_ptr_t)lds_block, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+template <class F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) { static_for_impl(f, std::make_integer_sequence<int, N>{}); }
 
 }  // namespace hxf

@@ -254,27 +254,6 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int S) {
 // NSTG so the compiler can see that the LDS reads of a stage do not alias the
 // DMAs in flight (otherwise it waits for all of them).  Split K (grid.y)
 // writes fp32 partials; a reduction kernel finishes them.
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-typedef __attribute__((address_space(1))) void* global_ptr_t;
-
-__device__ __forceinline__ void dma16(const void* g, void* lds_block) {
-  __builtin_amdgcn_global_load_lds((global_ptr_t)g, (lds_ptr_t)lds_block, 16, 0, 0);
-}
-
-// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-template <class F, int... Is>
-__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
-  (f(std::integral_constant<int, Is>{}), ...);
-}
-template <int N, class F>
-__device__ __forceinline__ void static_for(F&& f) { static_for_impl(f, std::make_integer_sequence<int, N>{}); }
-
 constexpr int ST_WV = 4, ST_NTW = 2, ST_NSTG = 3;   // 4 wavefronts x 2 tiles = 128 columns per workgroup
 
 template <int MT, int EPI, bool SPLIT>

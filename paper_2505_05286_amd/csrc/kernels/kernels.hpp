@@ -9,13 +9,17 @@ namespace hxf {
 // Physical KV layout (per layer; K pool then V pool), kv-head major:
 //   K: [Hkv][n_blocks][dh/8][16 tokens][8]  (8-dimension chunks of the 16 tokens
 //      side by side: the order in which a wavefront feeds them to the MFMA)
-//   V: [Hkv][n_blocks][dh][16 tokens]       (a dimension's 16 tokens contiguous)
+//   V: [Hkv][n_blocks][dh][16 positions]    (a dimension's 16 tokens contiguous, token t
+//      at position v_pos(t): groups of four tokens in the order 0-3, 8-11, 4-7, 12-15,
+//      the key order of the 32x32x16 MFMA's P operand in the prefill kernel)
 // so one (page, kv-head) is one contiguous 16*dh*2-byte tile in each pool, and
 // the pages of one kv-head of a sequence allocated together are contiguous.
 constexpr int kPage = 16;
 __host__ __device__ inline size_t kv_tile(int kvh, int64_t n_blocks, int blk, int dh) {
   return ((size_t)kvh * n_blocks + blk) * kPage * dh;
 }
+// Position of token t (0..15) inside a V page row: bits 2 and 3 swapped.
+__host__ __device__ inline int v_pos(int t) { return (t & 3) | ((t >> 1) & 4) | ((t << 1) & 8); }
 
 // ------------------------------------------------------------------ GEMM
 enum { EPI_BF16 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3 };

@@ -48,8 +48,8 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(uint16_t* qkv, const float*
   const int blk = s / kPage, off = s % kPage;
   if (h >= Hq + Hkv) {                                     // v: no rotation
     uint16_t* vp = v_pool + kv_tile(h - Hq - Hkv, n_blocks, blk, dh);
-    vp[i * kPage + off] = a;
-    vp[(i + half) * kPage + off] = b;
+    vp[i * kPage + v_pos(off)] = a;
+    vp[(i + half) * kPage + v_pos(off)] = b;
     return;
   }
   const float x1 = bf2f(a), x2 = bf2f(b);
@@ -75,7 +75,7 @@ __global__ __launch_bounds__(256) void kv_scatter_kernel(const uint16_t* k, cons
   for (int j = threadIdx.x; j < Hkv * dh; j += 256) {
     const int kh = j / dh, d = j % dh;
     k_pool[kv_tile(kh, n_blocks, blk, dh) + k_offset(d, off)] = k[(size_t)t * Hkv * dh + j];
-    v_pool[kv_tile(kh, n_blocks, blk, dh) + d * kPage + off] = v[(size_t)t * Hkv * dh + j];
+    v_pool[kv_tile(kh, n_blocks, blk, dh) + d * kPage + v_pos(off)] = v[(size_t)t * Hkv * dh + j];
   }
 }
 

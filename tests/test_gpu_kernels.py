@@ -129,10 +129,14 @@ def _make_pools(nb, hkv, dh):
     return kp, vp
 
 
+# token t of a V page row is stored at position t with bits 2 and 3 swapped
+V_POS = np.array([(t & 3) | ((t >> 1) & 4) | ((t << 1) & 8) for t in range(16)])
+
+
 def _logical_pool(kp, vp, nb, hkv, dh):
     """Read the physical pools back into the oracle's logical [nb, 16, Hkv, dh] layout."""
     k = host_f64(kp).reshape(hkv, nb, dh // 8, 16, 8).transpose(1, 3, 0, 2, 4).reshape(nb, 16, hkv, dh)
-    v = host_f64(vp).reshape(hkv, nb, dh, 16).transpose(1, 3, 0, 2)
+    v = host_f64(vp).reshape(hkv, nb, dh, 16)[..., V_POS].transpose(1, 3, 0, 2)
     return k, v
 
 
