@@ -247,7 +247,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeAttnArgs a) {
 // tile); the V pool stores each page row with its tokens in that order (see
 // v_pos), so the V^T operand of a lane is one contiguous 16-byte LDS read.  Softmax is
 // online in log2 units, one cross-lane exchange (xor 32) per tile for the max.
-template <int DH>
+template <int DH, int PT>
 __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   constexpr int KS = DH / 16;                  // 16-dim steps of QK^T
   constexpr int DT = DH / 32;                  // 32-dim tiles of O^T
@@ -274,11 +274,11 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   const int h = lane >> 5;
 
   // this lane's two pairs (columns lane % 32 of the wavefront's two pair tiles)
-  int qpos[2];
-  bf16x8 qf[2][KS];
+  int qpos[PT];
+  bf16x8 qf[PT][KS];
 #pragma unroll
-  for (int pt = 0; pt < 2; ++pt) {
-    const int p = w * 64 + pt * 32 + (lane & 31);
+  for (int pt = 0; pt < PT; ++pt) {
+    const int p = (w * PT + pt) * 32 + (lane & 31);
     const bool ok = p < npairs;
     const int qi = ok ? p / G : 0, hj = ok ? p % G : 0;
     qpos[pt] = ok ? pos0 + it.q0 + qi : -1;     // -1: every key masked
@@ -311,65 +311,87 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
     }
   };
 
-  f32x16 o[2][DT];
+  f32x16 o[PT][DT];
 #pragma unroll
-  for (int pt = 0; pt < 2; ++pt)
+  for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) o[pt][dt][e] = 0.f;
-  float m[2] = {kNegInf, kNegInf}, l[2] = {0.f, 0.f};
+  // running maxima start finite, so that fully masked pairs keep zero weights, never NaN
+  float m[PT], l[PT];
+#pragma unroll
+  for (int pt = 0; pt < PT; ++pt) {
+    m[pt] = -1e30f;
+    l[pt] = 0.f;
+  }
   // operand offsets inside a stage: K for key lane%32 (page (lane%32)/16), dims chunk ks*2 + h;
   // V^T for dim dt*32 + lane%32, page s, positions 8h..8h+7
   const int k_off = ((lane & 31) >> 4) * (KT / 2) + (lane & 15) * 8 + h * 128;
   const int v_off = KT + (lane & 31) * 16 + h * 8;
 
   auto compute = [&](const bf16_t* base, int t) __attribute__((always_inline)) {
-    f32x16 s[2];
+    f32x16 s[PT];
 #pragma unroll
-    for (int pt = 0; pt < 2; ++pt)
+    for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[pt][e] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const bf16x8 kf = as_bf16x8(*reinterpret_cast<const uint4*>(base + k_off + ks * 256));
 #pragma unroll
-      for (int pt = 0; pt < 2; ++pt) s[pt] = mfma32x32x16(kf, qf[pt][ks], s[pt]);
+      for (int pt = 0; pt < PT; ++pt) s[pt] = mfma32x32x16(kf, qf[pt][ks], s[pt]);
     }
     const int k0 = t * 32;
     const bool edge = (k0 + 32 > kend) || (k0 + 31 > pos0 + it.q0);   // wavefront-uniform: a mask is needed
-    bf16x8 pf[2][2];
+    if (edge) {
 #pragma unroll
-    for (int pt = 0; pt < 2; ++pt) {
-      float x[16];
+      for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        x[r] = s[pt][r] * a.scale_log2;
-        if (edge) {
+        for (int r = 0; r < 16; ++r) {
           const int key = k0 + (r >> 2) * 8 + h * 4 + (r & 3);
-          if (key > qpos[pt] || key >= kend) x[r] = kNegInf;
+          if (key > qpos[pt] || key >= kend) s[pt][r] = kNegInf;
         }
-      }
-      float mx = x[0];
+    }
+    // raw-score maxima (the scale is positive), then one wavefront-wide decision for
+    // both pair tiles: the reference max only moves when a score exceeds it by more
+    // than 2^8 (the exponentials then stay below 256, harmless in fp32 and bf16)
+    float mx[PT];
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, x[r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-      const float m_new = fmaxf(m[pt], mx);
-      const bool live = m_new != kNegInf;
-      const float alpha = live ? exp2f(m[pt] - m_new) : 1.f;
+    for (int pt = 0; pt < PT; ++pt) {
+      float v = s[pt][0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) v = fmaxf(v, s[pt][r]);
+      v = fmaxf(v, __shfl_xor(v, 32, kWave));
+      mx[pt] = v * a.scale_log2;
+    }
+    bool grow = false;
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt) grow = grow || mx[pt] > m[pt] + 8.f;
+    if (__any(grow)) {
+#pragma unroll
+      for (int pt = 0; pt < PT; ++pt) {
+        const float m_new = fmaxf(m[pt], mx[pt]);
+        const float alpha = __builtin_amdgcn_exp2f(m[pt] - m_new);
+        m[pt] = m_new;
+        l[pt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) o[pt][dt][e] *= alpha;
+      }
+    }
+    bf16x8 pf[PT][2];
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt) {
       float ps = 0.f;
       float pv[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        pv[r] = live ? exp2f(x[r] - m_new) : 0.f;
+        pv[r] = __builtin_amdgcn_exp2f(fmaf(s[pt][r], a.scale_log2, -m[pt]));   // masked: exp2(-inf) = 0
         ps += pv[r];
       }
-      m[pt] = m_new;
-      l[pt] = l[pt] * alpha + ps;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[pt][dt][e] *= alpha;
+      l[pt] += ps;
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
         bf16x8 v;
@@ -390,7 +412,7 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
           vv.x &= lo.x; vv.y &= lo.y; vv.z &= hi.x; vv.w &= hi.y;
         }
 #pragma unroll
-        for (int pt = 0; pt < 2; ++pt) o[pt][dt] = mfma32x32x16(as_bf16x8(vv), pf[pt][st], o[pt][dt]);
+        for (int pt = 0; pt < PT; ++pt) o[pt][dt] = mfma32x32x16(as_bf16x8(vv), pf[pt][st], o[pt][dt]);
       }
     }
   };
@@ -414,12 +436,12 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   });
 
   // O^T lane holds pair lane % 32 and dims dt*32 + 8*(r/4) + 4h + r%4
-  float lt[2];
+  float lt[PT];
 #pragma unroll
-  for (int pt = 0; pt < 2; ++pt) lt[pt] = l[pt] + __shfl_xor(l[pt], 32, kWave);
+  for (int pt = 0; pt < PT; ++pt) lt[pt] = l[pt] + __shfl_xor(l[pt], 32, kWave);
 #pragma unroll
-  for (int pt = 0; pt < 2; ++pt) {
-    const int p = w * 64 + pt * 32 + (lane & 31);
+  for (int pt = 0; pt < PT; ++pt) {
+    const int p = (w * PT + pt) * 32 + (lane & 31);
     if (p >= npairs) continue;
     const float inv = 1.f / lt[pt];
     const int qi = p / G, hj = p % G;
@@ -438,7 +460,10 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
 
 }  // namespace
 
-int prefill_queries_per_item(int group) { return 256 / group; }
+// pair tiles of 32 (query, head) pairs per wavefront in the prefill kernel
+constexpr int kPrefillPT = 1;
+
+int prefill_queries_per_item(int group) { return 4 * 32 * kPrefillPT / group; }
 
 hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (a.n_items <= 0) return hipSuccess;
@@ -463,8 +488,8 @@ hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st) {
 
 hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st) {
   if (a.n_items <= 0) return hipSuccess;
-  if (a.dh == 128) hipLaunchKernelGGL(prefill_flash_kernel<128>, dim3(a.n_items), dim3(256), 0, st, a);
-  else if (a.dh == 64) hipLaunchKernelGGL(prefill_flash_kernel<64>, dim3(a.n_items), dim3(256), 0, st, a);
+  if (a.dh == 128) hipLaunchKernelGGL((prefill_flash_kernel<128, kPrefillPT>), dim3(a.n_items), dim3(256), 0, st, a);
+  else if (a.dh == 64) hipLaunchKernelGGL((prefill_flash_kernel<64, kPrefillPT>), dim3(a.n_items), dim3(256), 0, st, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
