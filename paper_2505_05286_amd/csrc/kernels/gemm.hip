@@ -596,19 +596,22 @@ hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st, bool reduce = t
 template <int EPI>
 hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st, bool reduce) {
   a.k_chunk = p.k_chunk;
-  if (p.stream)
-    return p.bm <= 32 ? launch_stream<2, EPI>(a, p.splits, st, reduce) : launch_stream<4, EPI>(a, p.splits, st, reduce);
+  if (p.stream) {
+    if (p.bm <= 32) return launch_stream<2, EPI>(a, p.splits, st, reduce);
+    if (p.bm <= 64) return launch_stream<4, EPI>(a, p.splits, st, reduce);
+    if (p.bm <= 128) return launch_stream<8, EPI>(a, p.splits, st, reduce);
+    return launch_stream<16, EPI>(a, p.splits, st, reduce);
+  }
   if (p.big) {
     // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0 (and BN % 128 == 0)
     if (EPI == EPI_SWIGLU && a.N % 64 != 0) return launch_tile<128, 128, 64, 2, EPI>(a, 1, st);
-    if (p.bm == 128) return launch_big_dma<128, 256, 4, EPI>(a, st);
+    if (p.bm == 128) return p.bn == 128 ? launch_big_dma<128, 128, 4, EPI>(a, st) : launch_big_dma<128, 256, 4, EPI>(a, st);
     if (p.bn == 128) return launch_big_dma<256, 128, 4, EPI>(a, st);
     if constexpr (EPI != EPI_SWIGLU)
       if (p.bn == 192) return launch_big_dma<256, 192, 4, EPI>(a, st);
     return launch_big_dma<256, 256, 4, EPI>(a, st);
   }
-  if (p.bm == 128) return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce);
-  return launch_tile<64, 64, 128, 2, EPI>(a, p.splits, st, reduce);
+  return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce);
 }
 
 // One 16-byte chunk of the packed layout per thread: chunk q is tile q / 64 and,
@@ -637,30 +640,17 @@ hipError_t pack_weight_launch(const uint16_t* W, int N, int K, uint16_t* out, hi
   return hipGetLastError();
 }
 
-// Kernel, tile and split-K choice.  M <= 64 (decode): the weight-streaming
-// kernel.  64 < M <= 256: 64x64 tiles, split along K until the grid has about
-// 1024 workgroups, keeping at least 256 K-elements per split.  256 < M <= 512:
-// 128x128 tiles.  M > 512: the LDS-DMA kernel with 256-row tiles.
+// Kernel, tile and split-K choice.  M <= 256: the weight-streaming kernel, except
+// for wide outputs (N >= 16384) above 64 rows, which take the big-tile kernel as
+// every M > 512 does.  256 < M <= 512: 128x128 tiles of the LDS-staged kernel.
 GemmPlan gemm_plan(int M, int N, int K, int max_splits) {
   GemmPlan p;
-  if (M <= 64) {
-    // weight streaming: 128 columns per workgroup; split K in powers of two while the
-    // grid stays within one workgroup per CU and every split keeps >= 512 of K
-    p.stream = true;
-    p.bm = M <= 32 ? 32 : 64;
-    const int tiles = (N + 127) / 128;
-    int s = 1;
-    while (s * 2 <= max_splits && tiles * s * 2 <= 256 && K / (s * 2) >= 512) s *= 2;
-    p.k_chunk = (((K + s - 1) / s) + 63) / 64 * 64;
-    p.splits = (K + p.k_chunk - 1) / p.k_chunk;
-    return p;
-  }
-  if (M > 512) {
-    // the tile (of 256x256, 256x192, 128x256, 256x128) minimising
-    // max(1, tiles / 256 CUs) * tile area * a per-flop factor measured on the
-    // 2048-row projections (narrower wavefront tiles read more LDS per MFMA)
+  // LDS-DMA big tiles: the candidate minimising max(1, tiles / 256 CUs) * tile area * a
+  // per-flop factor measured on the projections (narrower wavefront tiles read more LDS
+  // per MFMA)
+  auto big = [&]() {
     struct Cand { int bm, bn; double f; };
-    const Cand cands[4] = {{256, 256, 1.0}, {256, 192, 1.0}, {128, 256, 1.1}, {256, 128, 1.15}};
+    const Cand cands[5] = {{256, 256, 1.0}, {256, 192, 1.0}, {128, 256, 1.1}, {256, 128, 1.15}, {128, 128, 1.3}};
     double best = 0;
     for (const Cand& c : cands) {
       const double tiles = (double)((M + c.bm - 1) / c.bm) * ((N + c.bn - 1) / c.bn);
@@ -675,20 +665,23 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits) {
     p.splits = 1;
     p.k_chunk = K;
     return p;
-  }
-  if (M > 256) {
-    p.bm = 128;
-    p.splits = 1;
-    p.k_chunk = K;
+  };
+  if (M > 512 || (M > 64 && M <= 256 && N >= 16384)) return big();
+  if (M <= 256) {
+    // weight streaming (16 * MT rows): 128 columns per workgroup; split K in powers of
+    // two while the grid stays within one workgroup per CU and each split keeps >= 512 of K
+    p.stream = true;
+    p.bm = M <= 32 ? 32 : M <= 64 ? 64 : M <= 128 ? 128 : 256;
+    const int tiles = (N + 127) / 128;
+    int s = 1;
+    while (s * 2 <= max_splits && tiles * s * 2 <= 256 && K / (s * 2) >= 512) s *= 2;
+    p.k_chunk = (((K + s - 1) / s) + 63) / 64 * 64;
+    p.splits = (K + p.k_chunk - 1) / p.k_chunk;
     return p;
   }
-  p.bm = 64;
-  const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
-  int s = 1;
-  while (s < max_splits && tiles * s < 1024 && (K / (s * 2)) >= 256) s *= 2;
-  const int kc = (((K + s - 1) / s) + BK_MAX - 1) / BK_MAX * BK_MAX;
-  p.splits = (K + kc - 1) / kc;
-  p.k_chunk = kc;
+  p.bm = 128;
+  p.splits = 1;
+  p.k_chunk = K;
   return p;
 }
 

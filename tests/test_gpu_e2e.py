@@ -79,6 +79,23 @@ def oracle_schedule(reqs, n_blocks, max_seqs, chunk, vocab):
     return ids, order, steps, {r: s.block_table(r) for r in ids}
 
 
+def compare_free_running(name, gpu_tok, ref_tok, ref_lg):
+    """Free-running greedy ids must equal the oracle's up to the first near tie (the
+    oracle's logit of the GPU's choice within TOL * max|logit| of its own top logit);
+    the contexts differ after that, so the rest is left to the teacher-forced run."""
+    ref_tok = list(map(int, ref_tok))
+    assert len(gpu_tok) == len(ref_tok), (name, gpu_tok, ref_tok)
+    for j, (g, r) in enumerate(zip(gpu_tok, ref_tok)):
+        if g == r:
+            continue
+        lg = np.asarray(ref_lg[j], np.float64)
+        gap = (lg[r] - lg[g]) / np.max(np.abs(lg))
+        assert gap <= TOL, f"{name}: step {j} gpu {g} oracle {r}, oracle logit gap {gap:.3e} is no near tie"
+        log(f"{name}: near tie at step {j} (gap {gap:.2e}): gpu {g}, oracle {r}; comparison stops there")
+        return j
+    return len(ref_tok)
+
+
 def compare_forced(name, gpu_tok, gpu_logits, ref_lg):
     worst, ties = 0.0, 0
     assert len(gpu_logits) == len(ref_lg), (len(gpu_logits), len(ref_lg))
@@ -117,7 +134,7 @@ def test_cfg1_tiny_full():
         assert eng.inst.block_table(rid) == o_bt[rid]
         toks = eng.inst.tokens(rid)
         log(f"cfg1 req {rid}: gpu {toks} oracle {list(ref_tok[k])}")
-        assert toks == list(map(int, ref_tok[k]))
+        compare_free_running(f"cfg1 req {rid}", toks, ref_tok[k], ref_lg[k])
     done = eng.inst.drain()
     assert sorted(d["id"] for d in done) == o_ids
     # teacher forced, logits of every sampled row

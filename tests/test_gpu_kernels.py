@@ -60,7 +60,8 @@ def _gemm_case(M_, N, K, epi, seed):
                                     (32, 136, 160), (17, 8192, 1024), (65, 4096, 4096),
                                     (256, 1024, 688), (300, 1000, 688),
                                     (2080, 384, 512), (600, 1000, 688), (2080, 6144, 1024), (1031, 4096, 1384),
-                                    (2048, 4096, 256), (2080, 4096, 264), (2048, 6144, 96)])
+                                    (2048, 4096, 256), (2080, 4096, 264), (2048, 6144, 96), (200, 32768, 512),
+                                    (96, 20000, 256), (250, 6144, 1024)])
 @pytest.mark.parametrize("epi", [hxf.EPI_BF16, hxf.EPI_RESID, hxf.EPI_F32])
 def test_gemm(M_, N, K, epi):
     _gemm_case(M_, N, K, epi, seed=M_ * 7 + N + K + epi)
