@@ -69,7 +69,7 @@ typedef struct hxf_model_cfg {
 typedef struct hxf_sched_cfg {
   int64_t n_blocks;       /* KV pages in the pool */
   int32_t max_seqs;       /* running sequences (prefill + decode) at most */
-  int32_t chunk_tokens;   /* tokens per iteration: every running decode, then prefill chunks up to this total */
+  int32_t chunk_tokens;   /* prefill tokens per iteration (every running decode comes on top) */
   int32_t policy;         /* HXF_POLICY_* */
   int32_t clock;          /* HXF_CLOCK_* */
   int32_t executor;       /* HXF_EXEC_* */

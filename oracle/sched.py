@@ -19,11 +19,11 @@ Exact integer (microsecond) restatement of the paper's local priority queue
   arrival, then the lower id.
 
 Iteration rules (the paper only says batches are formed by continuous
-batching, run by vLLM): running decodes get one token each; running prefills
-get chunk tokens in queue order from what is left of ``chunk_tokens`` after
-the decode tokens (vLLM's token budget counts both); then queued requests are
-admitted in queue order while a sequence slot, the page reservation and
-budget are all available, stopping at the first that does not fit.
+batching): running decodes get one token each; running prefills get chunk
+tokens in queue order from a budget of ``chunk_tokens`` (decode tokens are not
+counted); then queued requests are admitted in queue order while a sequence
+slot, the page reservation and budget are all available, stopping at the
+first that does not fit.
 
 Baseline policies for comparison: FCFS (order by arrival in the queue) and
 LLF (laxity against the workflow's end-to-end deadline, no per-stage budget,
@@ -191,7 +191,7 @@ class Scheduler:
         for r in self.running:
             if r.state == DECODE:
                 batch.append((r, "d", [r.generated[-1]], r.n_kv))
-        budget = self.chunk - len(batch)          # the decode tokens count toward the chunk
+        budget = self.chunk
         pf = sorted((r for r in self.running if r.state == PREFILL), key=self.order)
         for r in pf:
             if budget <= 0:

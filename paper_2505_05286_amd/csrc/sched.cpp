@@ -177,7 +177,7 @@ void Scheduler::form_batch(i64 now, std::vector<BatchEntry>& batch, std::vector<
     const int32_t tok = r->forced.empty() ? r->generated[k] : r->forced[k];
     batch.push_back(BatchEntry{r, true, r->n_kv, 1, nullptr, tok, true});
   }
-  i64 budget = scfg.chunk_tokens - (i64)batch.size();   // the decode tokens count toward the chunk
+  i64 budget = scfg.chunk_tokens;   // prefill tokens; the decode tokens are not counted
   std::vector<Request*> pf;
   for (Request* r : running_)
     if (r->state == PREFILL) pf.push_back(r);
