@@ -373,8 +373,10 @@ def main():
     value = BATCH * args.steps / dt
     launches = max(prof["decode_attn_launches"], 1)
     avg_ms = prof["decode_attn_ms"] / launches
+    merge_ms = prof["decode_merge_ms"] / launches
     bytes_per_launch = prof["decode_attn_bytes"] / launches
     achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9
+    achieved_merged = bytes_per_launch / ((avg_ms + merge_ms) * 1e-3) / 1e9
     sum_ctx_now = sum(inst.request_state(r)["n_kv"] for r in ids)
     out = {
         "metric": METRIC,
@@ -398,7 +400,11 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": DECODE_ATTN_TRAFFIC["bytes_per_launch"],
                      "traffic_sample": DECODE_ATTN_TRAFFIC,
                      "kernel": "decode_attn_kernel<128>", "avg_launch_us": round(avg_ms * 1e3, 2),
-                     "bytes_per_launch": int(bytes_per_launch)},
+                     "bytes_per_launch": int(bytes_per_launch),
+                     "with_merge": {"kernels": "decode_attn_kernel<128> + decode_merge_kernel<128>",
+                                    "avg_us": round((avg_ms + merge_ms) * 1e3, 2),
+                                    "achieved": round(achieved_merged, 1),
+                                    "frac": round(achieved_merged / HBM_PEAK_GBS, 4)}},
     }
     del eng, inst
     if not args.no_cpu_baseline:

@@ -218,12 +218,14 @@ int hxf_last_batch(hxf_instance* inst, uint64_t* ids, int32_t cap, int32_t* n,
 /* fp32 logits (vocab floats) of the request's row in the last iteration; HXF_ENOTFOUND if it had none. */
 int hxf_last_logits(hxf_instance* inst, uint64_t id, float* dst, int32_t cap);
 
-/* Kernel timing of the decode-attention launches (HIP events on the bound
- * stream), for roofline reporting.  Enabling resets the counters. */
+/* Kernel timing of the decode-attention launches (HIP events stamped with the
+ * kernels' own start and end on the bound stream), for roofline reporting.
+ * Enabling resets the counters. */
 typedef struct hxf_profile {
   int64_t decode_attn_launches;  /* split-K attention kernel launches timed */
   int64_t decode_attn_bytes;     /* algorithmic K+V bytes those launches read (context tokens x 2 x dh x 2 B x kv-heads) */
-  double decode_attn_ms;         /* summed kernel time */
+  double decode_attn_ms;         /* summed split-K kernel time */
+  double decode_merge_ms;        /* summed time of the log-sum-exp merge kernels that follow them */
 } hxf_profile;
 
 int hxf_profile_enable(hxf_instance* inst, int32_t on);

@@ -302,6 +302,7 @@ int hxf_profile_get(hxf_instance* inst, hxf_profile* out) {
   out->decode_attn_launches = p->decode_attn_launches;
   out->decode_attn_bytes = p->decode_attn_bytes;
   out->decode_attn_ms = p->decode_attn_ms;
+  out->decode_merge_ms = p->decode_merge_ms;
   return HXF_OK;
 }
 

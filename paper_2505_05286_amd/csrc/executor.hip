@@ -169,7 +169,7 @@ class HipExecutor : public Executor {
   int32_t* host_sampled_ = nullptr;
   std::vector<uint64_t> last_rows_;   // request id per logits row of the last iteration
   bool ev_ = false;
-  std::vector<hipEvent_t> ev_pool_;
+  std::vector<hipEvent_t> ev_pool_, ev_merge_;
 };
 
 int HipExecutor::gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M,
@@ -269,6 +269,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     err = "run: metadata exceeds the workspace plan";
     return HXF_EINVAL;
   }
+  order_decode_items(ditems.data(), ditems.size());
   std::memcpy(hm + o_ditems, ditems.data(), ditems.size() * sizeof(DecodeItem));
   std::memcpy(hm + o_merges, merges.data(), merges.size() * sizeof(MergeItem));
   std::memcpy(hm + o_pitems, pitems.data(), pitems.size() * sizeof(PrefillItem));
@@ -361,7 +362,16 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
         prof.decode_attn_launches += 1;
         prof.decode_attn_bytes += kv_tokens * 2 * dh * 2;
       }
-      HXF_HIP(decode_merge_launch(da, st_));
+      hipEvent_t e2 = nullptr, e3 = nullptr;
+      if (prof.on) {
+        HXF_HIP(hipEventCreate(&e2));
+        HXF_HIP(hipEventCreate(&e3));
+      }
+      HXF_HIP(decode_merge_launch(da, st_, e2, e3));
+      if (prof.on) {
+        ev_merge_.push_back(e2);
+        ev_merge_.push_back(e3);
+      }
     }
     HXF_HIP(prefill_attn_launch(pa, st_));
     int pend_o = 0;
@@ -396,6 +406,14 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
       (void)hipEventDestroy(ev_pool_[i + 1]);
     }
     ev_pool_.clear();
+    for (size_t i = 0; i + 1 < ev_merge_.size(); i += 2) {
+      float ms = 0.f;
+      HXF_HIP(hipEventElapsedTime(&ms, ev_merge_[i], ev_merge_[i + 1]));
+      prof.decode_merge_ms += ms;
+      (void)hipEventDestroy(ev_merge_[i]);
+      (void)hipEventDestroy(ev_merge_[i + 1]);
+    }
+    ev_merge_.clear();
   }
   sampled.assign(host_sampled_, host_sampled_ + R);
   return HXF_OK;

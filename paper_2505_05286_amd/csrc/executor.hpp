@@ -36,6 +36,7 @@ struct Profile {
   double decode_attn_ms = 0;     // decode attention kernel (split-K part) time
   int64_t decode_attn_launches = 0;
   int64_t decode_attn_bytes = 0; // algorithmic KV bytes read by those launches
+  double decode_merge_ms = 0;    // log-sum-exp merge kernel time of the same iterations
 };
 
 std::unique_ptr<Executor> make_hip_executor(const hxf_model_cfg& m, const hxf_sched_cfg& s,

@@ -195,43 +195,79 @@ __global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
 }
 
 // Log-sum-exp merge of the split-K partials; one wavefront per (entry, q-head).
-// The partials' maxima are reduced across lanes first, then the weighted sums
-// are accumulated with independent (unrolled) loads.
+// Lane j holds (max, sum) of partial j, so the common maximum, the weights and
+// their sum take one load and two cross-lane reductions; the partial outputs of
+// the first kMergeChunk partials are loaded before that, so a merge of up to
+// kMergeChunk partials is one memory round trip.  Partials beyond 64 (contexts
+// over 64 partitions) are weighted from broadcast loads.
+constexpr int kMergeChunk = 8;
+
 template <int DH>
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeAttnArgs a) {
   const int G = a.Hq / a.Hkv;
-  const int job = blockIdx.x * 4 + (threadIdx.x >> 6);
+  // wavefront-uniform job: the item and the output row come through scalar loads
+  const int job = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (job >= a.n_merges * G) return;
   const int lane = threadIdx.x & 63;
   const MergeItem mi = a.merges[job / G];
   const int g = job % G;
-  const float2* ml = reinterpret_cast<const float2*>(a.part_ml);
-  float M = kNegInf;
-  for (int p = lane; p < mi.n_part; p += kWave) M = fmaxf(M, ml[(size_t)(mi.part0 + p) * G + g].x);
-  M = wave_max(M);
+  const int n = mi.n_part;
+  const int orow = a.q_row[mi.entry];
   constexpr int PER = DH / 64;   // dims per lane
+  const float2* ml = reinterpret_cast<const float2*>(a.part_ml) + (size_t)mi.part0 * G + g;
+  const float* po = a.part_o + ((size_t)mi.part0 * G + g) * DH + lane * PER;
+  const size_t ostride = (size_t)G * DH;
+  float x[kMergeChunk][PER];
+#pragma unroll
+  for (int j = 0; j < kMergeChunk; ++j) {
+    if (j < n) {
+      if constexpr (PER == 2) {
+        const float2 v = *reinterpret_cast<const float2*>(po + j * ostride);
+        x[j][0] = v.x;
+        x[j][PER - 1] = v.y;
+      } else {
+        x[j][0] = po[j * ostride];
+      }
+    }
+  }
+  const float2 mine = lane < n ? ml[(size_t)lane * G] : make_float2(kNegInf, 0.f);
+  float M = mine.x;
+  for (int p = lane + kWave; p < n; p += kWave) M = fmaxf(M, ml[(size_t)p * G].x);
+  M = wave_max(M);
+  const float wl = lane < n ? exp2f(mine.x - M) : 0.f;
+  float L = wave_sum(wl * mine.y);
   float acc[PER];
 #pragma unroll
   for (int k = 0; k < PER; ++k) acc[k] = 0.f;
-  float L = 0.f;
-#pragma unroll 4
-  for (int p = 0; p < mi.n_part; ++p) {
-    const size_t b = (size_t)(mi.part0 + p) * G + g;
-    const float2 v = ml[b];
-    const float w = exp2f(v.x - M);
-    L += w * v.y;
-    const float* o = a.part_o + b * DH + lane * PER;
-    if (PER == 2) {
-      const float2 x = *reinterpret_cast<const float2*>(o);
-      acc[0] += w * x.x;
-      acc[PER - 1] += w * x.y;
+#pragma unroll
+  for (int j = 0; j < kMergeChunk; ++j) {
+    if (j < n) {
+      const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wl), j));
+#pragma unroll
+      for (int k = 0; k < PER; ++k) acc[k] += w * x[j][k];
+    }
+  }
+  for (int p = kMergeChunk; p < n; ++p) {
+    float w;
+    if (p < kWave) {
+      w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wl), p));
+    } else {
+      const float2 v = ml[(size_t)p * G];
+      w = exp2f(v.x - M);
+      L += w * v.y;
+    }
+    const float* o = po + p * ostride;
+    if constexpr (PER == 2) {
+      const float2 v = *reinterpret_cast<const float2*>(o);
+      acc[0] += w * v.x;
+      acc[PER - 1] += w * v.y;
     } else {
       acc[0] += w * o[0];
     }
   }
   const float inv = 1.f / L;
-  uint16_t* out = a.out + (size_t)a.q_row[mi.entry] * a.out_stride + (mi.kvh * G + g) * DH + lane * PER;
-  if (PER == 2) *reinterpret_cast<uint32_t*>(out) = pack_bf2(acc[0] * inv, acc[PER - 1] * inv);
+  uint16_t* out = a.out + (size_t)orow * a.out_stride + (mi.kvh * G + g) * DH + lane * PER;
+  if constexpr (PER == 2) *reinterpret_cast<uint32_t*>(out) = pack_bf2(acc[0] * inv, acc[PER - 1] * inv);
   else out[0] = f2bf(acc[0] * inv);
 }
 
@@ -477,12 +513,15 @@ hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_
   return hipGetLastError();
 }
 
-hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st) {
+hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (a.n_merges <= 0) return hipSuccess;
   const int jobs = a.n_merges * (a.Hq / a.Hkv);
-  if (a.dh == 128) hipLaunchKernelGGL(decode_merge_kernel<128>, dim3((jobs + 3) / 4), dim3(256), 0, st, a);
-  else if (a.dh == 64) hipLaunchKernelGGL(decode_merge_kernel<64>, dim3((jobs + 3) / 4), dim3(256), 0, st, a);
-  else return hipErrorInvalidValue;
+  if (a.dh == 128)
+    hipExtLaunchKernelGGL(decode_merge_kernel<128>, dim3((jobs + 3) / 4), dim3(256), 0, st, ev_start, ev_stop, 0, a);
+  else if (a.dh == 64)
+    hipExtLaunchKernelGGL(decode_merge_kernel<64>, dim3((jobs + 3) / 4), dim3(256), 0, st, ev_start, ev_stop, 0, a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 namespace hxf {
 
 // Physical KV layout (per layer; K pool then V pool), kv-head major:
@@ -87,6 +89,12 @@ hipError_t kv_scatter_launch(const uint16_t* k, const uint16_t* v, const int32_t
 struct DecodeItem {
   int32_t entry, kvh, t0, t1, part, pad0, pad1, pad2;
 };
+// Launch order of the decode items: longest first (equal lengths keep their
+// order), so that the wavefronts that start last, when the chip drains, are the
+// short tail partitions.  Partial slots are unchanged, so the merge is unaffected.
+inline void order_decode_items(DecodeItem* it, size_t n) {
+  std::stable_sort(it, it + n, [](const DecodeItem& x, const DecodeItem& y) { return x.t1 - x.t0 > y.t1 - y.t0; });
+}
 // One merge job per (entry, kv-head): partials [part0, part0 + n_part).
 struct MergeItem {
   int32_t entry, kvh, part0, n_part;
@@ -115,7 +123,8 @@ struct DecodeAttnArgs {
 // ev_start / ev_stop (may be null): events that record the kernel's own start and end.
 hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start = nullptr,
                               hipEvent_t ev_stop = nullptr);
-hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st);
+hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start = nullptr,
+                               hipEvent_t ev_stop = nullptr);
 
 // One prefill work item: queries [q0, q0 + nq) (chunk-local) of entry `entry`, kv-head `kvh`.
 struct PrefillItem {

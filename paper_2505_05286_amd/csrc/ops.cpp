@@ -153,6 +153,7 @@ int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_poo
       merges[b * Hkv + h] = mi;
     }
   }
+  order_decode_items(items, (size_t)n);
   hipStream_t st = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
   if (hipMemcpyAsync(ws, host.data(), host.size(), hipMemcpyHostToDevice, st) != hipSuccess) return HXF_EDEVICE;

@@ -88,7 +88,7 @@ class RequestState(C.Structure):
 
 class Profile(C.Structure):
     _fields_ = [("decode_attn_launches", C.c_int64), ("decode_attn_bytes", C.c_int64),
-                ("decode_attn_ms", C.c_double)]
+                ("decode_attn_ms", C.c_double), ("decode_merge_ms", C.c_double)]
 
 
 _lib = None
