@@ -186,7 +186,7 @@ int HipExecutor::gemm(const uint16_t* A, int lda, const uint16_t* B, const uint1
   a.lda = lda;
   a.ldc = ldc;
   a.kt = (K + 31) / 32;
-  GemmPlan p = gemm_plan(M, N, K, kMaxSplits);
+  GemmPlan p = gemm_plan(M, N, K, kMaxSplits, epi == EPI_SWIGLU);
   if (p.splits > 1 && (int64_t)p.splits * M * N * 4 > plan_.part_bytes) {
     err = "gemm: split-K partial buffer too small";
     return HXF_EINVAL;

@@ -5,7 +5,8 @@
 //   M <= 64      gemm_stream_kernel: weight streaming through LDS DMA, split K;
 //   64 < M <= 512 gemm_nt_kernel: 64x64 / 128x128 tiles of 16x16x32 MFMAs, K
 //                staged through LDS from registers, split K for M <= 256;
-//   M > 512      gemm_big_dma_kernel: 256-row tiles of 32x32x16 MFMAs fed by LDS DMA.
+//   M > 512      gemm_big_kernel: macro tiles of up to 256 x 256 on 32x32x16 MFMAs fed
+//                by LDS DMA, four or eight wavefronts, tile shape chosen per GEMM.
 // Workgroups are renumbered so that consecutive output tiles (which share a
 // weight slice) land on the same XCD and its L2.
 #include <algorithm>
@@ -405,26 +406,33 @@ hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st, bool reduce) 
 // Prefill-sized M: BM x BN macro tiles on the 32x32x16 bf16 MFMA, fed by the
 // LDS DMA path.  A stage is 32 of K: the BM/16 A blocks (16 rows x 32 columns
 // of the activations, 1 KB each, in the MFMA operand order [k/8][row][8]) and
-// the BN/16 packed weight tiles, DMA'd by the four wavefronts together; NSTG
-// stages in flight in distinct LDS arrays (see the streaming kernel for the
-// wait and barrier discipline).  Wavefront (wm, wn) owns rows wm*BM/2.. and
-// columns wn*BN/2.. as BM/64 x BN/64 tiles of 32 x 32.  SwiGLU groups logical columns by 64
-// (32 gate rows, then the 32 matching up rows) so one lane holds both.
-template <int BM, int BN, int NSTG, int EPI, int OCC = 1>
-__global__ __launch_bounds__(256, OCC) void gemm_big_dma_kernel(GemmArgs a) {
-  constexpr int TM = BM / 64, TN = BN / 64;
-  constexpr int AB = BM / 16, BB = BN / 16;                 // 1 KB blocks per stage
-  constexpr int STAGE = (AB + BB) * 512;
-  constexpr int A_W = AB / 4, B_W = BB / 4;                  // blocks each wavefront moves per stage
-  constexpr int PER_W = A_W + B_W;                           // DMA instructions per wavefront per stage
+// the BN/16 packed weight tiles, DMA'd by the WM x WN wavefronts together (each
+// moves the same number of blocks; where the blocks do not divide evenly the
+// last block is moved again, an identical write); NSTG stages in flight in
+// distinct LDS arrays (see the streaming kernel for the wait and barrier
+// discipline).  Wavefront (wm, wn) owns rows wm*BM/WM.. and columns wn*BN/WN..
+// as tiles of 32 x 32.  With eight wavefronts two share each SIMD, so one issues
+// MFMAs while the other waits on LDS.  BM is any multiple of 32 so that the
+// row tiles can match the batch (2080 rows = 13 x 160).  SwiGLU groups logical
+// columns by 64 (32 gate rows, then the 32 matching up rows) so one lane holds
+// both; it needs BN/WN a multiple of 64.
+template <int BM, int BN, int WM, int WN, int NSTG, int EPI>
+__global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
+  constexpr int W = WM * WN;
+  constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
+  static_assert(TM * WM * 32 == BM && TN * WN * 32 == BN, "wavefront tiling");
+  constexpr int AB = BM / 16, BB = BN / 16, NBLK = AB + BB;   // 1 KB blocks per stage
+  constexpr int PER_W = (NBLK + W - 1) / W;                   // DMA instructions per wavefront per stage
+  constexpr int STAGE = NBLK * 512;
   constexpr bool SW = (EPI == EPI_SWIGLU);
-  static_assert(AB % 4 == 0 && BB % 4 == 0 && NSTG >= 2 && NSTG <= 4, "stage layout");
-  __shared__ __attribute__((aligned(1024))) bf16_t L0[STAGE], L1[STAGE], L2[NSTG > 2 ? STAGE : 8],
-      L3[NSTG > 3 ? STAGE : 8];
+  static_assert(!SW || TN % 2 == 0, "SwiGLU pairs 32-column tiles");
+  static_assert(NSTG >= 3 && NSTG <= 5 && NSTG * STAGE * 2 <= 160 * 1024, "stage layout");
+  __shared__ __attribute__((aligned(1024))) bf16_t L0[STAGE], L1[STAGE], L2[STAGE], L3[NSTG > 3 ? STAGE : 8],
+      L4[NSTG > 4 ? STAGE : 8];
   auto slot = [&](auto ic) -> bf16_t* {
     constexpr int I = decltype(ic)::value;
     if constexpr (I == 0) return L0; else if constexpr (I == 1) return L1; else if constexpr (I == 2) return L2;
-    else return L3;
+    else if constexpr (I == 3) return L3; else return L4;
   };
   const int tiles_m = (a.M + BM - 1) / BM;
   const int tiles_n = (a.N + BN - 1) / BN;
@@ -432,34 +440,45 @@ __global__ __launch_bounds__(256, OCC) void gemm_big_dma_kernel(GemmArgs a) {
   const int tn = L / tiles_m, tm = L % tiles_m;
   const int m0 = tm * BM, n0 = tn * BN;
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w / WN, wn = w % WN;
   const int nst = (a.K + 31) / 32;
 
-  // this wavefront's DMA sources: A row-blocks w*A_W.. and weight tiles w*B_W.. (no
-  // per-block branches, so the compiler keeps track of which LDS array each DMA writes)
-  const bf16_t* asrc[A_W];
-  const bf16_t* bsrc[B_W];
+  // This wavefront's DMA blocks w*PER_W + u: an A block (16 activation rows, the
+  // lane's row and 8-column chunk) or a packed weight tile (1 KB contiguous).  No
+  // per-block branches at issue time, so the compiler keeps track of which LDS
+  // array each DMA writes.
+  const bf16_t* src[PER_W];
+  int step[PER_W];   // elements per stage: 32 along an activation row, 512 for a weight tile
+  int dst[PER_W];
 #pragma unroll
-  for (int u = 0; u < A_W; ++u) asrc[u] = a.A + (size_t)min(m0 + (w * A_W + u) * 16 + (lane & 15), a.M - 1) * a.lda;
-#pragma unroll
-  for (int v = 0; v < B_W; ++v) {
-    const int c = min(n0 + (w * B_W + v) * 16, a.N - 1) & ~15;  // logical column of the tile (past N: repeat)
-    const bf16_t* mat = a.B;
-    int row = c;
-    if (SW) {
-      const int g = c >> 6, w64 = c & 63;
-      mat = (w64 < 32) ? a.B : a.B2;
-      row = g * 32 + (w64 & 31);
+  for (int u = 0; u < PER_W; ++u) {
+    const int gb = min(w * PER_W + u, NBLK - 1);
+    dst[u] = gb * 512;
+    if (gb < AB) {
+      src[u] = a.A + (size_t)min(m0 + gb * 16 + (lane & 15), a.M - 1) * a.lda + (lane >> 4) * 8;
+      step[u] = 32;
+    } else {
+      const int c = min(n0 + (gb - AB) * 16, a.N - 1) & ~15;   // logical column of the tile (past N: repeat)
+      const bf16_t* mat = a.B;
+      int row = c;
+      if (SW) {
+        const int g = c >> 6, w64 = c & 63;
+        mat = (w64 < 32) ? a.B : a.B2;
+        row = g * 32 + (w64 & 31);
+      }
+      src[u] = mat + (size_t)(row >> 4) * a.kt * 512 + lane * 8;
+      step[u] = 512;
     }
-    bsrc[v] = mat + (size_t)(row >> 4) * a.kt * 512 + lane * 8;
   }
+  // A past K: the last 16-byte chunk of the row is read again (its weights are zero)
+  const int a_last = a.K - 8 - (lane >> 4) * 8;
   auto issue = [&](int s, bf16_t* base) {
-    const int st = min(s, nst - 1);                          // past the end: reload the last stage (unused)
-    const int ka = min(st * 32 + (lane >> 4) * 8, a.K - 8);  // stays in the row; the weights are zero past K
+    const int st = min(s, nst - 1);   // past the end: reload the last stage (unused)
 #pragma unroll
-    for (int u = 0; u < A_W; ++u) dma16(asrc[u] + ka, base + (w * A_W + u) * 512);
-#pragma unroll
-    for (int v = 0; v < B_W; ++v) dma16(bsrc[v] + (size_t)st * 512, base + (AB + w * B_W + v) * 512);
+    for (int u = 0; u < PER_W; ++u) {
+      const int off = step[u] == 32 ? min(st * 32, a_last) : st * 512;
+      dma16(src[u] + off, base + dst[u]);
+    }
   };
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -475,9 +494,9 @@ __global__ __launch_bounds__(256, OCC) void gemm_big_dma_kernel(GemmArgs a) {
   const int lo = ((lane & 31) >> 4) * 512 + (lane >> 5) * 128 + (lane & 15) * 8;
   int a_off[TM], b_off[TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) a_off[i] = (wm * (BM / 32) + i * 2) * 512 + lo;
+  for (int i = 0; i < TM; ++i) a_off[i] = ((wm * TM + i) * 2) * 512 + lo;
 #pragma unroll
-  for (int j = 0; j < TN; ++j) b_off[j] = (AB + wn * (BN / 32) + j * 2) * 512 + lo;
+  for (int j = 0; j < TN; ++j) b_off[j] = (AB + (wn * TN + j) * 2) * 512 + lo;
   auto compute = [&](const bf16_t* base) {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
@@ -512,11 +531,12 @@ __global__ __launch_bounds__(256, OCC) void gemm_big_dma_kernel(GemmArgs a) {
 
   // lane holds column l % 32 and rows 8*(r/4) + 4*(lane/32) + r%4 of each 32x32 tile
   const int l32 = lane & 31, rq = (lane >> 5) * 4;
+  const int wr0 = m0 + wm * (BM / WM), wc0 = n0 + wn * (BN / WN);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     if (EPI == EPI_RESID) {
       // residual loads of RB rows first, then the adds and stores (one wait per RB rows)
-      constexpr int RB = TN > 3 ? 4 : TN > 2 ? 8 : 16;
+      constexpr int RB = TN > 3 ? 4 : TN > 1 ? 8 : 16;
       float* C = reinterpret_cast<float*>(a.C);
 #pragma unroll
       for (int r0 = 0; r0 < 16; r0 += RB) {
@@ -524,19 +544,18 @@ __global__ __launch_bounds__(256, OCC) void gemm_big_dma_kernel(GemmArgs a) {
 #pragma unroll
         for (int r = 0; r < RB; ++r) {
           const int rr = r0 + r;
-          const int row = min(m0 + wm * (BM / 2) + i * 32 + (rr >> 2) * 8 + rq + (rr & 3), a.M - 1);
+          const int row = min(wr0 + i * 32 + (rr >> 2) * 8 + rq + (rr & 3), a.M - 1);
 #pragma unroll
-          for (int j = 0; j < TN; ++j)
-            old[r][j] = C[(size_t)row * a.ldc + min(n0 + wn * (BN / 2) + j * 32 + l32, a.N - 1)];
+          for (int j = 0; j < TN; ++j) old[r][j] = C[(size_t)row * a.ldc + min(wc0 + j * 32 + l32, a.N - 1)];
         }
 #pragma unroll
         for (int r = 0; r < RB; ++r) {
           const int rr = r0 + r;
-          const int row = m0 + wm * (BM / 2) + i * 32 + (rr >> 2) * 8 + rq + (rr & 3);
+          const int row = wr0 + i * 32 + (rr >> 2) * 8 + rq + (rr & 3);
           if (row >= a.M) continue;
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
-            const int col = n0 + wn * (BN / 2) + j * 32 + l32;
+            const int col = wc0 + j * 32 + l32;
             if (col < a.N) C[(size_t)row * a.ldc + col] = old[r][j] + acc[i][j][rr];
           }
         }
@@ -545,12 +564,12 @@ __global__ __launch_bounds__(256, OCC) void gemm_big_dma_kernel(GemmArgs a) {
     }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = m0 + wm * (BM / 2) + i * 32 + (r >> 2) * 8 + rq + (r & 3);
+      const int row = wr0 + i * 32 + (r >> 2) * 8 + rq + (r & 3);
       if (row >= a.M) continue;
       if (SW) {
 #pragma unroll
         for (int j = 0; j < TN; j += 2) {
-          const int lc = n0 + wn * (BN / 2) + j * 32;   // first (gate) logical column of the 64-group
+          const int lc = wc0 + j * 32;   // first (gate) logical column of the 64-group
           if (lc >= a.N) continue;
           const float g = acc[i][j][r], u = acc[i][j + 1][r];
           reinterpret_cast<bf16_t*>(a.C)[(size_t)row * a.ldc + (lc >> 6) * 32 + l32] =
@@ -559,11 +578,10 @@ __global__ __launch_bounds__(256, OCC) void gemm_big_dma_kernel(GemmArgs a) {
       } else {
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          const int col = n0 + wn * (BN / 2) + j * 32 + l32;
+          const int col = wc0 + j * 32 + l32;
           if (col >= a.N) continue;
           const size_t o = (size_t)row * a.ldc + col;
           if (EPI == EPI_BF16) reinterpret_cast<bf16_t*>(a.C)[o] = f2bf(acc[i][j][r]);
-          else if (EPI == EPI_RESID) reinterpret_cast<float*>(a.C)[o] += acc[i][j][r];
           else reinterpret_cast<float*>(a.C)[o] = acc[i][j][r];
         }
       }
@@ -571,11 +589,44 @@ __global__ __launch_bounds__(256, OCC) void gemm_big_dma_kernel(GemmArgs a) {
   }
 }
 
-template <int BM, int BN, int NSTG, int EPI, int OCC = 1>
-hipError_t launch_big_dma(const GemmArgs& a, hipStream_t st) {
+// Macro-tile shapes of the big kernel: (BM, BN, WM x WN wavefronts), a per-flop cost
+// factor measured on the projection shapes (smaller tiles move more bytes per flop,
+// one-row wavefront grids read more LDS per MFMA), and whether the wavefront column
+// span suits SwiGLU.  Stages: as many as fit 160 KB of LDS, at most five.
+struct BigCfg {
+  int bm, bn, wm, wn;
+  double f;
+  bool swiglu;
+};
+constexpr BigCfg kBig[] = {
+    {256, 256, 4, 2, 1.02, true}, {224, 256, 1, 8, 1.10, false}, {192, 256, 2, 4, 1.0, true},
+    {160, 256, 1, 8, 1.17, false}, {128, 256, 2, 4, 1.3, true},    {128, 128, 2, 2, 1.6, true},
+};
+constexpr int kNumBig = sizeof(kBig) / sizeof(kBig[0]);
+
+template <int BM, int BN, int WM, int WN, int EPI>
+hipError_t launch_big(const GemmArgs& a, hipStream_t st) {
+  constexpr int STAGE_BYTES = (BM + BN) * 64;
+  constexpr int NSTG = std::min(5, 160 * 1024 / STAGE_BYTES);
   const int nb = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_big_dma_kernel<BM, BN, NSTG, EPI, OCC>), dim3(nb), dim3(256), 0, st, a);
+  hipLaunchKernelGGL((gemm_big_kernel<BM, BN, WM, WN, NSTG, EPI>), dim3(nb), dim3(64 * WM * WN), 0, st, a);
   return hipGetLastError();
+}
+
+template <int EPI>
+hipError_t launch_big_cfg(const GemmArgs& a, int cfg, hipStream_t st) {
+  switch (cfg) {
+    case 0: return launch_big<256, 256, 4, 2, EPI>(a, st);
+    case 2: return launch_big<192, 256, 2, 4, EPI>(a, st);
+    case 4: return launch_big<128, 256, 2, 4, EPI>(a, st);
+    case 5: return launch_big<128, 128, 2, 2, EPI>(a, st);
+    default: break;
+  }
+  if constexpr (EPI != EPI_SWIGLU) {
+    if (cfg == 1) return launch_big<224, 256, 1, 8, EPI>(a, st);
+    if (cfg == 3) return launch_big<160, 256, 1, 8, EPI>(a, st);
+  }
+  return hipErrorInvalidValue;
 }
 
 template <int BM, int BN, int BK, int NS, int EPI>
@@ -603,13 +654,9 @@ hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st, bool reduce
     return launch_stream<16, EPI>(a, p.splits, st, reduce);
   }
   if (p.big) {
-    // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0 (and BN % 128 == 0)
+    // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0
     if (EPI == EPI_SWIGLU && a.N % 64 != 0) return launch_tile<128, 128, 64, 2, EPI>(a, 1, st);
-    if (p.bm == 128) return p.bn == 128 ? launch_big_dma<128, 128, 4, EPI>(a, st) : launch_big_dma<128, 256, 4, EPI>(a, st);
-    if (p.bn == 128) return launch_big_dma<256, 128, 4, EPI>(a, st);
-    if constexpr (EPI != EPI_SWIGLU)
-      if (p.bn == 192) return launch_big_dma<256, 192, 4, EPI>(a, st);
-    return launch_big_dma<256, 256, 4, EPI>(a, st);
+    return launch_big_cfg<EPI>(a, p.cfg, st);
   }
   return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce);
 }
@@ -643,22 +690,22 @@ hipError_t pack_weight_launch(const uint16_t* W, int N, int K, uint16_t* out, hi
 // Kernel, tile and split-K choice.  M <= 256: the weight-streaming kernel, except
 // for wide outputs (N >= 16384) above 64 rows, which take the big-tile kernel as
 // every M > 512 does.  256 < M <= 512: 128x128 tiles of the LDS-staged kernel.
-GemmPlan gemm_plan(int M, int N, int K, int max_splits) {
+GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu) {
   GemmPlan p;
-  // LDS-DMA big tiles: the candidate minimising max(1, tiles / 256 CUs) * tile area * a
-  // per-flop factor measured on the projections (narrower wavefront tiles read more LDS
-  // per MFMA)
+  // big tiles: the shape minimising whole rounds of one workgroup per CU times tile area
+  // times its cost factor (the last round costs as much as a full one)
   auto big = [&]() {
-    struct Cand { int bm, bn; double f; };
-    const Cand cands[5] = {{256, 256, 1.0}, {256, 192, 1.0}, {128, 256, 1.1}, {256, 128, 1.15}, {128, 128, 1.3}};
     double best = 0;
-    for (const Cand& c : cands) {
-      const double tiles = (double)((M + c.bm - 1) / c.bm) * ((N + c.bn - 1) / c.bn);
-      const double cost = std::max(1.0, tiles / 256.0) * c.bm * c.bn * c.f;
+    for (int c = 0; c < kNumBig; ++c) {
+      const BigCfg& g = kBig[c];
+      if (swiglu && !g.swiglu) continue;
+      const int tiles = ((M + g.bm - 1) / g.bm) * ((N + g.bn - 1) / g.bn);
+      const double cost = (double)((tiles + 255) / 256) * g.bm * g.bn * g.f;
       if (best == 0 || cost < best - 1e-6) {
         best = cost;
-        p.bm = c.bm;
-        p.bn = c.bn;
+        p.cfg = c;
+        p.bm = g.bm;
+        p.bn = g.bn;
       }
     }
     p.big = true;

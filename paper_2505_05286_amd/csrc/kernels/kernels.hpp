@@ -41,13 +41,15 @@ struct GemmArgs {
 struct GemmPlan {
   bool stream = false;  // decode-sized M: LDS-DMA weight-streaming kernel
   bool big = false;     // prefill-sized M: LDS-DMA 32x32x16 MFMA kernel
+  int cfg = 0;          // big kernel: macro-tile configuration
   int bm = 128;
   int bn = 128;
   int splits = 1;
   int k_chunk = 0;
 };
 
-GemmPlan gemm_plan(int M, int N, int K, int max_splits);
+// swiglu: the plan is for the SwiGLU epilogue (N = 2F logical columns)
+GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu = false);
 // With reduce == false a split-K plan leaves its fp32 partials [splits][M][N] in
 // a.partial for the consumer to sum (no reduction launch).
 hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st, bool reduce = true);

@@ -57,7 +57,7 @@ int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void*
   if (epi == HXF_EPI_SWIGLU && (!B2 || N % 32)) return HXF_EINVAL;
   if (ldc < (epi == HXF_EPI_SWIGLU ? N / 2 : N)) return HXF_EINVAL;
   if (M == 0) return HXF_OK;
-  GemmPlan p = gemm_plan(M, N, K, 8);
+  GemmPlan p = gemm_plan(M, N, K, 8, epi == HXF_EPI_SWIGLU);
   if (p.splits > 1 && (!workspace || ws_bytes < (int64_t)p.splits * M * N * 4)) return HXF_ENOMEM;
   GemmArgs a{};
   a.A = (const uint16_t*)A;

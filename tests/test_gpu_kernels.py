@@ -61,7 +61,7 @@ def _gemm_case(M_, N, K, epi, seed):
                                     (256, 1024, 688), (300, 1000, 688),
                                     (2080, 384, 512), (600, 1000, 688), (2080, 6144, 1024), (1031, 4096, 1384),
                                     (2048, 4096, 256), (2080, 4096, 264), (2048, 6144, 96), (200, 32768, 512),
-                                    (96, 20000, 256), (250, 6144, 1024)])
+                                    (96, 20000, 256), (250, 6144, 1024), (2300, 6144, 72), (960, 11008, 72)])
 @pytest.mark.parametrize("epi", [hxf.EPI_BF16, hxf.EPI_RESID, hxf.EPI_F32])
 def test_gemm(M_, N, K, epi):
     _gemm_case(M_, N, K, epi, seed=M_ * 7 + N + K + epi)
@@ -70,7 +70,7 @@ def test_gemm(M_, N, K, epi):
 @pytest.mark.parametrize("M_,N,K", [(5, 64, 256), (64, 2 * 688, 256), (33, 2 * 688, 2048), (64, 2 * 14336, 4096),
                                     (20, 2 * 4096, 4096), (64, 2 * 96, 8192), (2080, 2 * 4096, 200),
                                     (300, 2 * 1376, 512), (128, 2 * 14336, 4096), (700, 2 * 688, 256),
-                                    (2080, 2 * 2080, 512)])
+                                    (2080, 2 * 2080, 512), (1040, 2 * 5504, 72), (520, 2 * 3584, 72)])
 def test_gemm_swiglu(M_, N, K):
     _gemm_case(M_, N, K, hxf.EPI_SWIGLU, seed=M_ + N + K)
 
