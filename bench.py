@@ -242,6 +242,61 @@ def workload5(n_wf, policy):
     return st
 
 
+ABLATION_SCENARIOS = [
+    # (name, arrival-rate multiple of 0.5 workflows/s, SLO multiple of the isolated latency, tenant mix)
+    ("configured: 0.5 wf/s, SLO 10x", 1.0, 10, None),
+    ("2x load: 1.0 wf/s, SLO 10x", 2.0, 10, None),
+    ("3x load: 1.5 wf/s, SLO 10x", 3.0, 10, None),
+    ("tight SLO: 0.5 wf/s, SLO 3x", 1.0, 3, None),
+    ("two tenants at 1.0 wf/s: SLO 4x (even) / 20x (odd)", 2.0, None, (4, 20)),
+]
+
+
+def policy_ablation(n_wf=300):
+    """Local-queue policy ablation (PQ vs FCFS vs LLF) on config-5 workflows, run by
+    the scheduler-only executor on the virtual clock: the iteration time is the
+    calibrated cost model's, so no GPU is needed and every run is deterministic.
+    Reports SLO attainment and P95 latency per scenario and policy."""
+    import numpy as np
+
+    import synth
+    from paper_2505_05286_amd import hxf
+    from paper_2505_05286_amd.workflows import Driver
+
+    shape = synth.model_shape("qwen32b")
+    cost, it = COST_PS["qwen32b"]
+    pols = [("pq", hxf.POLICY_PQ), ("fcfs", hxf.POLICY_FCFS), ("llf", hxf.POLICY_LLF)]
+    out = []
+    for name, rate, slo, mix in ABLATION_SCENARIOS:
+        row = {"scenario": name}
+        for pname, pol in pols:
+            wfs = cfg5_workflows(n_wf, shape.vocab)
+            for w in wfs:
+                w.arrival_us = int(w.arrival_us / rate)
+                scale = slo if mix is None else mix[w.wid % 2]
+                w.slo_us = w.slo_us * scale // 10   # generated at 10x the isolated latency
+            mcfg = hxf.model_cfg(shape, 8192 + 64 + 256 + 512 + 256 + 16)
+            scfg = hxf.sched_cfg(40_000, 128, 2048, cost, it, policy=pol, executor=hxf.EXEC_NULL)
+            inst = hxf.Instance(mcfg, scfg)
+            d = Driver(inst, wfs)
+            d.run()
+            st = d.stats()
+            lat = np.array([w.finish_us - w.arrival_us for w in d.wf], dtype=np.float64)
+            res = {"slo_attainment": round(st["slo_attainment"], 4), "p95_latency_s": round(st["p95_latency_s"], 2),
+                   "mean_latency_s": round(st["mean_latency_s"], 2)}
+            if mix is not None:
+                for t, sc in enumerate(mix):
+                    sel = [w for w in d.wf if w.wid % 2 == t]
+                    res[f"slo_attainment_{sc}x"] = round(float(np.mean([w.finish_us - w.arrival_us <= w.slo_us
+                                                                        for w in sel])), 4)
+            row[pname] = res
+            del inst
+            progress(f"{name}: {pname} {res}")
+        out.append(row)
+    return {"ablation": "local queue policy, config 5 (32B shape), virtual clock", "workflows": n_wf,
+            "scenarios": out}
+
+
 def attn_kernel_probe(reps=8):
     """Only the paged decode-attention kernel (plus its merge) on the benchmark's
     64 contexts, `reps` times, then one 1 GiB device copy of known size: the short
@@ -301,6 +356,8 @@ def main():
     ap.add_argument("--policy", default="pq", choices=("pq", "fcfs", "llf"), help="workload 5: local queue policy")
     ap.add_argument("--attn-kernel-probe", action="store_true",
                     help="run only the decode-attention kernel and a calibration copy (for counter runs)")
+    ap.add_argument("--policy-ablation", action="store_true",
+                    help="PQ / FCFS / LLF on config-5 workflows, virtual clock, scheduler only (CPU)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
@@ -309,6 +366,10 @@ def main():
 
     if args.attn_kernel_probe:
         print(json.dumps(attn_kernel_probe()), flush=True)
+        return
+
+    if args.policy_ablation:
+        print(json.dumps(policy_ablation(300 if args.n_workflows == 16 else args.n_workflows)), flush=True)
         return
 
     if args.workload != 2:

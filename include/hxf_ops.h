@@ -83,7 +83,8 @@ int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k
 
 /* Decode attention, one query token per sequence: q bf16 [B, Hq, dh] (rotated), attends to positions
  * [0, ctx_host[b]) of sequence b through block table bt [B, bt_stride] (device); out bf16 [B, Hq, dh].
- * Split into partitions of 512 tokens per (sequence, kv-head), merged by log-sum-exp.
+ * Each (sequence, kv-head) context is split into equal page-aligned partitions (at least 256 tokens,
+ * sized so that the work items fill the wavefronts the chip holds at once), merged by log-sum-exp.
  * workspace: hxf_op_decode_attention_workspace_bytes(...) bytes. */
 int64_t hxf_op_decode_attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
                                                 const int32_t* ctx_host);

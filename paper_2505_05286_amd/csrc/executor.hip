@@ -64,7 +64,7 @@ WsPlan plan_workspace(const hxf_model_cfg& m, const hxf_sched_cfg& s) {
   p.r_max = s.max_seqs;
   p.e_max = s.max_seqs;
   p.bt_w = ceil_div(m.max_context, kPage);
-  p.dec_items_max = (int64_t)s.max_seqs * hkv * ceil_div(m.max_context, kDecodePartition);
+  p.dec_items_max = (int64_t)s.max_seqs * hkv * ceil_div(m.max_context, kDecodeMinPartition);
   p.merges_max = (int64_t)s.max_seqs * hkv;
   const int qpi = prefill_queries_per_item((int)G);
   p.pf_items_max = hkv * (ceil_div(s.chunk_tokens, qpi) + s.max_seqs);
@@ -203,12 +203,15 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   const int G = hq / hkv;
   const int qkv_w = (hq + 2 * hkv) * dh;
   int T = 0, R = 0, n_dec = 0, bt_w = 1;
+  int64_t dec_ctx = 0;
   for (const auto& e : batch) {
     T += e.n;
     R += e.logits ? 1 : 0;
     n_dec += e.decode ? 1 : 0;
+    if (e.decode) dec_ctx += (int64_t)e.pos0 + 1;
     bt_w = std::max<int>(bt_w, (int)ceil_div((int64_t)e.pos0 + e.n, kPage));
   }
+  const int64_t dec_target = decode_target_tokens(dec_ctx, n_dec, hkv);
   if (T > plan_.t_max || R > plan_.r_max || E > plan_.e_max) {
     err = "run: batch exceeds the workspace plan";
     return HXF_EINVAL;
@@ -245,10 +248,11 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     for (int j = 0; j < bt_w; ++j) hm[o_bt + (int64_t)e * bt_w + j] = j < np ? bt[j] : 0;
     if (be.decode) {
       const int ctx = be.pos0 + 1;
+      const int plen = decode_part_len(ctx, dec_target);
       for (int h = 0; h < hkv; ++h) {
         MergeItem mi{e, h, n_part, 0};
-        for (int t0 = 0; t0 < ctx; t0 += kDecodePartition) {
-          ditems.push_back(DecodeItem{e, h, t0, std::min(ctx, t0 + kDecodePartition), n_part++, 0, 0, 0});
+        for (int t0 = 0; t0 < ctx; t0 += plen) {
+          ditems.push_back(DecodeItem{e, h, t0, std::min(ctx, t0 + plen), n_part++, 0, 0, 0});
           ++mi.n_part;
         }
         merges.push_back(mi);

@@ -11,10 +11,6 @@
 
 namespace hxf {
 
-// Decode attention splits each sequence's context into partitions of this many
-// tokens (32 pages); every (sequence, kv-head, partition) is one work item.
-constexpr int kDecodePartition = 512;
-
 struct WsPlan {
   int64_t t_max = 0, r_max = 0, e_max = 0, bt_w = 0;
   int64_t dec_items_max = 0, merges_max = 0, pf_items_max = 0;

@@ -22,9 +22,20 @@ struct DecodeLayout {
   int64_t items = 0, merges = 0, off_items = 0, off_merges = 0, off_qrow = 0, off_o = 0, off_ml = 0, total = 0;
 };
 
+// Partition target of a decode batch (the same split the executor uses).
+int64_t decode_target(int B, int Hkv, const int32_t* ctx) {
+  int64_t sum = 0;
+  for (int b = 0; b < B; ++b) sum += std::max(ctx[b], 1);
+  return decode_target_tokens(sum, B, Hkv);
+}
+
 DecodeLayout decode_layout(int B, int Hq, int Hkv, int dh, const int32_t* ctx) {
   DecodeLayout L;
-  for (int b = 0; b < B; ++b) L.items += (int64_t)Hkv * ((std::max(ctx[b], 1) + kDecodePartition - 1) / kDecodePartition);
+  const int64_t target = decode_target(B, Hkv, ctx);
+  for (int b = 0; b < B; ++b) {
+    const int c = std::max(ctx[b], 1);
+    L.items += (int64_t)Hkv * ((c + decode_part_len(c, target) - 1) / decode_part_len(c, target));
+  }
   L.merges = (int64_t)B * Hkv;
   const int G = Hq / Hkv;
   int64_t o = 0;
@@ -141,12 +152,14 @@ int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_poo
   auto* merges = reinterpret_cast<MergeItem*>(host.data() + L.off_merges);
   auto* qrow = reinterpret_cast<int32_t*>(host.data() + L.off_qrow);
   int n = 0;
+  const int64_t target = decode_target(B, Hkv, ctx);
   for (int b = 0; b < B; ++b) {
     qrow[b] = b;
+    const int plen = decode_part_len(ctx[b], target);
     for (int h = 0; h < Hkv; ++h) {
       MergeItem mi{b, h, n, 0};
-      for (int t0 = 0; t0 < ctx[b]; t0 += kDecodePartition) {
-        items[n] = DecodeItem{b, h, t0, std::min(ctx[b], t0 + kDecodePartition), n, 0, 0, 0};
+      for (int t0 = 0; t0 < ctx[b]; t0 += plen) {
+        items[n] = DecodeItem{b, h, t0, std::min(ctx[b], t0 + plen), n, 0, 0, 0};
         ++n;
         ++mi.n_part;
       }

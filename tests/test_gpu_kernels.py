@@ -245,6 +245,15 @@ def test_decode_attention_cfg2_full_size_sampled():
     _decode_case(ctxs, 32, 8, 128, seed=2, sample=sample)
 
 
+def test_decode_attention_one_item_per_pair():
+    """260 sequences x 8 kv-heads: at least as many (sequence, kv-head) pairs as the
+    chip holds wavefronts, so every pair is one work item (no split)."""
+    rng = np.random.default_rng(260)
+    ctxs = [int(c) for c in rng.integers(1, 300, 260)]
+    sample = list(range(0, 260, 13)) + [259]
+    _decode_case(ctxs, 32, 8, 128, seed=260, sample=sample)
+
+
 def _prefill_case(chunks, hq, hkv, dh, seed):
     """chunks: list of (pos0, n): n new queries at positions pos0.. over a context of pos0+n."""
     t = torch()
