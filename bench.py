@@ -33,7 +33,7 @@ HBM_PEAK_GBS = 8000.0
 # (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, over `bench.py --attn-kernel-probe`,
 # each scaled by what the counter reads for a 1 GiB copy: 2.000 and 1.000); valid
 # for the kernel as it stands, to be re-measured whenever it changes.
-DECODE_ATTN_TRAFFIC = {"bytes_per_launch": 843_250_061, "algorithmic_bytes_per_launch": 829_956_096,
+DECODE_ATTN_TRAFFIC = {"bytes_per_launch": 838_258_660, "algorithmic_bytes_per_launch": 829_956_096,
                        "sample": "attention probe, 64 contexts of the benchmark, 202626 tokens"}
 BATCH = 64
 MAX_NEW = 1000
