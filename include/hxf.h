@@ -144,6 +144,8 @@ typedef struct hxf_step_info {
   int64_t t_iter_us;        /* virtual or measured duration of the iteration */
   int64_t free_blocks;      /* free KV pages after the iteration */
   int64_t iteration;        /* index of this iteration */
+  int64_t sum_decode_ctx;   /* cost-model term: sum of the decode rows' context lengths */
+  int64_t prefill_attn;     /* cost-model term: sum over prefill chunks of chunk_len * (chunk_start + chunk_len) */
 } hxf_step_info;
 
 typedef struct hxf_completion {

@@ -271,6 +271,7 @@ class Scheduler:
                     n_prefill_tokens=sum(len(b[2]) for b in batch if b[1] == "p"),
                     n_logit_rows=len(rows), t_iter_us=dt, n_admitted=len(admitted),
                     n_finished=len(finished), free_blocks=self.alloc.n_free(),
+                    sum_decode_ctx=sum_ctx, prefill_attn=attn,
                     admitted=admitted, batch_ids=sorted(b[0].id for b in batch))
         return OK, info
 

@@ -171,6 +171,8 @@ int hxf_step(hxf_instance* inst, int64_t now_us, hxf_step_info* out) {
   }
   std::sort(inst->last_ids.begin(), inst->last_ids.end());
   info.n_tokens = (int32_t)n_tok;
+  info.sum_decode_ctx = sum_ctx;
+  info.prefill_attn = attn;
   info.n_admitted = (int32_t)inst->admitted.size();
   info.t_iter_us = dt;
   S.commit(inst->batch, inst->sampled, now_us + dt, &info.n_finished);

@@ -64,7 +64,8 @@ class DeviceBuffers(C.Structure):
 class StepInfo(C.Structure):
     _fields_ = [("n_tokens", C.c_int32), ("n_decode", C.c_int32), ("n_prefill_tokens", C.c_int32),
                 ("n_logit_rows", C.c_int32), ("n_admitted", C.c_int32), ("n_finished", C.c_int32),
-                ("t_iter_us", C.c_int64), ("free_blocks", C.c_int64), ("iteration", C.c_int64)]
+                ("t_iter_us", C.c_int64), ("free_blocks", C.c_int64), ("iteration", C.c_int64),
+                ("sum_decode_ctx", C.c_int64), ("prefill_attn", C.c_int64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

@@ -43,6 +43,7 @@ class Driver:
         self.inst = inst
         self.wf = sorted(workflows, key=lambda w: w.arrival_us)
         self.measured = measured
+        self.deadlocked = False
         self.by_id = {}
         self.iterations = 0
         self.tokens = 0
@@ -86,7 +87,11 @@ class Driver:
                     now = max(now, self.wf[nxt].arrival_us)
                     continue
                 if active:
-                    raise RuntimeError("instance idle with unfinished workflows (retained KV exhausted the pool?)")
+                    # Nothing is runnable, nothing else arrives, and workflows are unfinished:
+                    # the KV that finished stages retain for their forks fills the pool and the
+                    # queued requests cannot be admitted (no preemption).  Stop; the unfinished
+                    # workflows count as SLO misses.
+                    self.deadlocked = True
                 break
             self.iterations += 1
             self.tokens += info["n_tokens"]
@@ -108,16 +113,22 @@ class Driver:
         return now
 
     def stats(self):
-        lat = np.array([w.finish_us - w.arrival_us for w in self.wf], dtype=np.float64)
+        """Latency and SLO attainment per workflow; a workflow that never finished (a
+        deadlocked run) has infinite latency and misses its SLO."""
+        done = [w for w in self.wf if w.finish_us >= 0]
+        lat = np.array([w.finish_us - w.arrival_us if w.finish_us >= 0 else np.inf for w in self.wf], dtype=np.float64)
         slo = np.array([w.slo_us for w in self.wf], dtype=np.float64)
-        makespan = max(w.finish_us for w in self.wf) - min(w.arrival_us for w in self.wf)
+        makespan = max(w.finish_us for w in done) - min(w.arrival_us for w in self.wf) if done else 0
+        p95 = float(np.percentile(lat, 95))
         return {
             "workflows": len(self.wf),
+            "finished": len(done),
+            "deadlocked": self.deadlocked,
             "slo_attainment": float(np.mean(lat <= slo)),
-            "p95_latency_s": float(np.percentile(lat, 95) / 1e6),
-            "mean_latency_s": float(lat.mean() / 1e6),
-            "p95_slo_scale": float(np.percentile(lat / (slo / 10.0), 95)),
-            "throughput_wf_per_s": len(self.wf) / (makespan / 1e6),
+            "p95_latency_s": p95 / 1e6 if np.isfinite(p95) else None,
+            "mean_latency_s": float(np.mean([w.finish_us - w.arrival_us for w in done]) / 1e6) if done else None,
+            "p95_slo_scale": float(np.percentile(lat / (slo / 10.0), 95)) if np.isfinite(p95) else None,
+            "throughput_wf_per_s": len(done) / (makespan / 1e6) if makespan > 0 else 0.0,
             "iterations": self.iterations,
             "prefill_tokens": self.prefill_tokens,
             "decode_tokens": self.decode_tokens,

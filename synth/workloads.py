@@ -9,8 +9,9 @@ Token ids are uniform in [0, vocab).  Times are integer microseconds.
 
 End-to-end SLOs are ``slo_scale`` times a reference isolated latency
 ``REF_US(L_in, L_out)`` summed over the workflow's critical path.  The
-reference per-token figures below are fixed data (order-of-magnitude MI355X
-figures for each shape), not a model of the hardware.
+reference figures below are fixed data: a lone request's latency on one MI355X
+(chunked prefill, batch-1 decode at ~4k context), as measured for each 8B/32B
+shape by ``bench.py --calibrate``; the tiny shape's are nominal.
 """
 from dataclasses import dataclass, field
 from typing import List, Optional, Tuple
@@ -20,8 +21,8 @@ import numpy as np
 # Reference isolated latency per shape: base + per-prompt-token + per-output-token (us).
 REF_LATENCY = {
     "tiny": (200, 0.05, 150),
-    "llama8b": (2000, 0.10, 6000),
-    "qwen32b": (4000, 0.40, 12000),
+    "llama8b": (3855, 18.8, 3949),
+    "qwen32b": (13126, 75.6, 13368),
 }
 
 
@@ -126,10 +127,11 @@ def cfg5(vocab=152064, n_wf=300, mean_interarrival_s=2.0, slo_scale=10, model="q
         schema = _ids(rng, vocab, l1)
         corr = [_ids(rng, vocab, s["corr_in"]) for _ in range(s["n_corr"])]
         ev = _ids(rng, vocab, s["eval_in"])
-        ctx1 = l1 + s["s1_out"]
+        # forks re-prefill only the parent's partial last page (at most 16 tokens) plus
+        # their appended tokens
         iso = (ref_isolated_us(model, l1, s["s1_out"])
-               + ref_isolated_us(model, ctx1, s["cand_out"])
-               + ref_isolated_us(model, ctx1 + s["cand_out"] + s["corr_in"], s["corr_out"])
+               + ref_isolated_us(model, 16, s["cand_out"])
+               + ref_isolated_us(model, 16 + s["corr_in"], s["corr_out"])
                + ref_isolated_us(model, s["eval_in"], s["eval_out"]))
         out.append(Workflow(w, int(arrivals[w]), slo_scale * iso, l1, schema, corr, ev))
     return out

@@ -56,7 +56,7 @@ class Pair:
         ids, adm = self.g.last_batch()
         assert ids == io["batch_ids"] and adm == io["admitted"]
         for k in ("n_tokens", "n_decode", "n_prefill_tokens", "n_logit_rows", "t_iter_us", "n_admitted",
-                  "n_finished", "free_blocks"):
+                  "n_finished", "free_blocks", "sum_decode_ctx", "prefill_attn"):
             assert ig[k] == io[k], k
         assert self.o.queue_order() == self.g.queue_order()
         return so, io
