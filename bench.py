@@ -113,8 +113,9 @@ def load_model(name, n_layers=None):
     return shape, dm
 
 
-def step_until(inst, now, cond, timed=None):
-    """Step until cond(info) is true; return (now, iterations, prefill tokens, decode rows, seconds)."""
+def step_until(inst, now, cond, timed=None, per_step=None):
+    """Step until cond(info) is true; return (now, iterations, prefill tokens, decode rows, seconds).
+    per_step(info) is called after every iteration."""
     import torch
     from paper_2505_05286_amd import hxf
     it = pf = dec = 0
@@ -128,6 +129,8 @@ def step_until(inst, now, cond, timed=None):
         it += 1
         pf += info["n_prefill_tokens"]
         dec += info["n_logit_rows"]
+        if per_step is not None:
+            per_step(info)
         if cond(info):
             break
     torch.cuda.synchronize()
@@ -184,7 +187,18 @@ def workload4():
     for p in pid:
         inst.release(p)
     progress("timed: 256 forked branches decoding 256 tokens each")
-    now, it2, pf2, dec2, dt2 = step_until(inst, now, lambda i: False)
+    shared = (len(parents[0].prompt) - 1) // 16 * 16         # tokens of the parents' shared full pages
+    kv = {"logical": 0, "unique": 0}
+
+    def count(info):
+        # (token, kv-head) pairs of context attended this iteration, per sequence and once per page
+        kv["logical"] += info["sum_decode_ctx"]
+        kv["unique"] += info["sum_decode_ctx"] - (info["n_decode"] - len(parents)) * shared
+    inst.profile_enable(True)
+    now, it2, pf2, dec2, dt2 = step_until(inst, now, lambda i: False, per_step=count)
+    prof = inst.profile()
+    inst.profile_enable(False)
+    per_tok = 2 * shape.n_kv_heads * shape.head_dim * 2 * shape.n_layers     # K+V bytes per token, all layers
     for c in corr:
         inst.submit(now, c.workflow, 2, 0, c.wf_slo_us, c.prompt, c.max_new_tokens, parent=fid[(c.workflow, c.branch)])
     for (w, b), f in fid.items():
@@ -196,6 +210,12 @@ def workload4():
             "parent_prefill_tokens_per_s": round(pf1 / dt1, 1),
             "branch_decode_tokens_per_s": round(dec2 / dt2, 1), "branch_iterations": it2,
             "branch_ms_per_iteration": round(dt2 / it2 * 1e3, 3),
+            "branch_kv_gb_per_iteration": {"logical": round(kv["logical"] * per_tok / it2 / 1e9, 2),
+                                           "unique": round(kv["unique"] * per_tok / it2 / 1e9, 2),
+                                           "read": round(prof["decode_attn_bytes"] / it2 / 1e9, 2)},
+            "branch_attention_ms_per_iteration": round(prof["decode_attn_ms"] / it2, 3),
+            "branch_attention_read_tb_per_s": round(prof["decode_attn_bytes"] / (prof["decode_attn_ms"] * 1e-3) / 1e12,
+                                                    3),
             "correction_prefill_tokens_per_s": round(pf3 / dt3, 1)}
 
 

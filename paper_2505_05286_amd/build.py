@@ -18,6 +18,7 @@ BUILD = os.path.join(PKG, "_build")
 
 SOURCES = [
     "sched.cpp",
+    "decode_plan.cpp",
     "api.cpp",
     "ops.cpp",
     "executor.hip",

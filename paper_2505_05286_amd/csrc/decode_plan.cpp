@@ -1,0 +1,116 @@
+// Decode-attention work list: prefix groups, partitions, partial slots.
+#include "decode_plan.hpp"
+
+#include <algorithm>
+
+namespace hxf {
+
+namespace {
+
+struct Stream {
+  int64_t len;      // tokens
+  int first;        // first token
+  int rows[kDecodeRows];
+  int n_rows;       // sequences served (indices into seqs)
+  int slot_off;     // offset of this stream's pieces inside each row's slot block
+};
+
+}  // namespace
+
+void plan_decode(const std::vector<DecodeSeq>& seqs, int hkv, int G, DecodePlan& out) {
+  out.items.clear();
+  out.merges.clear();
+  out.n_parts = 0;
+  out.kv_tokens = 0;
+  const int n = (int)seqs.size();
+  if (n == 0) return;
+  const int R = std::max(1, std::min(kDecodeRows, 16 / G));
+
+  // prefix groups: equal first page, shared length = the shortest common run of full pages
+  std::vector<int> order, shared(n, 0);
+  for (int i = 0; i < n; ++i)
+    if (seqs[i].pages) order.push_back(i);
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int a, int b) { return seqs[a].pages[0] < seqs[b].pages[0]; });
+  std::vector<std::vector<int>> groups;
+  const int n_known = (int)order.size();
+  for (int i = 0; i < n_known;) {
+    int j = i + 1;
+    while (j < n_known && seqs[order[j]].pages[0] == seqs[order[i]].pages[0]) ++j;
+    if (j - i >= 2) {
+      const DecodeSeq& lead = seqs[order[i]];
+      int s = lead.ctx / kPage;
+      for (int k = i + 1; k < j; ++k) {
+        const DecodeSeq& m = seqs[order[k]];
+        int c = 0;
+        const int lim = std::min(s, m.ctx / kPage);
+        while (c < lim && m.pages[c] == lead.pages[c]) ++c;
+        s = c;
+      }
+      if (s > 0) {
+        std::vector<int> g(order.begin() + i, order.begin() + j);
+        std::sort(g.begin(), g.end());
+        for (int k : g) shared[k] = s * kPage;
+        groups.push_back(std::move(g));
+      }
+    }
+    i = j;
+  }
+
+  // streams: shared prefixes (R sequences at a time), then every sequence's own tokens
+  std::vector<Stream> streams;
+  for (const auto& g : groups) {
+    for (size_t c = 0; c < g.size(); c += R) {
+      Stream st{shared[g[0]], 0, {0}, 0, 0};
+      for (size_t k = c; k < g.size() && k < c + R; ++k) st.rows[st.n_rows++] = g[k];
+      streams.push_back(st);
+    }
+  }
+  for (int i = 0; i < n; ++i)
+    if (seqs[i].ctx > shared[i]) {
+      Stream st{seqs[i].ctx - shared[i], shared[i], {i}, 1, 0};
+      streams.push_back(st);
+    }
+  int64_t total = 0;
+  for (const auto& st : streams) total += st.len;
+  const int64_t target = decode_target_tokens(total, (int64_t)streams.size(), hkv);
+
+  // pieces per stream; slot blocks per sequence (shared pieces first, then own pieces)
+  std::vector<int> plen(streams.size()), npieces(streams.size()), nslots(n, 0);
+  for (size_t k = 0; k < streams.size(); ++k) {
+    plen[k] = decode_part_len((int)streams[k].len, target);
+    npieces[k] = (int)((streams[k].len + plen[k] - 1) / plen[k]);
+    streams[k].slot_off = nslots[streams[k].rows[0]];
+    for (int r = 0; r < streams[k].n_rows; ++r) nslots[streams[k].rows[r]] += npieces[k];
+  }
+  std::vector<int64_t> base(n);   // slot of (sequence i, kv-head 0); kv-head h adds h * nslots[i]
+  int64_t slot = 0;
+  for (int i = 0; i < n; ++i) {
+    base[i] = slot;
+    slot += (int64_t)hkv * nslots[i];
+    for (int h = 0; h < hkv; ++h)
+      out.merges.push_back(MergeItem{seqs[i].entry, h, (int32_t)(base[i] + (int64_t)h * nslots[i]), nslots[i]});
+  }
+  out.n_parts = slot;
+  for (size_t k = 0; k < streams.size(); ++k) {
+    const Stream& st = streams[k];
+    for (int h = 0; h < hkv; ++h)
+      for (int p = 0; p < npieces[k]; ++p) {
+        DecodeItem it{};
+        it.kvh = h;
+        it.t0 = st.first + p * plen[k];
+        it.t1 = (int)std::min<int64_t>(st.first + st.len, (int64_t)it.t0 + plen[k]);
+        it.n_rows = st.n_rows;
+        for (int r = 0; r < kDecodeRows; ++r) {
+          const int i = st.rows[std::min(r, st.n_rows - 1)];
+          it.entry[r] = seqs[i].entry;
+          it.part[r] = (int32_t)(base[i] + (int64_t)h * nslots[i] + st.slot_off + p);
+        }
+        out.kv_tokens += it.t1 - it.t0;
+        out.items.push_back(it);
+      }
+  }
+  order_decode_items(out.items.data(), out.items.size());
+}
+
+}  // namespace hxf

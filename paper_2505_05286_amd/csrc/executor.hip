@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstring>
 
+#include "decode_plan.hpp"
 #include "kernels/kernels.hpp"
 
 namespace hxf {
@@ -64,14 +65,15 @@ WsPlan plan_workspace(const hxf_model_cfg& m, const hxf_sched_cfg& s) {
   p.r_max = s.max_seqs;
   p.e_max = s.max_seqs;
   p.bt_w = ceil_div(m.max_context, kPage);
-  p.dec_items_max = (int64_t)s.max_seqs * hkv * ceil_div(m.max_context, kDecodeMinPartition);
+  p.dec_items_max = decode_parts_bound(s.max_seqs, hkv, m.max_context);
   p.merges_max = (int64_t)s.max_seqs * hkv;
   const int qpi = prefill_queries_per_item((int)G);
   p.pf_items_max = hkv * (ceil_div(s.chunk_tokens, qpi) + s.max_seqs);
   // metadata (int32 words), sections packed in this order, each 64-word aligned
   auto words = [](int64_t n) { return (n + 63) & ~int64_t(63); };
   const int64_t meta_words = words(p.t_max) * 3 + words(p.r_max) + words(p.e_max) * 2 +
-                             words(p.e_max * p.bt_w) + words(p.dec_items_max * 8) + words(p.merges_max * 4) +
+                             words(p.e_max * p.bt_w) + words(p.dec_items_max * (int64_t)(sizeof(DecodeItem) / 4)) +
+                             words(p.merges_max * 4) +
                              words(p.pf_items_max * 4);
   p.meta_bytes = meta_words * 4;
   // split-K partials: largest splits*M*N over the GEMM shapes at M <= 256
@@ -168,6 +170,7 @@ class HipExecutor : public Executor {
   void* host_meta_ = nullptr;
   int32_t* host_sampled_ = nullptr;
   std::vector<uint64_t> last_rows_;   // request id per logits row of the last iteration
+  DecodePlan dplan_;                  // decode-attention work list of the current iteration
   bool ev_ = false;
   std::vector<hipEvent_t> ev_pool_, ev_merge_;
 };
@@ -203,15 +206,12 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   const int G = hq / hkv;
   const int qkv_w = (hq + 2 * hkv) * dh;
   int T = 0, R = 0, n_dec = 0, bt_w = 1;
-  int64_t dec_ctx = 0;
   for (const auto& e : batch) {
     T += e.n;
     R += e.logits ? 1 : 0;
     n_dec += e.decode ? 1 : 0;
-    if (e.decode) dec_ctx += (int64_t)e.pos0 + 1;
     bt_w = std::max<int>(bt_w, (int)ceil_div((int64_t)e.pos0 + e.n, kPage));
   }
-  const int64_t dec_target = decode_target_tokens(dec_ctx, n_dec, hkv);
   if (T > plan_.t_max || R > plan_.r_max || E > plan_.e_max) {
     err = "run: batch exceeds the workspace plan";
     return HXF_EINVAL;
@@ -223,9 +223,8 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   const int64_t o_ids = sec(T), o_pos = sec(T), o_slot = sec(T), o_lrow = sec(R), o_row0 = sec(E), o_pos0 = sec(E),
                 o_bt = sec((int64_t)E * bt_w);
   int row = 0, r = 0;
-  int n_part = 0;
-  std::vector<DecodeItem> ditems;
-  std::vector<MergeItem> merges;
+  std::vector<DecodeSeq> dseqs;
+  dseqs.reserve(n_dec);
   std::vector<PrefillItem> pitems;
   const int qpi = prefill_queries_per_item(G);
   last_rows_.clear();
@@ -247,33 +246,28 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     const int np = (int)ceil_div((int64_t)be.pos0 + be.n, kPage);
     for (int j = 0; j < bt_w; ++j) hm[o_bt + (int64_t)e * bt_w + j] = j < np ? bt[j] : 0;
     if (be.decode) {
-      const int ctx = be.pos0 + 1;
-      const int plen = decode_part_len(ctx, dec_target);
-      for (int h = 0; h < hkv; ++h) {
-        MergeItem mi{e, h, n_part, 0};
-        for (int t0 = 0; t0 < ctx; t0 += plen) {
-          ditems.push_back(DecodeItem{e, h, t0, std::min(ctx, t0 + plen), n_part++, 0, 0, 0});
-          ++mi.n_part;
-        }
-        merges.push_back(mi);
-      }
+      dseqs.push_back(DecodeSeq{e, be.pos0 + 1, bt.data()});
     } else {
       for (int h = 0; h < hkv; ++h)
         for (int q0 = 0; q0 < be.n; q0 += qpi) pitems.push_back(PrefillItem{e, h, q0, std::min(qpi, be.n - q0)});
     }
     row += be.n;
   }
-  if ((int64_t)ditems.size() > plan_.dec_items_max || (int64_t)pitems.size() > plan_.pf_items_max) {
+  plan_decode(dseqs, hkv, G, dplan_);
+  const std::vector<DecodeItem>& ditems = dplan_.items;
+  const std::vector<MergeItem>& merges = dplan_.merges;
+  if ((int64_t)ditems.size() > plan_.dec_items_max || dplan_.n_parts > plan_.dec_items_max ||
+      (int64_t)pitems.size() > plan_.pf_items_max) {
     err = "run: attention work list exceeds the workspace plan";
     return HXF_EINVAL;
   }
-  const int64_t o_ditems = sec((int64_t)ditems.size() * 8), o_merges = sec((int64_t)merges.size() * 4),
+  constexpr int64_t kItemWords = sizeof(DecodeItem) / 4;
+  const int64_t o_ditems = sec((int64_t)ditems.size() * kItemWords), o_merges = sec((int64_t)merges.size() * 4),
                 o_pitems = sec((int64_t)pitems.size() * 4);
   if (w * 4 > plan_.meta_bytes) {
     err = "run: metadata exceeds the workspace plan";
     return HXF_EINVAL;
   }
-  order_decode_items(ditems.data(), ditems.size());
   std::memcpy(hm + o_ditems, ditems.data(), ditems.size() * sizeof(DecodeItem));
   std::memcpy(hm + o_merges, merges.data(), merges.size() * sizeof(MergeItem));
   std::memcpy(hm + o_pitems, pitems.data(), pitems.size() * sizeof(PrefillItem));
@@ -327,8 +321,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   pa.dh = dh;
   pa.scale_log2 = scale_log2;
 
-  int64_t kv_tokens = 0;
-  for (const auto& it : ditems) kv_tokens += it.t1 - it.t0;
+  const int64_t kv_tokens = dplan_.kv_tokens;
 
   HXF_HIP(embed_rmsnorm_launch(dm + o_ids, (const uint16_t*)b_.embed, (const uint16_t*)layers_[0].attn_norm, resid,
                                h, T, d, m_.rms_eps, st_));

@@ -170,6 +170,8 @@ __device__ __forceinline__ void load_q(bf16x8* qf, const uint16_t* qrow, bool ok
     qf[s] = ok ? as_bf16x8(*reinterpret_cast<const uint4*>(qrow + s * 32 + rq * 8)) : as_bf16x8(make_uint4(0, 0, 0, 0));
 }
 
+static_assert(kDecodeRows == 4, "the row selects below assume four rows");
+
 template <int DH>
 __global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
   const int lane = threadIdx.x;
@@ -177,21 +179,26 @@ __global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
   if (w >= a.n_items) return;
   const DecodeItem it = a.items[w];
   const int G = a.Hq / a.Hkv;
+  // column (lane % 16) = (row, head of the group); rows past n_rows are idle columns
   const int col = lane & 15;
-  const bool ok = col < G;
-  const int head = it.kvh * G + (ok ? col : 0);
+  const int row = col / G, g = col - row * G;
+  const bool ok = row < it.n_rows && row < kDecodeRows;
+  const int r = ok ? row : 0;
+  const int entry = r == 0 ? it.entry[0] : r == 1 ? it.entry[1] : r == 2 ? it.entry[2] : it.entry[3];
+  const int part = r == 0 ? it.part[0] : r == 1 ? it.part[1] : r == 2 ? it.part[2] : it.part[3];
+  const int head = it.kvh * G + (ok ? g : 0);
   bf16x8 qf[DH / 32];
-  load_q<DH>(qf, a.q + (size_t)a.q_row[it.entry] * a.q_stride + head * DH, ok, lane);
+  load_q<DH>(qf, a.q + (size_t)a.q_row[entry] * a.q_stride + head * DH, ok, lane);
   AttnState<DH> S;
-  attn_range<DH, false>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)it.entry * a.bt_stride, a.n_blocks, it.kvh, it.t0,
-                        it.t1, 0x7FFFFFFF, a.scale_log2, lane);
+  attn_range<DH, false>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)it.entry[0] * a.bt_stride, a.n_blocks, it.kvh,
+                        it.t0, it.t1, 0x7FFFFFFF, a.scale_log2, lane);
   if (!ok) return;
   const int rq = lane >> 4;
-  float* o = a.part_o + ((size_t)it.part * G + col) * DH;
+  float* o = a.part_o + ((size_t)part * G + g) * DH;
 #pragma unroll
   for (int n = 0; n < DH / 16; ++n)
     *reinterpret_cast<float4*>(o + n * 16 + rq * 4) = make_float4(S.acc[n][0], S.acc[n][1], S.acc[n][2], S.acc[n][3]);
-  if (rq == 0) *reinterpret_cast<float2*>(a.part_ml + ((size_t)it.part * G + col) * 2) = make_float2(S.m, S.l);
+  if (rq == 0) *reinterpret_cast<float2*>(a.part_ml + ((size_t)part * G + g) * 2) = make_float2(S.m, S.l);
 }
 
 // Log-sum-exp merge of the split-K partials; one wavefront per (entry, q-head).

@@ -86,10 +86,17 @@ hipError_t kv_scatter_launch(const uint16_t* k, const uint16_t* v, const int32_t
                              uint16_t* v_pool, int64_t n_blocks, int T, int Hkv, int dh, hipStream_t st);
 
 // ------------------------------------------------------------------ attention
-// One decode work item: tokens [t0, t1) of batch entry `entry`, kv-head `kvh`;
-// its partial result goes to slot `part`.
+// One decode work item: tokens [t0, t1) of kv-head `kvh`, read through the block
+// table of entry[0], attended by the queries of entries entry[0 .. n_rows) (more
+// than one when they share those pages: forks of one parent); row r's partial
+// result goes to slot part[r].  The 16 query columns of a wavefront are (row, head)
+// pairs, so at most min(kDecodeRows, 16 / G) rows.
+constexpr int kDecodeRows = 4;
 struct DecodeItem {
-  int32_t entry, kvh, t0, t1, part, pad0, pad1, pad2;
+  int32_t kvh, t0, t1, n_rows;
+  int32_t entry[kDecodeRows];
+  int32_t part[kDecodeRows];
+  int32_t pad[4];
 };
 // Launch order of the decode items: longest first (equal lengths keep their
 // order), so that the wavefronts that start last, when the chip drains, are the

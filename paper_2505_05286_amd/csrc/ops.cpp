@@ -6,6 +6,7 @@
 #include <cstring>
 #include <vector>
 
+#include "decode_plan.hpp"
 #include "executor.hpp"
 #include "hxf_ops.h"
 #include "kernels/kernels.hpp"
@@ -19,31 +20,28 @@ int64_t al(int64_t x) { return (x + 255) & ~int64_t(255); }
 int dev_rc(hipError_t e) { return e == hipSuccess ? HXF_OK : HXF_EDEVICE; }
 
 struct DecodeLayout {
-  int64_t items = 0, merges = 0, off_items = 0, off_merges = 0, off_qrow = 0, off_o = 0, off_ml = 0, total = 0;
+  int64_t items = 0, merges = 0, parts = 0, off_items = 0, off_merges = 0, off_qrow = 0, off_o = 0, off_ml = 0,
+          total = 0;
 };
 
-// Partition target of a decode batch (the same split the executor uses).
-int64_t decode_target(int B, int Hkv, const int32_t* ctx) {
-  int64_t sum = 0;
-  for (int b = 0; b < B; ++b) sum += std::max(ctx[b], 1);
-  return decode_target_tokens(sum, B, Hkv);
+void decode_seqs(int B, const int32_t* ctx, const int32_t* bt_host, int bt_stride, std::vector<DecodeSeq>& seqs) {
+  seqs.clear();
+  for (int b = 0; b < B; ++b)
+    seqs.push_back(DecodeSeq{b, std::max(ctx[b], 1), bt_host ? bt_host + (size_t)b * bt_stride : nullptr});
 }
 
-DecodeLayout decode_layout(int B, int Hq, int Hkv, int dh, const int32_t* ctx) {
+DecodeLayout decode_layout(const DecodePlan& P, int B, int Hq, int Hkv, int dh) {
   DecodeLayout L;
-  const int64_t target = decode_target(B, Hkv, ctx);
-  for (int b = 0; b < B; ++b) {
-    const int c = std::max(ctx[b], 1);
-    L.items += (int64_t)Hkv * ((c + decode_part_len(c, target) - 1) / decode_part_len(c, target));
-  }
+  L.items = (int64_t)P.items.size();
   L.merges = (int64_t)B * Hkv;
+  L.parts = P.n_parts;
   const int G = Hq / Hkv;
   int64_t o = 0;
   L.off_items = o; o = al(o + L.items * (int64_t)sizeof(DecodeItem));
   L.off_merges = o; o = al(o + L.merges * (int64_t)sizeof(MergeItem));
   L.off_qrow = o; o = al(o + (int64_t)B * 4);
-  L.off_o = o; o = al(o + L.items * G * dh * 4);
-  L.off_ml = o; o = al(o + L.items * G * 2 * 4);
+  L.off_o = o; o = al(o + L.parts * G * dh * 4);
+  L.off_ml = o; o = al(o + L.parts * G * 2 * 4);
   L.total = o;
   return L;
 }
@@ -132,41 +130,54 @@ int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k
                                   (uint16_t*)v_pool, n_blocks, T, Hkv, dh, (hipStream_t)stream));
 }
 
-int64_t hxf_op_decode_attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t dh, const int32_t* ctx) {
-  if (B < 0 || !ctx || !shapes_ok(Hq, Hkv, dh)) return -1;
-  return decode_layout(B, Hq, Hkv, dh, ctx).total;
+int64_t hxf_op_decode_attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t dh, const int32_t* ctx,
+                                                const int32_t* bt_host, int32_t bt_stride) {
+  if (B < 0 || !ctx || !shapes_ok(Hq, Hkv, dh) || (bt_host && bt_stride <= 0)) return -1;
+  std::vector<DecodeSeq> seqs;
+  decode_seqs(B, ctx, bt_host, bt_stride, seqs);
+  DecodePlan P;
+  plan_decode(seqs, Hkv, Hq / Hkv, P);
+  return decode_layout(P, B, Hq, Hkv, dh).total;
+}
+
+int hxf_op_decode_plan(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* ctx, const int32_t* bt_host, int32_t bt_stride,
+                       int32_t* items, int32_t items_cap, int32_t* n_items, int32_t* merges, int32_t merges_cap,
+                       int32_t* n_merges) {
+  if (B < 0 || !ctx || Hq <= 0 || Hkv <= 0 || Hq % Hkv || Hq / Hkv > 16 || (bt_host && bt_stride <= 0) || !n_items ||
+      !n_merges || (items_cap > 0 && !items) || (merges_cap > 0 && !merges))
+    return HXF_EINVAL;
+  std::vector<DecodeSeq> seqs;
+  decode_seqs(B, ctx, bt_host, bt_stride, seqs);
+  DecodePlan P;
+  plan_decode(seqs, Hkv, Hq / Hkv, P);
+  *n_items = (int32_t)P.items.size();
+  *n_merges = (int32_t)P.merges.size();
+  if ((int64_t)items_cap < (int64_t)P.items.size() || (int64_t)merges_cap < (int64_t)P.merges.size())
+    return HXF_ENOMEM;
+  std::memcpy(items, P.items.data(), P.items.size() * sizeof(DecodeItem));
+  std::memcpy(merges, P.merges.data(), P.merges.size() * sizeof(MergeItem));
+  return HXF_OK;
 }
 
 int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_pool, int64_t n_blocks, const int32_t* bt,
-                            int32_t bt_stride, const int32_t* ctx, void* out, int32_t B, int32_t Hq, int32_t Hkv,
-                            int32_t dh, void* workspace, int64_t ws_bytes, void* stream) {
+                            int32_t bt_stride, const int32_t* ctx, const int32_t* bt_host, void* out, int32_t B,
+                            int32_t Hq, int32_t Hkv, int32_t dh, void* workspace, int64_t ws_bytes, void* stream) {
   if (!q || !k_pool || !v_pool || n_blocks <= 0 || !bt || !ctx || !out || B < 0 || !shapes_ok(Hq, Hkv, dh))
     return HXF_EINVAL;
   if (B == 0) return HXF_OK;
   for (int b = 0; b < B; ++b)
     if (ctx[b] <= 0 || (ctx[b] + kPage - 1) / kPage > bt_stride) return HXF_EINVAL;
-  const DecodeLayout L = decode_layout(B, Hq, Hkv, dh, ctx);
+  std::vector<DecodeSeq> seqs;
+  decode_seqs(B, ctx, bt_host, bt_stride, seqs);
+  DecodePlan P;
+  plan_decode(seqs, Hkv, Hq / Hkv, P);
+  const DecodeLayout L = decode_layout(P, B, Hq, Hkv, dh);
   if (!workspace || ws_bytes < L.total) return HXF_ENOMEM;
   std::vector<uint8_t> host(L.off_o);
-  auto* items = reinterpret_cast<DecodeItem*>(host.data() + L.off_items);
-  auto* merges = reinterpret_cast<MergeItem*>(host.data() + L.off_merges);
+  std::memcpy(host.data() + L.off_items, P.items.data(), P.items.size() * sizeof(DecodeItem));
+  std::memcpy(host.data() + L.off_merges, P.merges.data(), P.merges.size() * sizeof(MergeItem));
   auto* qrow = reinterpret_cast<int32_t*>(host.data() + L.off_qrow);
-  int n = 0;
-  const int64_t target = decode_target(B, Hkv, ctx);
-  for (int b = 0; b < B; ++b) {
-    qrow[b] = b;
-    const int plen = decode_part_len(ctx[b], target);
-    for (int h = 0; h < Hkv; ++h) {
-      MergeItem mi{b, h, n, 0};
-      for (int t0 = 0; t0 < ctx[b]; t0 += plen) {
-        items[n] = DecodeItem{b, h, t0, std::min(ctx[b], t0 + plen), n, 0, 0, 0};
-        ++n;
-        ++mi.n_part;
-      }
-      merges[b * Hkv + h] = mi;
-    }
-  }
-  order_decode_items(items, (size_t)n);
+  for (int b = 0; b < B; ++b) qrow[b] = b;
   hipStream_t st = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
   if (hipMemcpyAsync(ws, host.data(), host.size(), hipMemcpyHostToDevice, st) != hipSuccess) return HXF_EDEVICE;
@@ -180,7 +191,7 @@ int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_poo
   a.bt = bt;
   a.bt_stride = bt_stride;
   a.items = reinterpret_cast<const DecodeItem*>(ws + L.off_items);
-  a.n_items = n;
+  a.n_items = (int)P.items.size();
   a.merges = reinterpret_cast<const MergeItem*>(ws + L.off_merges);
   a.n_merges = (int)L.merges;
   a.part_o = reinterpret_cast<float*>(ws + L.off_o);

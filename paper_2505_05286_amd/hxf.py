@@ -133,10 +133,13 @@ _SIGS = {
     "hxf_op_kv_scatter": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
                                     C.c_int32, C.c_int32, C.c_int32, C.c_void_p]),
     "hxf_op_decode_attention_workspace_bytes": (C.c_int64, [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
-                                                            C.POINTER(C.c_int32)]),
+                                                            C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.c_int32]),
+    "hxf_op_decode_plan": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
+                                     C.c_int32, C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32),
+                                     C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32)]),
     "hxf_op_decode_attention": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p, C.c_int32,
-                                          C.POINTER(C.c_int32), C.c_void_p, C.c_int32, C.c_int32, C.c_int32,
-                                          C.c_int32, C.c_void_p, C.c_int64, C.c_void_p]),
+                                          C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.c_void_p, C.c_int32,
+                                          C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p]),
     "hxf_op_prefill_attention_workspace_bytes": (C.c_int64, [C.c_int32, C.c_int32, C.c_int32,
                                                              C.POINTER(C.c_int32)]),
     "hxf_op_prefill_attention": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p, C.c_int32,
@@ -361,14 +364,34 @@ def op_kv_scatter(k, v, slot, k_pool, v_pool, n_blocks, T, Hkv, dh, stream=0):
         "hxf_op_kv_scatter")
 
 
-def op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, ctx):
+def op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, ctx, bt_host=None, bt_stride=0):
+    """bt_host: the block table [B, bt_stride] on the host (enables shared-prefix grouping) or None."""
     c, cp = _i32(ctx)
-    return lib().hxf_op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, cp)
+    b, bp = _i32(bt_host) if bt_host is not None else (None, None)
+    return lib().hxf_op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, cp, bp, bt_stride)
 
 
-def op_decode_attention(q, k_pool, v_pool, n_blocks, bt, bt_stride, ctx, out, B, Hq, Hkv, dh, ws, ws_bytes, stream=0):
+def op_decode_plan(B, Hq, Hkv, ctx, bt_host=None, bt_stride=0):
+    """The decode-attention work list: (items int32 [n, 16], merges int32 [m, 4])."""
     c, cp = _i32(ctx)
-    _op(lib().hxf_op_decode_attention(q, k_pool, v_pool, n_blocks, bt, bt_stride, cp, out, B, Hq, Hkv, dh, ws,
+    b, bp = _i32(bt_host) if bt_host is not None else (None, None)
+    ni, nm = C.c_int32(0), C.c_int32(0)
+    rc = lib().hxf_op_decode_plan(B, Hq, Hkv, cp, bp, bt_stride, None, 0, C.byref(ni), None, 0, C.byref(nm))
+    if rc not in (OK, ENOMEM):
+        raise HxfError(rc, "hxf_op_decode_plan")
+    items = np.zeros((ni.value, 16), np.int32)
+    merges = np.zeros((nm.value, 4), np.int32)
+    _op(lib().hxf_op_decode_plan(B, Hq, Hkv, cp, bp, bt_stride, items.ctypes.data_as(C.POINTER(C.c_int32)),
+                                 ni.value, C.byref(ni), merges.ctypes.data_as(C.POINTER(C.c_int32)), nm.value,
+                                 C.byref(nm)), "hxf_op_decode_plan")
+    return items, merges
+
+
+def op_decode_attention(q, k_pool, v_pool, n_blocks, bt, bt_stride, ctx, out, B, Hq, Hkv, dh, ws, ws_bytes, stream=0,
+                        bt_host=None):
+    c, cp = _i32(ctx)
+    b, bp = _i32(bt_host) if bt_host is not None else (None, None)
+    _op(lib().hxf_op_decode_attention(q, k_pool, v_pool, n_blocks, bt, bt_stride, cp, bp, out, B, Hq, Hkv, dh, ws,
                                       ws_bytes, stream or None), "hxf_op_decode_attention")
 
 

@@ -1,0 +1,125 @@
+"""The decode-attention work list (host logic, no GPU): every (sequence, kv-head)
+attends to each of its context tokens exactly once, its partials fill a block of
+consecutive slots, shared-prefix items only cover pages the rows really share, and
+the items fill the resident wavefronts without exceeding them."""
+import numpy as np
+import pytest
+
+from paper_2505_05286_amd import hxf
+
+from ._lib import ensure_built
+
+RESIDENT = 2048
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    ensure_built()
+
+
+def _tables(rng, ctxs, groups=()):
+    """Block tables: distinct pages per sequence, except that each group (list of
+    sequence indices) shares the first `shared` pages of its first member."""
+    width = max(-(-c // 16) for c in ctxs)
+    bt = np.full((len(ctxs), width), -1, np.int32)
+    nxt = 0
+    for i, c in enumerate(ctxs):
+        n = -(-c // 16)
+        bt[i, :n] = np.arange(nxt, nxt + n)
+        nxt += n
+    for members, shared in groups:
+        for m in members[1:]:
+            bt[m, :shared] = bt[members[0], :shared]
+    return bt
+
+
+def _check(ctxs, hq, hkv, bt=None):
+    B = len(ctxs)
+    G = hq // hkv
+    items, merges = hxf.op_decode_plan(B, hq, hkv, ctxs, bt, bt.shape[1] if bt is not None else 0)
+    assert merges.shape == (B * hkv, 4)
+    rows_max = min(4, 16 // G)
+    cover = {}          # (seq, kvh) -> list of (t0, t1)
+    slot_owner = {}
+    for it in items:
+        kvh, t0, t1, n_rows = it[:4]
+        ents, parts = it[4:8], it[8:12]
+        assert 1 <= n_rows <= rows_max and 0 <= t0 < t1
+        assert t0 % 16 == 0
+        for r in range(n_rows):
+            e = int(ents[r])
+            assert t1 <= ctxs[e]
+            if r > 0 and bt is not None:   # rows read entry[0]'s pages: they must be theirs too
+                p0, p1 = t0 // 16, -(-t1 // 16)
+                assert np.array_equal(bt[e, p0:p1], bt[ents[0], p0:p1])
+                assert t1 % 16 == 0 and t1 <= (ctxs[e] // 16) * 16     # only full pages are shared
+            cover.setdefault((e, int(kvh)), []).append((int(t0), int(t1)))
+            assert int(parts[r]) not in slot_owner
+            slot_owner[int(parts[r])] = (e, int(kvh))
+    for e, kvh, part0, n_part in merges:
+        ranges = sorted(cover[(int(e), int(kvh))])
+        assert ranges[0][0] == 0 and ranges[-1][1] == ctxs[e]
+        assert all(a[1] == b[0] for a, b in zip(ranges, ranges[1:]))
+        assert len(ranges) == n_part
+        assert all(slot_owner[s] == (e, kvh) for s in range(part0, part0 + n_part))
+    assert len(slot_owner) == sum(int(m[3]) for m in merges)
+    lengths = [int(t1 - t0) for t0, t1 in items[:, 1:3]]
+    assert lengths == sorted(lengths, reverse=True)       # longest first
+    return items, merges
+
+
+@pytest.mark.parametrize("hq,hkv", [(4, 2), (32, 8), (40, 8)])
+def test_plan_covers_every_token_once_without_tables(hq, hkv):
+    rng = np.random.default_rng(hq)
+    ctxs = [1, 15, 16, 17, 255, 256, 257, 1000, 4096, 8191] + [int(c) for c in rng.integers(1, 9000, 40)]
+    items, _ = _check(ctxs, hq, hkv)
+    assert (items[:, 3] == 1).all()
+
+
+def test_plan_fills_but_does_not_exceed_the_resident_wavefronts():
+    rng = np.random.default_rng(2)
+    ctxs = [int(c) for c in np.clip(rng.lognormal(np.log(3000), 0.5, 64), 1024, 8192)]
+    items, _ = _check(ctxs, 32, 8)
+    assert 0.8 * RESIDENT <= len(items) <= RESIDENT
+    # at least as many (sequence, kv-head) pairs as resident wavefronts: one item per pair
+    ctxs = [int(c) for c in rng.integers(1, 5000, 260)]
+    items, _ = _check(ctxs, 32, 8)
+    assert len(items) == 260 * 8
+
+
+def test_plan_shares_fork_prefixes():
+    """Two groups of 8 forks sharing 255 pages (4096-token parents), plus unrelated
+    sequences: the shared pages are read by items of min(4, 16/G) rows."""
+    rng = np.random.default_rng(4)
+    ctxs = [4096 + 16 + int(k) for k in rng.integers(1, 256, 16)] + [3000, 5000]
+    bt = _tables(rng, ctxs, groups=[(list(range(8)), 255), (list(range(8, 16)), 255)])
+    items, _ = _check(ctxs, 32, 8, bt)
+    shared = items[items[:, 3] > 1]
+    assert len(shared) > 0 and (shared[:, 3] == 4).all()
+    assert (shared[:, 2] <= 255 * 16).all()
+    # every fork reads the 4080 shared tokens through shared items only
+    tok = {}
+    for it in shared:
+        for r in range(it[3]):
+            tok[int(it[4 + r]), int(it[0])] = tok.get((int(it[4 + r]), int(it[0])), 0) + int(it[2] - it[1])
+    assert all(tok[(e, h)] == 255 * 16 for e in range(16) for h in range(8))
+    # the (token, kv-head) pairs read drop by the sharing factor on the shared part
+    read = int((items[:, 2] - items[:, 1]).sum())
+    logical = sum(ctxs) * 8
+    assert read == logical - 16 * 8 * 4080 + 4 * 8 * 4080
+
+
+def test_plan_groups_need_a_common_full_page():
+    """Equal first pages with a partial first page (context < 16) or nested forks with
+    different shared lengths: the group shares only what all members share."""
+    rng = np.random.default_rng(5)
+    ctxs = [700, 800, 900, 40]
+    bt = _tables(rng, ctxs, groups=[([0, 1, 2], 30)])
+    bt[2, 20:30] = 10_000 + np.arange(10)          # the third fork diverges after 20 pages
+    items, _ = _check(ctxs, 32, 8, bt)
+    shared = items[items[:, 3] > 1]
+    assert (shared[:, 2] <= 20 * 16).all() and (shared[:, 3] == 3).all()
+    ctxs = [10, 12]
+    bt = _tables(rng, ctxs, groups=[([0, 1], 1)])
+    items, _ = _check(ctxs, 32, 8, bt)
+    assert (items[:, 3] == 1).all()

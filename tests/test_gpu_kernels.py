@@ -254,6 +254,47 @@ def test_decode_attention_one_item_per_pair():
     _decode_case(ctxs, 32, 8, 128, seed=260, sample=sample)
 
 
+@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128)])
+def test_decode_attention_shared_prefix(hq, hkv, dh):
+    """Forks of two parents (255 and 40 shared full pages) decoding together with an
+    unrelated sequence: the shared pages are read once per group of rows, and every
+    fork's output equals attention over its whole context."""
+    t = torch()
+    rng = np.random.default_rng(hq * 3 + dh)
+    parents = [255 * 16, 40 * 16]
+    own = [[int(k) for k in rng.integers(1, 300, 8)], [int(k) for k in rng.integers(1, 40, 5)]]
+    lone = 1234
+    phys = parents + [k for o in own for k in o] + [lone]       # sequences that own pages
+    kp, vp, nb, bt0, bts, Kl, Vl = _fill_paged(rng, phys, hkv, dh)
+    seqs, o = [], len(parents)
+    for g, plen in enumerate(parents):
+        for k in own[g]:
+            seqs.append((plen + k, list(bts[g]) + list(bts[o])))
+            o += 1
+    seqs.append((lone, list(bts[o])))
+    ctxs = [c for c, _ in seqs]
+    B = len(seqs)
+    width = max(len(b) for _, b in seqs)
+    bt = np.zeros((B, width), np.int32)
+    for i, (_, b) in enumerate(seqs):
+        bt[i, :len(b)] = b
+    items, _ = hxf.op_decode_plan(B, hq, hkv, ctxs, bt, width)
+    assert (items[:, 3] > 1).any()
+    log(f"decode attention shared prefix B={B} hq={hq} hkv={hkv} dh={dh} items={len(items)}")
+    qb, qf = rand_bf16(rng, (B, hq, dh))
+    out = empty_i16(B * hq * dh)
+    wsn = hxf.op_decode_attention_workspace_bytes(B, hq, hkv, dh, ctxs, bt, width)
+    ws = t.empty(wsn, dtype=t.uint8, device="cuda:0")
+    q_d, bt_d = dev_bits(qb), i32(bt)
+    hxf.op_decode_attention(q_d.data_ptr(), kp.data_ptr(), vp.data_ptr(), nb, bt_d.data_ptr(), width, ctxs,
+                            out.data_ptr(), B, hq, hkv, dh, ws.data_ptr(), wsn, bt_host=bt)
+    t.cuda.synchronize()
+    got = host_f64(out).reshape(B, hq, dh)
+    for b, (c, pages) in enumerate(seqs):
+        ref = P.paged_attention(qf[b:b + 1], np.array([c - 1]), Kl, Vl, pages, c)[0]
+        np.testing.assert_allclose(got[b], ref, rtol=1e-2, atol=1e-2, err_msg=f"seq {b} ctx {c}")
+
+
 def _prefill_case(chunks, hq, hkv, dh, seed):
     """chunks: list of (pos0, n): n new queries at positions pos0.. over a context of pos0+n."""
     t = torch()
