@@ -497,19 +497,31 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
   for (int i = 0; i < TM; ++i) a_off[i] = ((wm * TM + i) * 2) * 512 + lo;
 #pragma unroll
   for (int j = 0; j < TN; ++j) b_off[j] = (AB + (wn * TN + j) * 2) * 512 + lo;
+  // all fragments of a stage are read first (distinct registers), then the MFMAs; the
+  // scheduling groups interleave one LDS read with one MFMA so that the reads' latency
+  // hides under the matrix pipe instead of stalling it
   auto compute = [&](const bf16_t* base) {
+    bf16x8 fa[2][TM], fb[2][TN];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      bf16x8 fb[TN];
 #pragma unroll
-      for (int j = 0; j < TN; ++j) fb[j] = as_bf16x8(*reinterpret_cast<const uint4*>(base + b_off[j] + q * 256));
+      for (int j = 0; j < TN; ++j) fb[q][j] = as_bf16x8(*reinterpret_cast<const uint4*>(base + b_off[j] + q * 256));
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const bf16x8 fa = as_bf16x8(*reinterpret_cast<const uint4*>(base + a_off[i] + q * 256));
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(fa, fb[j], acc[i][j]);
-      }
+      for (int i = 0; i < TM; ++i) fa[q][i] = as_bf16x8(*reinterpret_cast<const uint4*>(base + a_off[i] + q * 256));
     }
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(fa[q][i], fb[q][j], acc[i][j]);
+    constexpr int RD = 2 * (TM + TN), MF = 2 * TM * TN, PAIRS = RD < MF ? RD : MF;
+    static_for<PAIRS>([&](auto) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+    });
+    if constexpr (MF > PAIRS) __builtin_amdgcn_sched_group_barrier(0x008, MF - PAIRS, 0);
+    if constexpr (RD > PAIRS) __builtin_amdgcn_sched_group_barrier(0x100, RD - PAIRS, 0);
   };
 
   static_for<NSTG - 1>([&](auto ic) { issue(decltype(ic)::value, slot(ic)); });
