@@ -137,6 +137,31 @@ def step_until(inst, now, cond, timed=None, per_step=None):
     return now, it, pf, dec, time.perf_counter() - t0
 
 
+def workload1(reps=20):
+    """The tiny parity configuration end to end (4 requests, prompts 64-256, chunk 128,
+    8 greedy tokens each), repeated; timing is informational (launch-bound)."""
+    import synth
+    from paper_2505_05286_amd import hxf
+    from paper_2505_05286_amd.device import Engine
+    shape, dm = load_model("tiny")
+    reqs = synth.workloads.cfg1(shape.vocab)
+    cost, it = (200_000_000, 50_000, 0, 150_000_000), (150_000_000, 1_000_000, 0, 0)
+    times, iters = [], 0
+    for _ in range(reps):
+        eng = Engine(dm, max_context=512, n_blocks=64, max_seqs=8, chunk_tokens=128, cost_ps=cost, iter_ps=it,
+                     clock=hxf.CLOCK_MEASURED)
+        for r in reqs:
+            eng.inst.submit(0, r.workflow, 0, 0, r.wf_slo_us, r.prompt, r.max_new_tokens)
+        now, n, pf, dec, dt = step_until(eng.inst, 0, lambda i: False)
+        times.append(dt)
+        iters = n
+        del eng
+    t = sorted(times)[len(times) // 2]
+    return {"workload": "1: tiny decoder, 4 requests (prompts 64/128/192/256, chunk 128, 8 tokens each)",
+            "iterations": iters, "ms_per_run_median": round(t * 1e3, 3), "ms_per_iteration": round(t / iters * 1e3, 3),
+            "tokens_per_s": round((640 + 32) / t, 1)}
+
+
 def workload3():
     """Mixed iterations: 32 running decodes (context U[1024, 4096]) co-batched with chunked
     prefill (2048 tokens per iteration) of 16 prompts of length U[2048, 8192]."""
@@ -438,8 +463,8 @@ def main():
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", type=int, default=2, choices=(2, 3, 4, 5),
-                    help="2 (default) prints the benchmark line; 3-5 print per-workload measurements")
+    ap.add_argument("--workload", type=int, default=2, choices=(1, 2, 3, 4, 5),
+                    help="2 (default) prints the benchmark line; 1, 3-5 print per-workload measurements")
     ap.add_argument("--n-workflows", type=int, default=16, help="workload 5: workflows replayed")
     ap.add_argument("--policy", default="pq", choices=("pq", "fcfs", "llf"), help="workload 5: local queue policy")
     ap.add_argument("--attn-kernel-probe", action="store_true",
@@ -467,7 +492,8 @@ def main():
         return
 
     if args.workload != 2:
-        fn = {3: workload3, 4: workload4, 5: lambda: workload5(args.n_workflows, args.policy)}[args.workload]
+        fn = {1: workload1, 3: workload3, 4: workload4,
+              5: lambda: workload5(args.n_workflows, args.policy)}[args.workload]
         print(json.dumps(fn()), flush=True)
         return
 
