@@ -410,6 +410,43 @@ def policy_ablation(n_wf=300):
             "scenarios": out}
 
 
+def gemm_probe(reps=3, M=2080):
+    """Only the four prefill projections of the 8B shape at 2080 rows (a 2048-token chunk
+    plus 32 decodes), `reps` times each, through the library's GEMM entry point with
+    random bf16 operands: the short program the MFMA-counter runs profile."""
+    import torch
+
+    from paper_2505_05286_amd import hxf
+
+    hxf.lib()
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(0)
+    st = torch.cuda.current_stream().cuda_stream
+    shapes = [("qkv", 6144, 4096, hxf.EPI_BF16), ("o", 4096, 4096, hxf.EPI_RESID),
+              ("gate_up", 2 * 14336, 4096, hxf.EPI_SWIGLU), ("down", 4096, 14336, hxf.EPI_RESID)]
+    out = []
+    for name, N, K, epi in shapes:
+        rows = N // 2 if epi == hxf.EPI_SWIGLU else N
+        A = (torch.randn(M, K, device=dev, generator=g) * 0.5).to(torch.bfloat16)
+        packed = []
+        for _ in range(2 if epi == hxf.EPI_SWIGLU else 1):
+            W = (torch.randn(rows, K, device=dev, generator=g) * 0.02).to(torch.bfloat16)
+            P = torch.empty(hxf.packed_weight_bytes(rows, K) // 2, dtype=torch.int16, device=dev)
+            hxf.op_pack_weight(W.data_ptr(), rows, K, P.data_ptr(), st)
+            packed.append(P)
+        n_out = rows
+        C = torch.zeros(M, n_out, device=dev, dtype=torch.bfloat16 if epi in (hxf.EPI_BF16, hxf.EPI_SWIGLU)
+                        else torch.float32)
+        wsn = hxf.op_gemm_workspace_bytes(M, N, K)
+        ws = torch.empty(max(wsn, 256), dtype=torch.uint8, device=dev)
+        for _ in range(reps):
+            hxf.op_gemm(A.data_ptr(), K, packed[0].data_ptr(), packed[-1].data_ptr() if len(packed) > 1 else 0,
+                        C.data_ptr(), n_out, M, N, K, epi, ws.data_ptr(), ws.numel(), st)
+        torch.cuda.synchronize()
+        out.append({"gemm": name, "M": M, "N": N, "K": K, "flops": 2 * M * N * K, "launches": reps})
+    return {"probe": "prefill GEMMs at 2080 rows", "gemms": out}
+
+
 def attn_kernel_probe(reps=8):
     """Only the paged decode-attention kernel (plus its merge) on the benchmark's
     64 contexts, `reps` times, then one 1 GiB device copy of known size: the short
@@ -469,6 +506,8 @@ def main():
     ap.add_argument("--policy", default="pq", choices=("pq", "fcfs", "llf"), help="workload 5: local queue policy")
     ap.add_argument("--attn-kernel-probe", action="store_true",
                     help="run only the decode-attention kernel and a calibration copy (for counter runs)")
+    ap.add_argument("--gemm-probe", action="store_true",
+                    help="run only the four 2080-row prefill GEMMs (for MFMA counter runs)")
     ap.add_argument("--policy-ablation", action="store_true",
                     help="PQ / FCFS / LLF on config-5 workflows, virtual clock, scheduler only (CPU)")
     ap.add_argument("--calibrate", choices=("llama8b", "qwen32b"),
@@ -481,6 +520,10 @@ def main():
 
     if args.attn_kernel_probe:
         print(json.dumps(attn_kernel_probe()), flush=True)
+        return
+
+    if args.gemm_probe:
+        print(json.dumps(gemm_probe()), flush=True)
         return
 
     if args.calibrate:
