@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 
 #include "decode_plan.hpp"
@@ -71,7 +72,7 @@ WsPlan plan_workspace(const hxf_model_cfg& m, const hxf_sched_cfg& s) {
   p.pf_items_max = hkv * (ceil_div(s.chunk_tokens, qpi) + s.max_seqs);
   // metadata (int32 words), sections packed in this order, each 64-word aligned
   auto words = [](int64_t n) { return (n + 63) & ~int64_t(63); };
-  const int64_t meta_words = words(p.t_max) * 3 + words(p.r_max) + words(p.e_max) * 2 +
+  const int64_t meta_words = words(1) + words(p.t_max) * 3 + words(p.r_max) + words(p.e_max) * 2 +
                              words(p.e_max * p.bt_w) + words(p.dec_items_max * (int64_t)(sizeof(DecodeItem) / 4)) +
                              words(p.merges_max * 4) +
                              words(p.pf_items_max * 4);
@@ -126,9 +127,13 @@ class HipExecutor : public Executor {
     layers_.assign(b.layers, b.layers + m.n_layers);
     plan_ = plan_workspace(m, s);
     ws_ = reinterpret_cast<uint8_t*>(b.workspace);
+    const char* ng = std::getenv("HXF_NO_GRAPHS");
+    use_graphs_ = !(ng && ng[0] && ng[0] != '0');
   }
 
   ~HipExecutor() override {
+    drop_graphs();
+    if (graph_st_) (void)hipStreamDestroy(graph_st_);
     if (host_meta_) (void)hipHostFree(host_meta_);
     if (host_sampled_) (void)hipHostFree(host_sampled_);
     if (ev_) {
@@ -173,6 +178,23 @@ class HipExecutor : public Executor {
   DecodePlan dplan_;                  // decode-attention work list of the current iteration
   bool ev_ = false;
   std::vector<hipEvent_t> ev_pool_, ev_merge_;
+  // Decode-only iterations replay a captured HIP graph of the whole forward (metadata
+  // upload, every kernel, sampled ids back), keyed by the batch's launch shape; the
+  // graph reads the per-iteration metadata from the pinned staging buffer.
+  struct GraphRec {
+    int64_t key = 0;
+    hipGraphExec_t exec = nullptr;
+  };
+  std::vector<GraphRec> graphs_;
+  bool use_graphs_ = true;
+  // The legacy null stream cannot be captured: graphs then run on a stream of our own
+  // (blocking, default priority), which the null stream orders against.
+  hipStream_t graph_st_ = nullptr;
+  void drop_graphs() {
+    for (auto& g : graphs_)
+      if (g.exec) (void)hipGraphExecDestroy(g.exec);
+    graphs_.clear();
+  }
 };
 
 int HipExecutor::gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M,
@@ -217,9 +239,21 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     return HXF_EINVAL;
   }
   // ---------------------------------------------------------- metadata
+  // A decode-only batch uses a layout that depends only on its launch shape (E rows,
+  // block tables padded to a multiple of 64 pages, a fixed work-item capacity), so that
+  // its forward can be captured once and replayed; the decode-attention grid is then
+  // that capacity and the kernel reads the real item count from the metadata.
+  // (Profiling stamps the attention kernels' own start and end, which a captured graph
+  // cannot, so profiled iterations launch eagerly.)
+  const bool pure_decode = E > 0 && n_dec == E;
+  const bool graph = pure_decode && use_graphs_ && !prof.on;
+  if (graph) bt_w = (int)std::min<int64_t>(plan_.bt_w, ((bt_w + 63) / 64) * 64);
+  const int64_t item_cap =
+      graph ? std::min<int64_t>(plan_.dec_items_max, std::max<int64_t>(kDecodeResident, 2LL * E * hkv)) : 0;
   int32_t* hm = reinterpret_cast<int32_t*>(host_meta_);
   int64_t w = 0;
   auto sec = [&](int64_t n) { int64_t at = w; w += (n + 63) & ~int64_t(63); return at; };
+  const int64_t o_nitems = sec(1);
   const int64_t o_ids = sec(T), o_pos = sec(T), o_slot = sec(T), o_lrow = sec(R), o_row0 = sec(E), o_pos0 = sec(E),
                 o_bt = sec((int64_t)E * bt_w);
   int row = 0, r = 0;
@@ -257,22 +291,22 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   const std::vector<DecodeItem>& ditems = dplan_.items;
   const std::vector<MergeItem>& merges = dplan_.merges;
   if ((int64_t)ditems.size() > plan_.dec_items_max || dplan_.n_parts > plan_.dec_items_max ||
-      (int64_t)pitems.size() > plan_.pf_items_max) {
+      (int64_t)pitems.size() > plan_.pf_items_max || (graph && (int64_t)ditems.size() > item_cap)) {
     err = "run: attention work list exceeds the workspace plan";
     return HXF_EINVAL;
   }
   constexpr int64_t kItemWords = sizeof(DecodeItem) / 4;
-  const int64_t o_ditems = sec((int64_t)ditems.size() * kItemWords), o_merges = sec((int64_t)merges.size() * 4),
-                o_pitems = sec((int64_t)pitems.size() * 4);
+  const int64_t o_ditems = sec((graph ? item_cap : (int64_t)ditems.size()) * kItemWords),
+                o_merges = sec((int64_t)merges.size() * 4), o_pitems = sec((int64_t)pitems.size() * 4);
   if (w * 4 > plan_.meta_bytes) {
     err = "run: metadata exceeds the workspace plan";
     return HXF_EINVAL;
   }
+  hm[o_nitems] = (int32_t)ditems.size();
   std::memcpy(hm + o_ditems, ditems.data(), ditems.size() * sizeof(DecodeItem));
   std::memcpy(hm + o_merges, merges.data(), merges.size() * sizeof(MergeItem));
   std::memcpy(hm + o_pitems, pitems.data(), pitems.size() * sizeof(PrefillItem));
   int32_t* dm = dev<int32_t>(plan_.off_meta);
-  HXF_HIP(hipMemcpyAsync(dm, hm, w * 4, hipMemcpyHostToDevice, st_));
 
   // ---------------------------------------------------------- forward
   float* resid = dev<float>(plan_.off_resid);
@@ -293,7 +327,8 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   da.bt = dm + o_bt;
   da.bt_stride = bt_w;
   da.items = reinterpret_cast<const DecodeItem*>(dm + o_ditems);
-  da.n_items = (int)ditems.size();
+  da.n_items = graph ? (int)item_cap : (int)ditems.size();
+  da.n_items_dev = graph ? dm + o_nitems : nullptr;
   da.merges = reinterpret_cast<const MergeItem*>(dm + o_merges);
   da.n_merges = (int)merges.size();
   da.part_o = dev<float>(plan_.off_attn_o);
@@ -322,78 +357,122 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   pa.scale_log2 = scale_log2;
 
   const int64_t kv_tokens = dplan_.kv_tokens;
-
-  HXF_HIP(embed_rmsnorm_launch(dm + o_ids, (const uint16_t*)b_.embed, (const uint16_t*)layers_[0].attn_norm, resid,
-                               h, T, d, m_.rms_eps, st_));
-  // Split-K GEMMs of decode-sized batches hand their partials to the next kernel
-  // (RoPE/KV write, residual add + RMSNorm), which sums them in split order.
-  float* part = dev<float>(plan_.off_part);
-  int pend_down = 0;
-  for (int l = 0; l < m_.n_layers; ++l) {
-    const hxf_layer_weights& L = layers_[l];
-    uint16_t* kp = pool + (int64_t)l * 2 * layer_pool;
-    uint16_t* vp = kp + layer_pool;
-    if (l > 0)
-      HXF_HIP(resid_rmsnorm_launch(resid, part, pend_down, T, nullptr, (const uint16_t*)L.attn_norm, h, T, d,
-                                   m_.rms_eps, st_));
-    int pend_qkv = 0;
-    if (int rc = gemm(h, d, (const uint16_t*)L.wqkv, nullptr, qkv, qkv_w, T, qkv_w, d, EPI_BF16, err, &pend_qkv))
-      return rc;
-    if (pend_qkv)
-      HXF_HIP(rope_kv_partials_launch(qkv, part, pend_qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq,
-                                      hkv, dh, st_));
-    else
-      HXF_HIP(rope_kv_launch(qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq, hkv, dh, st_));
-    da.k_pool = pa.k_pool = kp;
-    da.v_pool = pa.v_pool = vp;
-    if (da.n_items) {
-      hipEvent_t e0 = nullptr, e1 = nullptr;
-      if (prof.on) {
-        HXF_HIP(hipEventCreate(&e0));
-        HXF_HIP(hipEventCreate(&e1));
-      }
-      HXF_HIP(decode_attn_launch(da, st_, e0, e1));
-      if (prof.on) {
-        ev_pool_.push_back(e0);
-        ev_pool_.push_back(e1);
-        prof.decode_attn_launches += 1;
-        prof.decode_attn_bytes += kv_tokens * 2 * dh * 2;
-      }
-      hipEvent_t e2 = nullptr, e3 = nullptr;
-      if (prof.on) {
-        HXF_HIP(hipEventCreate(&e2));
-        HXF_HIP(hipEventCreate(&e3));
-      }
-      HXF_HIP(decode_merge_launch(da, st_, e2, e3));
-      if (prof.on) {
-        ev_merge_.push_back(e2);
-        ev_merge_.push_back(e3);
-      }
-    }
-    HXF_HIP(prefill_attn_launch(pa, st_));
-    int pend_o = 0;
-    if (int rc = gemm(attn, hq * dh, (const uint16_t*)L.wo, nullptr, resid, d, T, d, hq * dh, EPI_RESID, err, &pend_o))
-      return rc;
-    HXF_HIP(resid_rmsnorm_launch(resid, part, pend_o, T, nullptr, (const uint16_t*)L.ffn_norm, h, T, d, m_.rms_eps,
-                                 st_));
-    if (int rc = gemm(h, d, (const uint16_t*)L.w_gate, (const uint16_t*)L.w_up, act, f, T, 2 * f, d, EPI_SWIGLU, err))
-      return rc;
-    if (int rc = gemm(act, f, (const uint16_t*)L.w_down, nullptr, resid, d, T, d, f, EPI_RESID, err, &pend_down))
-      return rc;
-  }
   uint16_t* hr = dev<uint16_t>(plan_.off_hr);
   float* logits = dev<float>(plan_.off_logits);
   int32_t* samp = dev<int32_t>(plan_.off_sampled);
-  if (R > 0) {
-    // (rows without logits never need the last down projection's partials)
-    HXF_HIP(resid_rmsnorm_launch(resid, part, pend_down, T, dm + o_lrow, (const uint16_t*)b_.final_norm, hr, R, d,
-                                 m_.rms_eps, st_));
-    if (int rc = gemm(hr, d, (const uint16_t*)b_.lm_head, nullptr, logits, m_.vocab, R, m_.vocab, d, EPI_F32, err))
-      return rc;
-    HXF_HIP(argmax_launch(logits, samp, R, m_.vocab, st_));
-    HXF_HIP(hipMemcpyAsync(host_sampled_, samp, (size_t)R * 4, hipMemcpyDeviceToHost, st_));
+
+  // The launch sequence (eager, or recorded by a stream capture).
+  auto forward = [&]() -> int {
+    HXF_HIP(hipMemcpyAsync(dm, hm, w * 4, hipMemcpyHostToDevice, st_));
+    HXF_HIP(embed_rmsnorm_launch(dm + o_ids, (const uint16_t*)b_.embed, (const uint16_t*)layers_[0].attn_norm,
+                                 resid, h, T, d, m_.rms_eps, st_));
+    // Split-K GEMMs of decode-sized batches hand their partials to the next kernel
+    // (RoPE/KV write, residual add + RMSNorm), which sums them in split order.
+    float* part = dev<float>(plan_.off_part);
+    int pend_down = 0;
+    for (int l = 0; l < m_.n_layers; ++l) {
+      const hxf_layer_weights& L = layers_[l];
+      uint16_t* kp = pool + (int64_t)l * 2 * layer_pool;
+      uint16_t* vp = kp + layer_pool;
+      if (l > 0)
+        HXF_HIP(resid_rmsnorm_launch(resid, part, pend_down, T, nullptr, (const uint16_t*)L.attn_norm, h, T, d,
+                                     m_.rms_eps, st_));
+      int pend_qkv = 0;
+      if (int rc = gemm(h, d, (const uint16_t*)L.wqkv, nullptr, qkv, qkv_w, T, qkv_w, d, EPI_BF16, err, &pend_qkv))
+        return rc;
+      if (pend_qkv)
+        HXF_HIP(rope_kv_partials_launch(qkv, part, pend_qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq,
+                                        hkv, dh, st_));
+      else
+        HXF_HIP(rope_kv_launch(qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq, hkv, dh, st_));
+      da.k_pool = pa.k_pool = kp;
+      da.v_pool = pa.v_pool = vp;
+      if (da.n_items) {
+        hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr, e3 = nullptr;
+        if (prof.on) {
+          HXF_HIP(hipEventCreate(&e0));
+          HXF_HIP(hipEventCreate(&e1));
+          HXF_HIP(hipEventCreate(&e2));
+          HXF_HIP(hipEventCreate(&e3));
+        }
+        HXF_HIP(decode_attn_launch(da, st_, e0, e1));
+        HXF_HIP(decode_merge_launch(da, st_, e2, e3));
+        if (prof.on) {
+          ev_pool_.push_back(e0);
+          ev_pool_.push_back(e1);
+          ev_merge_.push_back(e2);
+          ev_merge_.push_back(e3);
+        }
+      }
+      HXF_HIP(prefill_attn_launch(pa, st_));
+      int pend_o = 0;
+      if (int rc =
+              gemm(attn, hq * dh, (const uint16_t*)L.wo, nullptr, resid, d, T, d, hq * dh, EPI_RESID, err, &pend_o))
+        return rc;
+      HXF_HIP(resid_rmsnorm_launch(resid, part, pend_o, T, nullptr, (const uint16_t*)L.ffn_norm, h, T, d, m_.rms_eps,
+                                   st_));
+      if (int rc =
+              gemm(h, d, (const uint16_t*)L.w_gate, (const uint16_t*)L.w_up, act, f, T, 2 * f, d, EPI_SWIGLU, err))
+        return rc;
+      if (int rc = gemm(act, f, (const uint16_t*)L.w_down, nullptr, resid, d, T, d, f, EPI_RESID, err, &pend_down))
+        return rc;
+    }
+    if (R > 0) {
+      // (rows without logits never need the last down projection's partials)
+      HXF_HIP(resid_rmsnorm_launch(resid, part, pend_down, T, dm + o_lrow, (const uint16_t*)b_.final_norm, hr, R, d,
+                                   m_.rms_eps, st_));
+      if (int rc = gemm(hr, d, (const uint16_t*)b_.lm_head, nullptr, logits, m_.vocab, R, m_.vocab, d, EPI_F32, err))
+        return rc;
+      HXF_HIP(argmax_launch(logits, samp, R, m_.vocab, st_));
+      HXF_HIP(hipMemcpyAsync(host_sampled_, samp, (size_t)R * 4, hipMemcpyDeviceToHost, st_));
+    }
+    return HXF_OK;
+  };
+
+  if (!graph) {
+    if (int rc = forward()) return rc;
+    HXF_HIP(hipStreamSynchronize(st_));
+  } else {
+    // every launch of forward() goes to st_: point it at the capture stream meanwhile
+    struct StreamSwap {
+      hipStream_t& ref;
+      hipStream_t saved;
+      ~StreamSwap() { ref = saved; }
+    } swap{st_, st_};
+    if (!st_) {
+      if (!graph_st_) HXF_HIP(hipStreamCreate(&graph_st_));
+      st_ = graph_st_;
+    }
+    const int64_t key = ((int64_t)E << 32) | (int64_t)bt_w;
+    GraphRec* g = nullptr;
+    for (auto& x : graphs_)
+      if (x.key == key) g = &x;
+    if (!g) {
+      if (graphs_.size() >= 16) drop_graphs();
+      GraphRec rec;
+      rec.key = key;
+      HXF_HIP(hipStreamBeginCapture(st_, hipStreamCaptureModeThreadLocal));
+      const int rc = forward();
+      hipGraph_t cg = nullptr;
+      const hipError_t ec = hipStreamEndCapture(st_, &cg);
+      hipError_t ei = hipSuccess;
+      if (rc == HXF_OK && ec == hipSuccess) ei = hipGraphInstantiate(&rec.exec, cg, nullptr, nullptr, 0);
+      if (cg) (void)hipGraphDestroy(cg);
+      if (rc != HXF_OK) return rc;
+      if (ec != hipSuccess || ei != hipSuccess) {
+        err = std::string("HIP graph capture: ") + hipGetErrorString(ec != hipSuccess ? ec : ei);
+        return HXF_EDEVICE;
+      }
+      graphs_.push_back(std::move(rec));
+      g = &graphs_.back();
+    }
+    HXF_HIP(hipGraphLaunch(g->exec, st_));
+    HXF_HIP(hipStreamSynchronize(st_));
   }
-  HXF_HIP(hipStreamSynchronize(st_));
+  if (prof.on && da.n_items) {
+    prof.decode_attn_launches += m_.n_layers;
+    prof.decode_attn_bytes += (int64_t)m_.n_layers * kv_tokens * 2 * dh * 2;
+  }
   if (prof.on) {
     for (size_t i = 0; i + 1 < ev_pool_.size(); i += 2) {
       float ms = 0.f;

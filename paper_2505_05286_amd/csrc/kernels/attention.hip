@@ -176,7 +176,7 @@ template <int DH>
 __global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
   const int lane = threadIdx.x;
   const int w = blockIdx.x;
-  if (w >= a.n_items) return;
+  if (w >= (a.n_items_dev ? *a.n_items_dev : a.n_items)) return;
   const DecodeItem it = a.items[w];
   const int G = a.Hq / a.Hkv;
   // column (lane % 16) = (row, head of the group); rows past n_rows are idle columns
@@ -508,28 +508,30 @@ constexpr int kPrefillPT = 1;
 
 int prefill_queries_per_item(int group) { return 4 * 32 * kPrefillPT / group; }
 
+// With events, they take the kernel's own start and end timestamps; without, a plain
+// launch (the form a stream capture records).
+template <typename K>
+static hipError_t launch_stamped(K kernel, dim3 grid, dim3 block, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
+                                 const DecodeAttnArgs& a) {
+  if (e0 || e1) hipExtLaunchKernelGGL(kernel, grid, block, 0, st, e0, e1, 0, a);
+  else hipLaunchKernelGGL(kernel, grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
 hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (a.n_items <= 0) return hipSuccess;
-  // with events, they take the kernel's own start and end timestamps
-  if (a.dh == 128)
-    hipExtLaunchKernelGGL(decode_attn_kernel<128>, dim3(a.n_items), dim3(64), 0, st, ev_start, ev_stop, 0, a);
-  else if (a.dh == 64)
-    hipExtLaunchKernelGGL(decode_attn_kernel<64>, dim3(a.n_items), dim3(64), 0, st, ev_start, ev_stop, 0, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (a.dh == 128) return launch_stamped(decode_attn_kernel<128>, dim3(a.n_items), dim3(64), st, ev_start, ev_stop, a);
+  if (a.dh == 64) return launch_stamped(decode_attn_kernel<64>, dim3(a.n_items), dim3(64), st, ev_start, ev_stop, a);
+  return hipErrorInvalidValue;
 }
 
 hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (a.n_merges <= 0) return hipSuccess;
   const int jobs = a.n_merges * (a.Hq / a.Hkv);
-  if (a.dh == 128)
-    hipExtLaunchKernelGGL(decode_merge_kernel<128>, dim3((jobs + 3) / 4), dim3(256), 0, st, ev_start, ev_stop, 0, a);
-  else if (a.dh == 64)
-    hipExtLaunchKernelGGL(decode_merge_kernel<64>, dim3((jobs + 3) / 4), dim3(256), 0, st, ev_start, ev_stop, 0, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  const dim3 grid((jobs + 3) / 4);
+  if (a.dh == 128) return launch_stamped(decode_merge_kernel<128>, grid, dim3(256), st, ev_start, ev_stop, a);
+  if (a.dh == 64) return launch_stamped(decode_merge_kernel<64>, grid, dim3(256), st, ev_start, ev_stop, a);
+  return hipErrorInvalidValue;
 }
 
 hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st) {

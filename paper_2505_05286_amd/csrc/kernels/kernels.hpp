@@ -139,7 +139,8 @@ struct DecodeAttnArgs {
   const int32_t* bt;       // [entries][bt_stride]
   int bt_stride;
   const DecodeItem* items;
-  int n_items;
+  int n_items;                 // items, or the launch's capacity when n_items_dev is set
+  const int32_t* n_items_dev;  // may be null: the item count in device memory (captured launches)
   const MergeItem* merges;
   int n_merges;
   float* part_o;           // [parts][G][dh]

@@ -207,3 +207,47 @@ def test_policy_does_not_change_tokens_and_runs_are_deterministic():
     assert out[0][0] == out[1][0] == out[2][0]
     for a, b in zip(out[0][1], out[2][1]):
         np.testing.assert_array_equal(a, b)          # same policy twice: bit-identical logits
+
+
+@pytest.mark.parametrize("name,layers", [("tiny", None), ("llama8b", 2)])
+def test_graph_replays_match_eager_steps(name, layers, monkeypatch):
+    """Decode-only iterations replay a captured graph of the forward.  Two engines run
+    the same requests step by step, one replaying graphs and one launching eagerly,
+    interleaved (eager work and synchronisations between the replays); every step's
+    sampled ids and logits rows must be bit-identical, with the graph replayed many
+    times and re-captured when the block tables outgrow their padding."""
+    shape, dm, w = device_model(name, layers)
+    rng = np.random.default_rng(31)
+    prompts = [rng.integers(0, shape.vocab, n) for n in (40, 1000, 7, 300)]
+    engines = []
+    for env in (None, "1"):
+        if env is None:
+            monkeypatch.delenv("HXF_NO_GRAPHS", raising=False)
+        else:
+            monkeypatch.setenv("HXF_NO_GRAPHS", env)
+        eng = Engine(dm, max_context=4096, n_blocks=600, max_seqs=8, chunk_tokens=256, cost_ps=COST, iter_ps=ITER)
+        ids = [eng.inst.submit(0, i, 0, 0, 10 ** 7, p, 1100) for i, p in enumerate(prompts)]
+        engines.append((eng, ids))
+    monkeypatch.delenv("HXF_NO_GRAPHS", raising=False)
+    (ga, ia), (gb, ib) = engines
+    now, n_decode_steps = 0, 0
+    while True:
+        sa, infa = ga.inst.step(now)
+        sb, infb = gb.inst.step(now)
+        assert sa == sb
+        if sa == hxf.IDLE:
+            break
+        assert infa["n_tokens"] == infb["n_tokens"] and infa["n_decode"] == infb["n_decode"]
+        if infa["n_prefill_tokens"] == 0:
+            n_decode_steps += 1
+        for ra, rb in zip(ia, ib):
+            try:
+                la = ga.inst.last_logits(ra)
+            except hxf.HxfError:
+                continue
+            np.testing.assert_array_equal(la, gb.inst.last_logits(rb))
+        now += 1000
+    assert n_decode_steps > 1000
+    for ra, rb in zip(ia, ib):
+        assert ga.inst.tokens(ra) == gb.inst.tokens(rb)
+    log(f"{name}: {n_decode_steps} decode-only steps, graph replays bit-identical to eager launches")
