@@ -727,13 +727,13 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu) {
   };
   if (M > 512 || (M > 64 && M <= 256 && N >= 16384)) return big();
   if (M <= 256) {
-    // weight streaming (16 * MT rows): 128 columns per workgroup; split K in powers of
-    // two while the grid stays within one workgroup per CU and each split keeps >= 512 of K
+    // weight streaming (16 * MT rows): 128 columns per workgroup; K split into the most
+    // pieces that keep the grid within one workgroup per CU and >= 512 of K per piece
     p.stream = true;
     p.bm = M <= 32 ? 32 : M <= 64 ? 64 : M <= 128 ? 128 : 256;
     const int tiles = (N + 127) / 128;
     int s = 1;
-    while (s * 2 <= max_splits && tiles * s * 2 <= 256 && K / (s * 2) >= 512) s *= 2;
+    while (s + 1 <= max_splits && tiles * (s + 1) <= 256 && K / (s + 1) >= 512) ++s;
     p.k_chunk = (((K + s - 1) / s) + 63) / 64 * 64;
     p.splits = (K + p.k_chunk - 1) / p.k_chunk;
     return p;

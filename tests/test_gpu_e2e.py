@@ -251,3 +251,45 @@ def test_graph_replays_match_eager_steps(name, layers, monkeypatch):
     for ra, rb in zip(ia, ib):
         assert ga.inst.tokens(ra) == gb.inst.tokens(rb)
     log(f"{name}: {n_decode_steps} decode-only steps, graph replays bit-identical to eager launches")
+
+
+def test_graph_replays_match_eager_steps_with_forks(monkeypatch):
+    """The same comparison for forks of one retained parent decoding together (their
+    shared full pages attended by multi-row work items)."""
+    shape, dm, w = device_model("llama8b", 2)
+    rng = np.random.default_rng(41)
+    prompt = rng.integers(0, shape.vocab, 700)
+    apps = [rng.integers(0, shape.vocab, n) for n in (0, 3, 20, 40, 5)]
+    engines = []
+    for env in (None, "1"):
+        if env is None:
+            monkeypatch.delenv("HXF_NO_GRAPHS", raising=False)
+        else:
+            monkeypatch.setenv("HXF_NO_GRAPHS", env)
+        eng = Engine(dm, max_context=2048, n_blocks=300, max_seqs=8, chunk_tokens=256, cost_ps=COST, iter_ps=ITER)
+        par = eng.inst.submit(0, 0, 0, 0, 10 ** 7, prompt, 2, retain=True)
+        now = 0
+        while eng.inst.step(now)[0] != hxf.IDLE:
+            now += 1000
+        kids = [eng.inst.submit(now, 0, 1, 0, 10 ** 7, a, 400, parent=par) for a in apps]
+        engines.append((eng, kids, now))
+    monkeypatch.delenv("HXF_NO_GRAPHS", raising=False)
+    (ga, ka, now), (gb, kb, _) = engines
+    steps = 0
+    while True:
+        sa, _ = ga.inst.step(now)
+        sb, _ = gb.inst.step(now)
+        assert sa == sb
+        if sa == hxf.IDLE:
+            break
+        steps += 1
+        for ra, rb in zip(ka, kb):
+            try:
+                la = ga.inst.last_logits(ra)
+            except hxf.HxfError:
+                continue
+            np.testing.assert_array_equal(la, gb.inst.last_logits(rb))
+        now += 1000
+    assert steps > 390
+    for ra, rb in zip(ka, kb):
+        assert ga.inst.tokens(ra) == gb.inst.tokens(rb)
