@@ -287,6 +287,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     }
     row += be.n;
   }
+  order_prefill_items(pitems.data(), pitems.size(), hm + o_pos0);
   plan_decode(dseqs, hkv, G, dplan_);
   const std::vector<DecodeItem>& ditems = dplan_.items;
   const std::vector<MergeItem>& merges = dplan_.merges;

@@ -161,6 +161,14 @@ hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent
 struct PrefillItem {
   int32_t entry, kvh, q0, nq;
 };
+// Launch order of the prefill items: most visible keys first (pos0 of the item's
+// entry + q0 + nq; equal counts keep their order), so that under the causal mask
+// the short items fill the chip's tail instead of the long ones.
+inline void order_prefill_items(PrefillItem* it, size_t n, const int32_t* pos0_of_entry) {
+  std::stable_sort(it, it + n, [&](const PrefillItem& x, const PrefillItem& y) {
+    return pos0_of_entry[x.entry] + x.q0 + x.nq > pos0_of_entry[y.entry] + y.q0 + y.nq;
+  });
+}
 struct PrefillAttnArgs {
   const uint16_t* q;       // bf16 rows; entry e's query i at row row0[e] + i
   int q_stride;

@@ -232,6 +232,7 @@ int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_po
   for (int s = 0; s < S; ++s)
     for (int h = 0; h < Hkv; ++h)
       for (int q0 = 0; q0 < n_host[s]; q0 += qpi) items.push_back(PrefillItem{s, h, q0, std::min(qpi, n_host[s] - q0)});
+  order_prefill_items(items.data(), items.size(), pos0);
   const int64_t off_rp = al((int64_t)items.size() * (int64_t)sizeof(PrefillItem));
   std::vector<uint8_t> host(off_rp + (int64_t)S * 8);
   std::memcpy(host.data(), items.data(), items.size() * sizeof(PrefillItem));
