@@ -90,6 +90,98 @@ def cpu_baseline(shape, ctxs, n_layers_sample=4, iters=3):
             "measured_s": round(iters * (t_fwd + t_lm), 2)}
 
 
+def _blas_cores():
+    from threadpoolctl import threadpool_info
+    blas = [i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas"]
+    return int(max(blas) if blas else (os.cpu_count() or 1))
+
+
+def _oracle_iteration(shape, prefill, decodes, n_layers_sample, seed=0):
+    """Time one oracle forward (float64 numpy) of a batch through the first
+    `n_layers_sample` layers: `prefill` = list of (position, chunk length), `decodes` =
+    list of context lengths; earlier KV is random.  Returns (seconds for the sampled
+    layers, seconds for the final norm + LM head on the batch's logit rows)."""
+    import numpy as np
+
+    from oracle import model as M
+
+    part = shape.with_layers(n_layers_sample)
+    w = M.Weights(part)
+    for l in range(n_layers_sample):
+        w.layer(l)
+    w.lm_head_f32()
+    rng = np.random.default_rng(seed)
+    seqs, chunks = [], []
+    for pos, n in list(prefill) + [(c - 1, 1) for c in decodes]:
+        s = M.Sequence(n_layers_sample)
+        if pos > 0:
+            for l in range(n_layers_sample):
+                s.k[l] = rng.standard_normal((int(pos), shape.n_kv_heads, shape.head_dim))
+                s.v[l] = rng.standard_normal((int(pos), shape.n_kv_heads, shape.head_dim))
+        s.n = int(pos)
+        seqs.append(s)
+        chunks.append(rng.integers(0, shape.vocab, int(n)))
+    w.embed_rows(np.zeros(1, np.int64))
+    t0 = time.perf_counter()
+    M.forward(w, seqs, chunks)
+    t_all = time.perf_counter() - t0
+    h = rng.standard_normal((len(seqs), shape.d_model))
+    t0 = time.perf_counter()
+    w.logits(h)
+    t_lm = time.perf_counter() - t0
+    return max(t_all - t_lm, 1e-9), t_lm
+
+
+def oracle_baselines():
+    """The CPU oracle timed on each workload (a baseline only, never a target): the tiny
+    configuration in full; one representative iteration of workloads 3-5 through a
+    sample of layers, scaled to the full depth (decode cost of workload 4 scaled from
+    32 of its 256 sequences)."""
+    import numpy as np
+
+    import synth
+    from oracle import model as M
+
+    out = {"kind": "oracle", "cores": _blas_cores(), "workloads": []}
+    # 1: tiny, full run
+    shape = synth.model_shape("tiny")
+    reqs = synth.workloads.cfg1(shape.vocab)
+    w = M.Weights(shape)
+    t0 = time.perf_counter()
+    M.generate(w, [r.prompt for r in reqs], [r.max_new_tokens for r in reqs], keep_logits=False)
+    t = time.perf_counter() - t0
+    out["workloads"].append({"workload": 1, "value": round((640 + 32) / t, 1), "unit": "tokens/s",
+                             "sample": f"full run: 640 prompt + 32 generated tokens in {t:.2f} s"})
+    progress(f"oracle baseline 1: {t:.2f} s")
+    # 3: one mixed iteration (2048-token chunk at position 4096 + 32 decodes at 2560), 1 of 32 layers
+    shape = synth.model_shape("llama8b")
+    tl, tm = _oracle_iteration(shape, [(4096, 2048)], [2560] * 32, 1)
+    t_it = tl * shape.n_layers + tm
+    out["workloads"].append({"workload": 3, "value": round(2080 / t_it, 2), "unit": "tokens/s",
+                             "sample": (f"one mixed iteration (2048-token chunk at position 4096 + 32 decodes at "
+                                        f"context 2560) through 1 of 32 layers ({tl:.2f} s) plus the LM head "
+                                        f"({tm:.2f} s), scaled to 32 layers")})
+    progress(f"oracle baseline 3: {t_it:.1f} s per iteration")
+    # 4: one branch decode iteration, 32 of the 256 sequences at context 4352 (dense per sequence), 1 layer
+    tl, tm = _oracle_iteration(shape, [], [4352] * 32, 1)
+    t_it = (tl * shape.n_layers + tm) * 256 / 32
+    out["workloads"].append({"workload": 4, "value": round(256 / t_it, 2), "unit": "tokens/s",
+                             "sample": (f"one branch decode iteration of 32 of the 256 sequences (context 4352, "
+                                        f"per-sequence KV) through 1 of 32 layers ({tl:.2f} s) plus the LM head "
+                                        f"({tm:.2f} s), scaled to 32 layers and 256 sequences")})
+    progress(f"oracle baseline 4: {t_it:.1f} s per iteration")
+    # 5: 32B shape, one mixed iteration (2048-token chunk at 2048 + 64 decodes at 5000), 1 of 64 layers
+    shape = synth.model_shape("qwen32b")
+    tl, tm = _oracle_iteration(shape, [(2048, 2048)], [5000] * 64, 1)
+    t_it = tl * shape.n_layers + tm
+    out["workloads"].append({"workload": 5, "value": round(2112 / t_it, 2), "unit": "tokens/s",
+                             "sample": (f"one mixed iteration of the 32B shape (2048-token chunk at position 2048 + "
+                                        f"64 decodes at context 5000) through 1 of 64 layers ({tl:.2f} s) plus the "
+                                        f"LM head ({tm:.2f} s), scaled to 64 layers")})
+    progress(f"oracle baseline 5: {t_it:.1f} s per iteration")
+    return out
+
+
 # Calibrated cost-model coefficients in picoseconds (data, measured on one MI355X):
 # t_comp = (c0 + c1*L_in + c2*L_in^2 + d1*L_out) / 1e6 us  (Section 4.1's t_prefill + t_decode)
 # t_iter = (i0 + i1*T + i2*sum_decode_ctx + i3*prefill_attention_pairs) / 1e6 us
@@ -517,6 +609,8 @@ def main():
     ap.add_argument("--policy", default="pq", choices=("pq", "fcfs", "llf"), help="workload 5: local queue policy")
     ap.add_argument("--attn-kernel-probe", action="store_true",
                     help="run only the decode-attention kernel and a calibration copy (for counter runs)")
+    ap.add_argument("--oracle-baselines", action="store_true",
+                    help="time the CPU oracle on workloads 1, 3, 4 and 5 (host cores only)")
     ap.add_argument("--gemm-probe", action="store_true",
                     help="run only the four 2080-row prefill GEMMs (for MFMA counter runs)")
     ap.add_argument("--policy-ablation", action="store_true",
@@ -531,6 +625,10 @@ def main():
 
     if args.attn_kernel_probe:
         print(json.dumps(attn_kernel_probe()), flush=True)
+        return
+
+    if args.oracle_baselines:
+        print(json.dumps(oracle_baselines()), flush=True)
         return
 
     if args.gemm_probe:
