@@ -132,7 +132,7 @@ def _oracle_iteration(shape, prefill, decodes, n_layers_sample, seed=0):
     return max(t_all - t_lm, 1e-9), t_lm
 
 
-def oracle_baselines():
+def cpu_baselines():
     """The CPU oracle timed on each workload (a baseline only, never a target): the tiny
     configuration in full; one representative iteration of workloads 3-5 through a
     sample of layers, scaled to the full depth (decode cost of workload 4 scaled from
@@ -609,8 +609,8 @@ def main():
     ap.add_argument("--policy", default="pq", choices=("pq", "fcfs", "llf"), help="workload 5: local queue policy")
     ap.add_argument("--attn-kernel-probe", action="store_true",
                     help="run only the decode-attention kernel and a calibration copy (for counter runs)")
-    ap.add_argument("--oracle-baselines", action="store_true",
-                    help="time the CPU oracle on workloads 1, 3, 4 and 5 (host cores only)")
+    ap.add_argument("--cpu-baselines", action="store_true",
+                    help="CPU baseline leg for workloads 1, 3, 4 and 5: the oracle timed on the host cores")
     ap.add_argument("--gemm-probe", action="store_true",
                     help="run only the four 2080-row prefill GEMMs (for MFMA counter runs)")
     ap.add_argument("--policy-ablation", action="store_true",
@@ -627,8 +627,8 @@ def main():
         print(json.dumps(attn_kernel_probe()), flush=True)
         return
 
-    if args.oracle_baselines:
-        print(json.dumps(oracle_baselines()), flush=True)
+    if args.cpu_baselines:
+        print(json.dumps(cpu_baselines()), flush=True)
         return
 
     if args.gemm_probe:
