@@ -381,7 +381,8 @@ def workload5(n_wf, policy):
     d = Driver(eng.inst, wfs)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    d.run()
+    d.run(report=lambda it, now, fin: progress(f"{it} iterations, virtual {now / 1e6:.0f} s, {fin}/{n_wf} "
+                                                f"workflows done, {time.perf_counter() - t0:.0f} s"))
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     st = d.stats()

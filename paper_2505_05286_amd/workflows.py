@@ -73,7 +73,9 @@ class Driver:
                     self.inst.release(w.ids[s][k])
                     w.ids[s][k] = None
 
-    def run(self, max_iterations=10 ** 7):
+    def run(self, max_iterations=10 ** 7, report=None, report_every=500):
+        """Replay the workflows to completion; report(iterations, now_us, finished) is
+        called every `report_every` iterations when given."""
         now, nxt = 0, 0
         active = 0
         while nxt < len(self.wf) or active:
@@ -108,6 +110,8 @@ class Driver:
                     else:
                         w.finish_us = c["t_finish_us"]
                         active -= 1
+            if report is not None and self.iterations % report_every == 0:
+                report(self.iterations, now, sum(1 for w in self.wf if w.finish_us >= 0))
             if self.iterations >= max_iterations:
                 raise RuntimeError("iteration limit")
         return now
