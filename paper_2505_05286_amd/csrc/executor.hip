@@ -461,13 +461,20 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
       if (cg) (void)hipGraphDestroy(cg);
       if (rc != HXF_OK) return rc;
       if (ec != hipSuccess || ei != hipSuccess) {
-        err = std::string("HIP graph capture: ") + hipGetErrorString(ec != hipSuccess ? ec : ei);
-        return HXF_EDEVICE;
+        // the runtime could not capture or instantiate: stop using graphs, launch eagerly
+        (void)hipGetLastError();
+        if (rec.exec) (void)hipGraphExecDestroy(rec.exec);
+        use_graphs_ = false;
+      } else {
+        graphs_.push_back(std::move(rec));
+        g = &graphs_.back();
       }
-      graphs_.push_back(std::move(rec));
-      g = &graphs_.back();
     }
-    HXF_HIP(hipGraphLaunch(g->exec, st_));
+    if (g) {
+      HXF_HIP(hipGraphLaunch(g->exec, st_));
+    } else if (int rc = forward()) {
+      return rc;
+    }
     HXF_HIP(hipStreamSynchronize(st_));
   }
   if (prof.on && da.n_items) {
