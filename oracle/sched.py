@@ -63,6 +63,13 @@ def t_comp(cost, l_in, l_out):
     return floor_div(c0 + c1 * l_in + c2 * l_in * l_in + d1 * l_out, PS)
 
 
+def t_comp_mean(cost_sum, n_inst, l_in, l_out):
+    """Instance-average compute cost (Section 4.2): the mean of the N instances'
+    unfloored estimates, floored; cost_sum is their coefficients added up."""
+    c0, c1, c2, d1 = cost_sum
+    return floor_div(c0 + c1 * l_in + c2 * l_in * l_in + d1 * l_out, n_inst * PS)
+
+
 def slo_budget(t_slo_e2e, elapsed, c_j, rest_costs):
     """Per-request SLO budget (Section 4.2): remaining end-to-end time shared
     in proportion to this request's cost among it and the later stages."""
@@ -122,7 +129,10 @@ class Scheduler:
 
     # ------------------------------------------------------------ submit
     def submit(self, now, workflow, stage, wf_arrival, wf_slo, prompt, max_new, parent=0,
-               retain=False, rest=()):
+               retain=False, rest=(), budget_cost_sum=None, n_inst=1):
+        """Queue a request.  With ``budget_cost_sum`` (N instances' cost coefficients
+        summed) its SLO budget is shared out by the instance-average costs of
+        Section 4.2 instead of this instance's own estimates."""
         prompt = [int(t) for t in prompt]
         if max_new < 0 or (max_new == 0 and not retain) or stage < 0:
             raise SchedError(EINVAL, "bad output budget")
@@ -159,7 +169,12 @@ class Scheduler:
         r.max_new, r.retain, r.parent = max_new, bool(retain), parent
         r.t_comp = t_comp(self.cost, len(r.pf_tokens), max_new)
         rest_costs = [t_comp(self.cost, li, lo) for li, lo in rest]
-        r.t_slo = slo_budget(wf_slo, now - wf_arrival, r.t_comp, rest_costs)
+        if budget_cost_sum is None:
+            r.t_slo = slo_budget(wf_slo, now - wf_arrival, r.t_comp, rest_costs)
+        else:
+            mean_j = t_comp_mean(budget_cost_sum, n_inst, len(r.pf_tokens), max_new)
+            mean_rest = [t_comp_mean(budget_cost_sum, n_inst, li, lo) for li, lo in rest]
+            r.t_slo = slo_budget(wf_slo, now - wf_arrival, mean_j, mean_rest)
         r.enq = now
         if self.policy == POLICY_LLF:
             r.key = wf_arrival + wf_slo - (r.t_comp + sum(rest_costs))
@@ -178,6 +193,11 @@ class Scheduler:
         return r.id
 
     # ------------------------------------------------------------ introspection
+    def queue_cost(self):
+        """Queueing cost (Section 4.1): t_comp summed over the requests that are
+        queued or running."""
+        return sum(r.t_comp for r in self.reqs.values() if r.state in (QUEUED, PREFILL, DECODE))
+
     def queue_order(self):
         return [rid for _, rid in sorted(self.heap)]
 
