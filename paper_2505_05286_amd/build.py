@@ -19,6 +19,7 @@ BUILD = os.path.join(PKG, "_build")
 SOURCES = [
     "sched.cpp",
     "decode_plan.cpp",
+    "coord.cpp",
     "api.cpp",
     "ops.cpp",
     "executor.hip",

@@ -8,6 +8,7 @@
 
 #include "executor.hpp"
 #include "hxf.h"
+#include "hxf_coord.h"
 #include "sched.hpp"
 
 using namespace hxf;
@@ -138,6 +139,26 @@ int hxf_submit(hxf_instance* inst, const hxf_stage_req* req, int64_t now_us, uin
   GUARD_BEGIN
   return inst->sched.submit(*req, now_us, out_id, inst->err);
   GUARD_END
+}
+
+int hxf_submit_shared(hxf_instance* inst, const hxf_stage_req* req, int64_t now_us, const int64_t* cost_sum_ps,
+                      int32_t n_instances, uint64_t* out_id) {
+  if (!inst || !req || !out_id || !cost_sum_ps || n_instances < 1) return HXF_EINVAL;
+  GUARD_BEGIN
+  return inst->sched.submit(*req, now_us, out_id, inst->err, cost_sum_ps, n_instances);
+  GUARD_END
+}
+
+int hxf_queue_cost(hxf_instance* inst, int64_t* t_queue_us) {
+  if (!inst || !t_queue_us) return HXF_EINVAL;
+  *t_queue_us = inst->sched.queue_cost();
+  return HXF_OK;
+}
+
+int hxf_request_cost(hxf_instance* inst, int32_t l_in, int32_t l_out, int64_t* out) {
+  if (!inst || !out || l_in < 0 || l_out < 0) return HXF_EINVAL;
+  *out = hxf::t_comp_us(inst->sched.scfg.cost_ps, l_in, l_out);
+  return HXF_OK;
 }
 
 int hxf_step(hxf_instance* inst, int64_t now_us, hxf_step_info* out) {

@@ -11,6 +11,11 @@ i64 t_comp_us(const i64 c[4], i64 l_in, i64 l_out) {
   return (i64)floor_div(ps, kPsPerUs);
 }
 
+i64 t_comp_mean_us(const i64 sum[4], i64 n, i64 l_in, i64 l_out) {
+  i128 ps = (i128)sum[0] + (i128)sum[1] * l_in + (i128)sum[2] * l_in * l_in + (i128)sum[3] * l_out;
+  return (i64)floor_div(ps, (i128)n * kPsPerUs);
+}
+
 i64 slo_budget_us(i64 slo_e2e, i64 elapsed, i64 c_j, const std::vector<i64>& rest) {
   i128 remaining = (i128)slo_e2e - elapsed;
   i128 denom = c_j;
@@ -67,7 +72,12 @@ OrderKey Scheduler::order(const Request& r) const {
 
 static i64 pages_for(i64 n, i64 page) { return (n + page - 1) / page; }
 
-int Scheduler::submit(const hxf_stage_req& q, i64 now, uint64_t* out_id, std::string& err) {
+int Scheduler::submit(const hxf_stage_req& q, i64 now, uint64_t* out_id, std::string& err, const i64* budget_cost_sum,
+                      i64 n_instances) {
+  if (n_instances < 1) {
+    err = "submit: n_instances must be at least 1";
+    return HXF_EINVAL;
+  }
   if (q.max_new_tokens < 0 || (q.max_new_tokens == 0 && !q.retain_kv) || q.stage_index < 0) {
     err = "submit: bad output budget or stage index";
     return HXF_EINVAL;
@@ -145,7 +155,16 @@ int Scheduler::submit(const hxf_stage_req& q, i64 now, uint64_t* out_id, std::st
   r.t_comp = t_comp_us(scfg.cost_ps, (i64)r.pf_tokens.size(), r.max_new);
   std::vector<i64> rest;
   for (int32_t i = 0; i < q.n_rest; ++i) rest.push_back(t_comp_us(scfg.cost_ps, q.rest[i].l_in, q.rest[i].l_out));
-  r.t_slo = slo_budget_us(r.wf_slo, now - r.wf_arrival, r.t_comp, rest);
+  if (budget_cost_sum) {
+    // SLO budget from the instance-average costs of this and the later stages
+    std::vector<i64> mean_rest;
+    for (int32_t i = 0; i < q.n_rest; ++i)
+      mean_rest.push_back(t_comp_mean_us(budget_cost_sum, n_instances, q.rest[i].l_in, q.rest[i].l_out));
+    const i64 mean_j = t_comp_mean_us(budget_cost_sum, n_instances, (i64)r.pf_tokens.size(), r.max_new);
+    r.t_slo = slo_budget_us(r.wf_slo, now - r.wf_arrival, mean_j, mean_rest);
+  } else {
+    r.t_slo = slo_budget_us(r.wf_slo, now - r.wf_arrival, r.t_comp, rest);
+  }
   r.enq = now;
   if (scfg.policy == HXF_POLICY_LLF) {
     i64 s = r.t_comp;
@@ -164,6 +183,7 @@ int Scheduler::submit(const hxf_stage_req& q, i64 now, uint64_t* out_id, std::st
   auto ins = reqs_.emplace(r.id, std::move(r));
   Request& rr = ins.first->second;
   queue_.insert(order(rr));
+  queue_cost_ += rr.t_comp;
   *out_id = rr.id;
   return HXF_OK;
 }
@@ -242,6 +262,7 @@ void Scheduler::commit(std::vector<BatchEntry>& batch, const std::vector<int32_t
   for (Request* r : fin) {
     r->state = DONE;
     r->t_finish = t_end;
+    queue_cost_ -= r->t_comp;
     running_.erase(std::find(running_.begin(), running_.end(), r));
     if (!r->retain) alloc.release(r->bt);
     done_queue.push_back(r->id);
@@ -278,6 +299,7 @@ int Scheduler::cancel(uint64_t id, std::string& err) {
     return HXF_ESTATE;
   }
   r->state = CANCELLED;
+  queue_cost_ -= r->t_comp;
   return HXF_OK;
 }
 

@@ -35,6 +35,12 @@ i64 t_comp_us(const i64 cost_ps[4], i64 l_in, i64 l_out);
 // stages.  With one instance the average is the instance's own estimate.
 i64 slo_budget_us(i64 slo_e2e, i64 elapsed, i64 c_j, const std::vector<i64>& rest_costs);
 
+// Instance-average compute cost, Section 4.2: the mean over N instances of their
+// t_comp estimates, given the N instances' cost coefficients summed (t_comp is
+// linear in them): floor(sum of the unfloored estimates / N).  N = 1 with the
+// instance's own coefficients is t_comp_us itself.
+i64 t_comp_mean_us(const i64 cost_sum_ps[4], i64 n_instances, i64 l_in, i64 l_out);
+
 // Iteration duration of the virtual clock.
 i64 t_iter_us(const i64 iter_ps[4], i64 n_tokens, i64 sum_ctx_decode, i64 prefill_attn);
 
@@ -104,7 +110,13 @@ class Scheduler {
  public:
   Scheduler(const hxf_model_cfg& m, const hxf_sched_cfg& s);
 
-  int submit(const hxf_stage_req& q, i64 now, uint64_t* out_id, std::string& err);
+  // budget_cost_sum (may be null: this instance's own coefficients, N = 1): the cost
+  // coefficients of the n_instances instances summed, for the SLO budget's
+  // instance-average costs.  The urgency key always uses this instance's t_comp.
+  int submit(const hxf_stage_req& q, i64 now, uint64_t* out_id, std::string& err,
+             const i64* budget_cost_sum = nullptr, i64 n_instances = 1);
+  // Sum of t_comp over the requests that have not finished (queued or running).
+  i64 queue_cost() const { return queue_cost_; }
   // Batch formation at a batch boundary (admission in queue order).
   void form_batch(i64 now, std::vector<BatchEntry>& batch, std::vector<uint64_t>& admitted);
   // Apply sampled tokens, finish requests, free pages.
@@ -129,6 +141,7 @@ class Scheduler {
   std::set<OrderKey> queue_;
   std::vector<Request*> running_;   // admission order
   uint64_t next_id_ = 1;
+  i64 queue_cost_ = 0;
 };
 
 }  // namespace hxf

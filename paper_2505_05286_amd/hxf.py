@@ -117,6 +117,15 @@ _SIGS = {
     "hxf_last_logits": (C.c_int, [C.c_void_p, C.c_uint64, C.POINTER(C.c_float), C.c_int32]),
     "hxf_profile_enable": (C.c_int, [C.c_void_p, C.c_int32]),
     "hxf_profile_get": (C.c_int, [C.c_void_p, C.POINTER(Profile)]),
+    # coordinator decisions (hxf_coord.h)
+    "hxf_queue_cost": (C.c_int, [C.c_void_p, C.POINTER(C.c_int64)]),
+    "hxf_request_cost": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.POINTER(C.c_int64)]),
+    "hxf_submit_shared": (C.c_int, [C.c_void_p, C.POINTER(StageReq), C.c_int64, C.POINTER(C.c_int64), C.c_int32,
+                                    C.POINTER(C.c_uint64)]),
+    "hxf_wb_select": (C.c_int, [C.c_int32, C.POINTER(C.c_int64), C.POINTER(C.c_int64), C.c_double, C.c_double,
+                                C.POINTER(C.c_int32)]),
+    "hxf_ttest_greater": (C.c_int, [C.POINTER(C.c_double), C.c_int32, C.POINTER(C.c_double), C.c_int32,
+                                    C.POINTER(C.c_double), C.POINTER(C.c_double), C.POINTER(C.c_double)]),
     # ops
     "hxf_op_gemm_workspace_bytes": (C.c_int64, [C.c_int32, C.c_int32, C.c_int32]),
     "hxf_packed_weight_bytes": (C.c_int64, [C.c_int32, C.c_int32]),
@@ -239,7 +248,9 @@ class Instance:
         self._check(self.L.hxf_bind(self.h, C.byref(b), C.c_void_p(int(stream))), "hxf_bind")
 
     def submit(self, now, workflow_id, stage_index, wf_arrival, wf_slo, prompt, max_new, parent=0, retain=False,
-               rest=(), forced=None):
+               rest=(), forced=None, cost_sum=None, n_instances=1):
+        """Queue one stage request.  With cost_sum (the cost coefficients of n_instances
+        instances summed) the SLO budget uses their average costs (hxf_submit_shared)."""
         p, pp = _i32(prompt)
         rs = (StageShape * max(1, len(rest)))()
         for i, (li, lo) in enumerate(rest):
@@ -253,8 +264,25 @@ class Instance:
             f, fp = _i32(forced)
             q.n_forced, q.forced_ids = len(f), fp
         out = C.c_uint64()
-        self._check(self.L.hxf_submit(self.h, C.byref(q), int(now), C.byref(out)), "hxf_submit")
+        if cost_sum is None:
+            self._check(self.L.hxf_submit(self.h, C.byref(q), int(now), C.byref(out)), "hxf_submit")
+        else:
+            cs = (C.c_int64 * 4)(*[int(c) for c in cost_sum])
+            self._check(self.L.hxf_submit_shared(self.h, C.byref(q), int(now), cs, int(n_instances), C.byref(out)),
+                        "hxf_submit_shared")
         return out.value
+
+    def queue_cost(self):
+        """t_queue of Section 4.1: summed t_comp of the unfinished requests (us)."""
+        v = C.c_int64()
+        self._check(self.L.hxf_queue_cost(self.h, C.byref(v)), "hxf_queue_cost")
+        return v.value
+
+    def request_cost(self, l_in, l_out):
+        """t_comp of Section 4.1 on this instance's cost model (us)."""
+        v = C.c_int64()
+        self._check(self.L.hxf_request_cost(self.h, int(l_in), int(l_out), C.byref(v)), "hxf_request_cost")
+        return v.value
 
     def step(self, now):
         info = StepInfo()
@@ -320,6 +348,30 @@ class Instance:
 
 
 # ------------------------------------------------------------------ ops
+def wb_select(t_comp_us, t_queue_us, alpha, beta):
+    """Workload-balanced dispatch (Section 4.1): index of the best-scoring instance."""
+    n = len(t_comp_us)
+    c = (C.c_int64 * n)(*[int(v) for v in t_comp_us])
+    q = (C.c_int64 * n)(*[int(v) for v in t_queue_us])
+    out = C.c_int32()
+    rc = lib().hxf_wb_select(n, c, q, float(alpha), float(beta), C.byref(out))
+    if rc != OK:
+        raise HxfError(rc, "hxf_wb_select: bad arguments")
+    return out.value
+
+
+def ttest_greater(x_new, x_ref):
+    """One-sided Welch t-test of Section 4.3; returns (t, dof, p)."""
+    a = np.ascontiguousarray(x_new, dtype=np.float64)
+    b = np.ascontiguousarray(x_ref, dtype=np.float64)
+    t, dof, p = C.c_double(), C.c_double(), C.c_double()
+    rc = lib().hxf_ttest_greater(a.ctypes.data_as(C.POINTER(C.c_double)), len(a),
+                                 b.ctypes.data_as(C.POINTER(C.c_double)), len(b), C.byref(t), C.byref(dof), C.byref(p))
+    if rc != OK:
+        raise HxfError(rc, "hxf_ttest_greater: bad arguments")
+    return t.value, dof.value, p.value
+
+
 def _op(rc, what):
     if rc != OK:
         raise HxfError(rc, what)
