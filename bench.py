@@ -514,6 +514,72 @@ def policy_ablation(n_wf=300):
             "scenarios": out}
 
 
+CLUSTER_SPEEDS = (1.0, 1.0, 2.0, 2.0)
+CLUSTER_SCENARIOS = [
+    # (name, [(workflows, arrival rate in workflows/s), ...] in sequence)
+    ("steady 1.0 wf/s", [(300, 1.0)]),
+    ("steady 1.2 wf/s", [(300, 1.2)]),
+    ("shift 0.8 -> 1.6 wf/s", [(150, 0.8), (150, 1.6)]),
+]
+
+
+def cluster_sim():
+    """Coordinator across four scheduler-only instances (Sections 4.1-4.3) on config-5
+    workflows: two instances with this GPU's calibrated 32B cost models and two with
+    every coefficient doubled (an older GPU), on one virtual clock.  Round-robin vs
+    workload-balanced dispatch (fixed alpha, and online alpha tuning from alpha = 0),
+    with PQ or FCFS local queues.  CPU only; deterministic."""
+    import synth
+    from paper_2505_05286_amd import hxf
+    from paper_2505_05286_amd.cluster import Cluster, InstanceSpec, TunerCfg, calibrate_beta
+
+    shape = synth.model_shape("qwen32b")
+    cost, it = COST_PS["qwen32b"]
+    mcfg = hxf.model_cfg(shape, 8192 + 64 + 256 + 512 + 256 + 16)
+
+    def specs(policy):
+        return [InstanceSpec(tuple(int(c * k) for c in cost), tuple(int(c * k) for c in it), 40_000, 128, 2048,
+                             policy) for k in CLUSTER_SPEEDS]
+
+    runs = [("rr+pq", "rr", 0.0, hxf.POLICY_PQ, None), ("wb+fcfs tuned", "wb", 0.0, hxf.POLICY_FCFS, TunerCfg()),
+            ("wb+pq alpha 0", "wb", 0.0, hxf.POLICY_PQ, None), ("wb+pq alpha 0.5", "wb", 0.5, hxf.POLICY_PQ, None),
+            ("wb+pq alpha 0.9", "wb", 0.9, hxf.POLICY_PQ, None), ("wb+pq tuned", "wb", 0.0, hxf.POLICY_PQ, TunerCfg())]
+    out = []
+    for name, phases in CLUSTER_SCENARIOS:
+        n_total = sum(n for n, _ in phases)
+        wfs = cfg5_workflows(n_total, shape.vocab)
+        base = [w.arrival_us for w in wfs]     # generated at 0.5 workflows/s
+        t, k = 0.0, 0
+        for n, rate in phases:
+            start = base[k]
+            for i in range(k, k + n):
+                wfs[i].arrival_us = int(t + (base[i] - start) * 0.5 / rate)
+            t = wfs[k + n - 1].arrival_us + (base[k + n] - base[k + n - 1]) * 0.5 / rate if k + n < n_total else t
+            k += n
+        beta = calibrate_beta(mcfg, specs(hxf.POLICY_PQ), wfs[:20])
+        row = {"scenario": name, "beta_us2": beta}
+        for label, disp, alpha, pol, tuner in runs:
+            c = Cluster(mcfg, specs(pol), disp, alpha, beta, tuner=tuner)
+            t0 = time.perf_counter()
+            c.run(wfs)
+            dt = time.perf_counter() - t0
+            st = c.stats()
+            res = {"slo_attainment": round(st["slo_attainment"], 4), "p95_latency_s": st["p95_latency_s"],
+                   "mean_latency_s": round(st["mean_latency_s"], 2), "requests_per_instance": st["per_instance_requests"],
+                   "host_seconds": round(dt, 2)}
+            if tuner is not None:
+                res["retunings"] = [(round(x[0] / 1e6, 1), round(x[3], 5), x[4]) for x in c.alpha_log
+                                    if x[4] is not None]
+                res["windows_tested"] = len(c.alpha_log)
+                res["grid_search_s"] = round(sum(c.tune_seconds) / max(len(c.tune_seconds), 1), 2)
+            c.close()
+            row[label] = res
+            progress(f"{name}: {label} {res}")
+        out.append(row)
+    return {"cluster": "4 instances (2 x calibrated 32B cost model, 2 x half speed), config-5 workflows, "
+                       "virtual clock", "scenarios": out}
+
+
 def gemm_probe(reps=3, M=2080):
     """Only the four prefill projections of the 8B shape at 2080 rows (a 2048-token chunk
     plus 32 decodes), `reps` times each, through the library's GEMM entry point with
@@ -616,6 +682,8 @@ def main():
                     help="run only the four 2080-row prefill GEMMs (for MFMA counter runs)")
     ap.add_argument("--policy-ablation", action="store_true",
                     help="PQ / FCFS / LLF on config-5 workflows, virtual clock, scheduler only (CPU)")
+    ap.add_argument("--cluster-sim", action="store_true",
+                    help="coordinator across 4 heterogeneous scheduler-only instances: dispatch and alpha tuning (CPU)")
     ap.add_argument("--calibrate", choices=("llama8b", "qwen32b"),
                     help="fit the virtual-clock iteration and request cost models to this GPU")
     args = ap.parse_args()
@@ -638,6 +706,10 @@ def main():
 
     if args.calibrate:
         print(json.dumps(calibrate(args.calibrate)), flush=True)
+        return
+
+    if args.cluster_sim:
+        print(json.dumps(cluster_sim()), flush=True)
         return
 
     if args.policy_ablation:

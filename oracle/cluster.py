@@ -22,8 +22,8 @@ cost of 0 counts as 1 us; score ties go to the lowest instance index; events at
 one instant are taken as iteration ends (instance order), then arrivals, then
 iteration starts (instance order); the t-test is Welch's (unequal variances); a
 window closes at the first completion that gives it ``n_min`` queries and a span
-of ``t_min_us``; the replayed trace is the queries of the two windows compared,
-with their arrival times; P95 ties go to the smaller alpha; beta's references
+of ``t_min_us``; the replayed trace is every query that arrived between the
+earliest arrival among the compared windows' queries and the trigger; P95 ties go to the smaller alpha; beta's references
 are means over the warm-up dispatches (alpha = 0) of the instances' mean t_comp
 and mean t_queue (at least 1 us).
 
@@ -34,7 +34,6 @@ stages' (L_in, L_out)), ``stages``: lists of requests, each a dict with
 import heapq
 import math
 
-import numpy as np
 from scipy import special
 
 from . import sched as S
@@ -72,7 +71,13 @@ def welch_t_greater(x_new, x_ref):
 
 
 def percentile95(values):
-    return float(np.percentile(np.asarray(values, dtype=np.float64), 95))
+    """T_0.95 of Section 4.3, the time by which 95% of the queries have completed:
+    the smallest value with at least 95% of the values at or below it."""
+    ordered = sorted(values)
+    for v in ordered:
+        if 100 * sum(1 for u in ordered if u <= v) >= 95 * len(ordered):
+            return v
+    return ordered[-1]
 
 
 class Coordinator:
@@ -201,7 +206,8 @@ class Coordinator:
         t, dof, p = welch_t_greater([lat[id(w)] for w in new], [lat[id(w)] for w in ref])
         alpha = None
         if p < self.tuner["p"]:
-            trace = sorted(ref + new, key=lambda w: w["arrival"])
+            since = min(w["arrival"] for w in ref + new)
+            trace = [st["wf"] for st in self.states_by_wf if since <= st["wf"]["arrival"] <= now]
             alpha, _ = grid_search(self.specs, trace, self.beta, self.tuner["grid"], self.vocab)
             self.alpha = alpha
         self.alpha_history.append((now, t, dof, p, alpha))
@@ -223,7 +229,7 @@ def replay_p95(specs, trace, alpha, beta, vocab=2048):
 def grid_search(specs, trace, beta, grid, vocab=2048):
     """alpha* = argmin of the simulated P95 over the grid (first minimum)."""
     vals = [replay_p95(specs, trace, a, beta, vocab) for a in grid]
-    k = int(np.argmin(vals))
+    k = vals.index(min(vals))
     return grid[k], vals
 
 

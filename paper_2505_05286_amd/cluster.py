@@ -35,13 +35,16 @@ host reference):
   ``n_min`` completed queries and spans at least ``t_min_us``; the next window
   opens there.  The t-test compares the end-to-end latencies of the queries
   completed in the two most recent windows.
-* Replayed trace: the queries of the two windows compared (the ones the t-test
-  saw), replayed from empty instances with the same configurations and their
-  relative arrival times; ties in simulated P95 go to the smaller alpha.
+* Replayed trace: every query that arrived from the earliest arrival among the
+  two windows' queries up to the trigger (the compared queries and the load
+  around them), replayed from empty instances with the same configurations and
+  relative arrival times.  T_0.95 is the ceil(0.95 n)-th smallest latency; ties
+  go to the smaller alpha.
 * beta: C_ref is the mean over the warm-up dispatches of the instances' mean
   t_comp for the request, Q_ref the mean over the same dispatches of the
   instances' mean t_queue (at least 1 us); the warm-up dispatches with alpha = 0.
 """
+import time
 from dataclasses import dataclass, field
 from typing import List, Optional
 
@@ -81,8 +84,11 @@ class _Flow:
     finish_us: int = -1
 
 
-def p95(latencies):
-    return float(np.percentile(np.asarray(latencies, dtype=np.float64), 95))
+def completion_p95(latencies):
+    """The time within which 95% of the queries completed (Section 4.3's T_0.95): the
+    ceil(0.95 n)-th smallest latency; a query that never completed counts as infinite."""
+    v = sorted(latencies)
+    return v[(95 * len(v) + 99) // 100 - 1]
 
 
 class Cluster:
@@ -105,6 +111,7 @@ class Cluster:
         self.log = []                # (time, workflow, stage, index, instance, id) per request
         self.dispatch_log = []       # (mean t_comp, mean t_queue) per coordinator decision
         self.alpha_log = []          # (time, t, dof, p, alpha chosen or None)
+        self.tune_seconds = []       # host time of each alpha grid search
         self.deadlocked = False
         self.iterations = 0
 
@@ -154,7 +161,7 @@ class Cluster:
     def run(self, workflows, max_iterations=10 ** 8):
         """Replay the workflows (workflows.Workflow records, not modified); returns
         the per-workflow finish times (-1: never finished) in the input order."""
-        flows = [_Flow(w) for w in workflows]
+        flows = self.flows = [_Flow(w) for w in workflows]
         order = sorted(range(len(flows)), key=lambda i: (flows[i].wf.arrival_us, i))
         self.by_req = {}
         busy: List[Optional[int]] = [None] * self.n
@@ -222,15 +229,18 @@ class Cluster:
                                           [f.finish_us - f.wf.arrival_us for f in ref])
         chosen = None
         if p < self.tuner.p_threshold:
-            trace = sorted((f.wf for f in ref + new), key=lambda w: w.arrival_us)
+            t0 = min(f.wf.arrival_us for f in ref + new)
+            trace = [f.wf for f in self.flows if t0 <= f.wf.arrival_us <= now]
+            c0 = time.perf_counter()
             chosen, _ = tune_alpha(self.mcfg, self.specs, trace, self.beta, self.tuner.grid)
+            self.tune_seconds.append(time.perf_counter() - c0)
             self.alpha = chosen
         self.alpha_log.append((now, tstat, dof, p, chosen))
 
     def stats(self):
         lat = np.array([f.finish_us - f.wf.arrival_us if f.finish_us >= 0 else np.inf for f in self.flows])
         slo = np.array([f.wf.slo_us for f in self.flows], dtype=np.float64)
-        pp = float(np.percentile(lat, 95))
+        pp = float(completion_p95(list(lat)))
         return {"workflows": len(self.flows), "finished": int(np.sum(np.isfinite(lat))),
                 "deadlocked": self.deadlocked, "slo_attainment": float(np.mean(lat <= slo)),
                 "p95_latency_s": pp / 1e6 if np.isfinite(pp) else None,
@@ -251,14 +261,14 @@ def _shifted(trace):
 
 
 def simulated_p95(mcfg, specs, trace, alpha, beta):
-    """T_0.95(alpha) of Section 4.3: the 95th-percentile end-to-end latency of the trace
-    replayed on a fresh cluster with fixed alpha (unfinished queries count as infinite)."""
+    """T_0.95(alpha) of Section 4.3 on the trace replayed on a fresh cluster with fixed
+    alpha (a query that never finishes, e.g. when its instance's KV pool fills with
+    retained pages, counts as infinite)."""
     c = Cluster(mcfg, specs, "wb", alpha, beta)
     wfs = _shifted(trace)
     fin = c.run(wfs)
     c.close()
-    lat = [f - w.arrival_us if f >= 0 else np.inf for f, w in zip(fin, wfs)]
-    return float(np.percentile(np.asarray(lat, dtype=np.float64), 95))
+    return completion_p95([f - w.arrival_us if f >= 0 else float("inf") for f, w in zip(fin, wfs)])
 
 
 def tune_alpha(mcfg, specs, trace, beta, grid=ALPHA_GRID):

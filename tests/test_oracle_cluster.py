@@ -133,8 +133,13 @@ def test_welch_matches_the_library_t_test_routine():
 
 
 def test_percentile_definition():
-    assert K.percentile95(list(range(1, 101))) == pytest.approx(95.05)
-    assert K.percentile95([7]) == 7.0
+    # 95 of 1..100 are <= 95; with 20 values the 19th; one value is its own P95
+    assert K.percentile95(list(range(100, 0, -1))) == 95
+    assert K.percentile95(list(range(1, 21))) == 19
+    assert K.percentile95(list(range(1, 22))) == 20    # ceil(0.95 * 21) = 20
+    assert K.percentile95([7]) == 7
+    assert K.percentile95([3, float("inf"), 1] + [2] * 17) == 3    # 19 of 20 finite ones cover 95%
+    assert K.percentile95([3, float("inf"), float("inf")] + [2] * 17) == float("inf")
 
 
 # ---------------------------------------------------------------- the coordinator loop
