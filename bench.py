@@ -190,6 +190,8 @@ COST_PS = {
     # fitted to measured iterations on one MI355X by `bench.py --calibrate <model>`
     "llama8b": ((3_855_276_245, 17_641_835, 286, 3_948_937_446), (3_855_276_245, 15_173_800, 19_162, 572)),
     "qwen32b": ((13_126_065_958, 71_492_740, 997, 13_368_178_414), (13_126_065_958, 63_041_887, 43_718, 1_994)),
+    # provisional (8B's scaled by the weight ratio), to be replaced by a calibration
+    "llama70b": ((33_700_000_000, 154_000_000, 2_500, 34_500_000_000), (33_700_000_000, 133_000_000, 168_000, 5_000)),
 }
 
 
@@ -254,15 +256,33 @@ def workload1(reps=20):
             "tokens_per_s": round((640 + 32) / t, 1)}
 
 
-def workload3():
+MODEL_NAMES = {"llama8b": "Llama-3-8B", "qwen32b": "Qwen2.5-32B", "llama70b": "Llama-3.1-70B"}
+
+
+def describe(shape):
+    return (f"{MODEL_NAMES.get(shape.name, shape.name)} shape ({shape.n_layers} layers, d {shape.d_model}, "
+            f"{shape.n_q_heads}q/{shape.n_kv_heads}kv heads of {shape.head_dim}, SwiGLU {shape.ffn_dim}, "
+            f"vocab {shape.vocab})")
+
+
+def kv_pages_that_fit(shape, reserve_gb=8.0, frac=0.9):
+    """KV pages that fit the device memory left after the weights (a margin for the
+    workspace and torch's allocator kept aside)."""
+    import torch
+    free, _ = torch.cuda.mem_get_info()
+    page = 2 * shape.n_kv_heads * shape.head_dim * 2 * 16 * shape.n_layers
+    return int(max(free - reserve_gb * 1e9, 0) * frac // page)
+
+
+def workload3(model="llama8b"):
     """Mixed iterations: 32 running decodes (context U[1024, 4096]) co-batched with chunked
     prefill (2048 tokens per iteration) of 16 prompts of length U[2048, 8192]."""
     import synth
     from paper_2505_05286_amd import hxf
     from paper_2505_05286_amd.device import Engine
-    shape, dm = load_model("llama8b")
+    shape, dm = load_model(model)
     decodes, prompts = synth.workloads.cfg3(shape.vocab)
-    cost, it = COST_PS["llama8b"]
+    cost, it = COST_PS[model]
     total = sum(-(-(len(s.prompt) + 4096) // 16) for s in decodes) + sum(-(-len(s.prompt) // 16) for s in prompts)
     eng = Engine(dm, max_context=8192 + 4096, n_blocks=total + 256, max_seqs=64, chunk_tokens=2048, cost_ps=cost,
                  iter_ps=it, clock=hxf.CLOCK_MEASURED)
@@ -275,7 +295,7 @@ def workload3():
         inst.submit(now, s.workflow, 0, now, s.wf_slo_us, s.prompt, s.max_new_tokens)
     progress("timed: mixed chunked-prefill + decode iterations")
     now, iters, pf, dec, dt = step_until(inst, now, lambda i: i["n_prefill_tokens"] == 0)
-    return {"workload": "3: 8B, 16 prompts U[2048,8192] chunked 2048 + 32 decodes ctx U[1024,4096]",
+    return {"workload": f"3: {describe(shape)}, 16 prompts U[2048,8192] chunked 2048 + 32 decodes ctx U[1024,4096]",
             "iterations": iters, "ms_per_iteration": round(dt / iters * 1e3, 3), "prefill_tokens": pf,
             "prefill_tokens_per_s": round(pf / dt, 1), "decode_tokens_per_s": round(dec / dt, 1),
             "tokens_per_s": round((pf + dec) / dt, 1)}
@@ -347,13 +367,13 @@ def workload4():
             "correction_prefill_tokens_per_s": round(pf3 / dt3, 1)}
 
 
-def cfg5_workflows(n, vocab):
+def cfg5_workflows(n, vocab, model="qwen32b"):
     import numpy as np
     import synth
     from paper_2505_05286_amd.workflows import Req, Workflow
     s = synth.workloads.CFG5_SHAPE
     out = []
-    for w in synth.workloads.cfg5(vocab=vocab, n_wf=n):
+    for w in synth.workloads.cfg5(vocab=vocab, n_wf=n, model=model):
         stages = [[Req(w.schema, s["s1_out"], retain=True)],
                   [Req(np.zeros(0, np.int32), s["cand_out"], parent=(0, 0), retain=(b % 2 == 0))
                    for b in range(s["n_cand"])],
@@ -365,18 +385,22 @@ def cfg5_workflows(n, vocab):
     return out
 
 
-def workload5(n_wf, policy):
-    """Qwen2.5-32B-shaped replay of four-stage workflows (Poisson arrivals, 0.5/s) driven by
-    the local priority queue; scheduling runs on the virtual clock, the forward on the GPU."""
+def workload5(n_wf, policy, model="qwen32b", rate=0.5):
+    """Replay of four-stage workflows (Poisson arrivals, `rate` per second; configured:
+    the Qwen2.5-32B shape at 0.5/s) driven by the local priority queue; scheduling runs on
+    the virtual clock, the forward on the GPU."""
     from paper_2505_05286_amd import hxf
     from paper_2505_05286_amd.device import Engine
     from paper_2505_05286_amd.workflows import Driver
     import torch
-    shape, dm = load_model("qwen32b")
-    wfs = cfg5_workflows(n_wf, shape.vocab)
-    cost, it = COST_PS["qwen32b"]
+    shape, dm = load_model(model)
+    wfs = cfg5_workflows(n_wf, shape.vocab, model)
+    for w in wfs:
+        w.arrival_us = int(w.arrival_us * 0.5 / rate)    # generated at 0.5 workflows/s
+    cost, it = COST_PS[model]
     pol = {"pq": hxf.POLICY_PQ, "fcfs": hxf.POLICY_FCFS, "llf": hxf.POLICY_LLF}[policy]
-    eng = Engine(dm, max_context=8192 + 64 + 256 + 512 + 256 + 16, n_blocks=40_000, max_seqs=128,
+    n_blocks = min(40_000, kv_pages_that_fit(shape))
+    eng = Engine(dm, max_context=8192 + 64 + 256 + 512 + 256 + 16, n_blocks=n_blocks, max_seqs=128,
                  chunk_tokens=2048, cost_ps=cost, iter_ps=it, policy=pol)
     d = Driver(eng.inst, wfs)
     torch.cuda.synchronize()
@@ -386,7 +410,8 @@ def workload5(n_wf, policy):
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     st = d.stats()
-    st.update({"workload": f"5: 32B, {n_wf} four-stage workflows, Poisson 0.5/s, policy {policy}",
+    st.update({"workload": f"5: {describe(shape)}, {n_wf} four-stage workflows, Poisson {rate}/s, policy {policy}",
+               "kv_pages": n_blocks,
                "gpu_seconds": round(dt, 2), "prefill_tokens_per_s": round(st["prefill_tokens"] / dt, 1),
                "decode_tokens_per_s": round(st["decode_tokens"] / dt, 1)})
     return st
@@ -410,7 +435,7 @@ def calibrate(model):
     shape, dm = load_model(model)
     cost, it = COST_PS[model]
     chunk = 2048
-    n_blocks = 128 * (4096 + 16) // 16 + 1024
+    n_blocks = min(128 * (4096 + 16) // 16 + 1024, kv_pages_that_fit(shape))
     eng = Engine(dm, max_context=8192 + 64, n_blocks=n_blocks, max_seqs=128, chunk_tokens=chunk, cost_ps=cost,
                  iter_ps=it, clock=hxf.CLOCK_MEASURED)
     inst = eng.inst
@@ -684,7 +709,10 @@ def main():
                     help="PQ / FCFS / LLF on config-5 workflows, virtual clock, scheduler only (CPU)")
     ap.add_argument("--cluster-sim", action="store_true",
                     help="coordinator across 4 heterogeneous scheduler-only instances: dispatch and alpha tuning (CPU)")
-    ap.add_argument("--calibrate", choices=("llama8b", "qwen32b"),
+    ap.add_argument("--model", choices=("llama8b", "qwen32b", "llama70b"),
+                    help="model shape for workloads 2, 3 and 5 (default: 8B for 2 and 3, 32B for 5)")
+    ap.add_argument("--rate", type=float, default=0.5, help="workload 5: workflow arrival rate (per second)")
+    ap.add_argument("--calibrate", choices=("llama8b", "qwen32b", "llama70b"),
                     help="fit the virtual-clock iteration and request cost models to this GPU")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -717,8 +745,8 @@ def main():
         return
 
     if args.workload != 2:
-        fn = {1: workload1, 3: workload3, 4: workload4,
-              5: lambda: workload5(args.n_workflows, args.policy)}[args.workload]
+        fn = {1: workload1, 3: lambda: workload3(args.model or "llama8b"), 4: workload4,
+              5: lambda: workload5(args.n_workflows, args.policy, args.model or "qwen32b", args.rate)}[args.workload]
         print(json.dumps(fn()), flush=True)
         return
 
@@ -731,9 +759,9 @@ def main():
 
     hxf.lib()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    shape = synth.model_shape("llama8b")
+    shape = synth.model_shape(args.model or "llama8b")
     t0 = time.time()
-    progress("generating and uploading 8B-shaped bf16 weights")
+    progress(f"generating and uploading {shape.name}-shaped bf16 weights")
     dm = DeviceModel(shape, lambda l: synth.gen_layer(shape, l), synth.gen_embed(shape), synth.gen_lm_head(shape),
                      synth.norm_weight(shape), device="cuda:0")
     progress(f"weights ready in {time.time() - t0:.1f} s")
@@ -794,8 +822,9 @@ def main():
     achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9
     achieved_merged = bytes_per_launch / ((avg_ms + merge_ms) * 1e-3) / 1e9
     sum_ctx_now = sum(inst.request_state(r)["n_kv"] for r in ids)
+    default_shape = shape.name == "llama8b"
     out = {
-        "metric": METRIC,
+        "metric": METRIC if default_shape else METRIC.replace("8B shape", f"{MODEL_NAMES[shape.name]} shape"),
         "value": round(value, 2),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -807,14 +836,14 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": ("decode iteration, Llama-3-8B shape (32 layers, d 4096, 32q/8kv heads of 128, "
-                                "SwiGLU 14336, vocab 128256), 64 sequences, contexts lognormal(median 3000, "
-                                "sigma 0.5) clipped to [1024, 8192], 16-token KV pages"),
+        "config": {"workload": (f"decode iteration, {describe(shape)}, 64 sequences, contexts lognormal(median "
+                                "3000, sigma 0.5) clipped to [1024, 8192], 16-token KV pages"),
                    "batch": BATCH, "layers": shape.n_layers, "sum_context_tokens": int(sum_ctx_now)},
         "prefill_tokens_per_s": round(pf_tokens / t_pf, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": DECODE_ATTN_TRAFFIC["bytes_per_launch"],
-                     "traffic_sample": DECODE_ATTN_TRAFFIC,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": DECODE_ATTN_TRAFFIC["bytes_per_launch"] if default_shape else None,
+                     "traffic_sample": DECODE_ATTN_TRAFFIC if default_shape else None,
                      "kernel": "decode_attn_kernel<128>", "avg_launch_us": round(avg_ms * 1e3, 2),
                      "timing": (f"kernel-stamped HIP events on the {int(launches)} decode-attention launches of "
                                 f"{roof_steps} eager decode steps run right after the timed (graph-replayed) steps"),

@@ -56,6 +56,8 @@ MODELS = {
     "llama8b": ModelShape("llama8b", 32, 4096, 32, 8, 128, 14336, 128256, weight_seed=1),
     # Qwen2.5-32B shape, seed 4
     "qwen32b": ModelShape("qwen32b", 64, 5120, 40, 8, 128, 27648, 152064, weight_seed=4),
+    # Llama-3.1-70B shape (the model the paper serves), seed 5: 141 GB of bf16 weights, one MI355X
+    "llama70b": ModelShape("llama70b", 80, 8192, 64, 8, 128, 28672, 128256, weight_seed=5),
 }
 
 

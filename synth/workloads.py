@@ -23,6 +23,7 @@ REF_LATENCY = {
     "tiny": (200, 0.05, 150),
     "llama8b": (3855, 18.8, 3949),
     "qwen32b": (13126, 75.6, 13368),
+    "llama70b": (33700, 165.0, 34500),
 }
 
 

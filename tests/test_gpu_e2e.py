@@ -147,9 +147,10 @@ def test_cfg1_tiny_full():
 
 @pytest.mark.parametrize("name,layers,lens,chunk", [("llama8b", 2, (100, 300, 700), 256),
                                                     ("llama8b", 1, (600, 1500), 1024),
-                                                    ("qwen32b", 1, (90, 400), 128)])
+                                                    ("qwen32b", 1, (90, 400), 128),
+                                                    ("llama70b", 1, (90, 500), 256)])
 def test_full_width_layer_truncated(name, layers, lens, chunk):
-    """Full-width 8B and 32B shapes (vocab 128256 / 152064, GQA 4 / 5), few layers,
+    """Full-width 8B, 32B and 70B shapes (vocab 128256 / 152064, GQA 4 / 5 / 8), few layers,
     chunked prefill co-batched with decode, teacher forced."""
     shape, dm, w = device_model(name, layers)
     rng = np.random.default_rng(len(lens))

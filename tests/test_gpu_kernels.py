@@ -61,7 +61,8 @@ def _gemm_case(M_, N, K, epi, seed):
                                     (256, 1024, 688), (300, 1000, 688),
                                     (2080, 384, 512), (600, 1000, 688), (2080, 6144, 1024), (1031, 4096, 1384),
                                     (2048, 4096, 256), (2080, 4096, 264), (2048, 6144, 96), (200, 32768, 512),
-                                    (96, 20000, 256), (250, 6144, 1024), (2300, 6144, 72), (960, 11008, 72)])
+                                    (96, 20000, 256), (250, 6144, 1024), (2300, 6144, 72), (960, 11008, 72),
+                                    (64, 10240, 8192), (64, 8192, 28672), (2080, 10240, 1024)])
 @pytest.mark.parametrize("epi", [hxf.EPI_BF16, hxf.EPI_RESID, hxf.EPI_F32])
 def test_gemm(M_, N, K, epi):
     _gemm_case(M_, N, K, epi, seed=M_ * 7 + N + K + epi)
@@ -70,7 +71,8 @@ def test_gemm(M_, N, K, epi):
 @pytest.mark.parametrize("M_,N,K", [(5, 64, 256), (64, 2 * 688, 256), (33, 2 * 688, 2048), (64, 2 * 14336, 4096),
                                     (20, 2 * 4096, 4096), (64, 2 * 96, 8192), (2080, 2 * 4096, 200),
                                     (300, 2 * 1376, 512), (128, 2 * 14336, 4096), (700, 2 * 688, 256),
-                                    (2080, 2 * 2080, 512), (1040, 2 * 5504, 72), (520, 2 * 3584, 72)])
+                                    (2080, 2 * 2080, 512), (1040, 2 * 5504, 72), (520, 2 * 3584, 72),
+                                    (64, 2 * 28672, 8192)])
 def test_gemm_swiglu(M_, N, K):
     _gemm_case(M_, N, K, hxf.EPI_SWIGLU, seed=M_ + N + K)
 
@@ -141,7 +143,7 @@ def _logical_pool(kp, vp, nb, hkv, dh):
     return k, v
 
 
-@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128)])
+@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128), (64, 8, 128), (8, 1, 128)])
 def test_rope_kv_write(hq, hkv, dh):
     t = torch()
     rng = np.random.default_rng(hq + dh)
@@ -229,7 +231,7 @@ def _decode_case(ctxs, hq, hkv, dh, seed, sample=None):
         np.testing.assert_allclose(got[b], ref, rtol=1e-2, atol=1e-2, err_msg=f"seq {b} ctx {c}")
 
 
-@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128)])
+@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128), (64, 8, 128), (8, 1, 128)])
 def test_decode_attention_ragged(hq, hkv, dh):
     ctxs = [1, 15, 16, 17, 31, 32, 33, 255, 256, 257, 511, 700, 1500]
     _decode_case(ctxs, hq, hkv, dh, seed=hq)
@@ -254,7 +256,7 @@ def test_decode_attention_one_item_per_pair():
     _decode_case(ctxs, 32, 8, 128, seed=260, sample=sample)
 
 
-@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128)])
+@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128), (64, 8, 128), (8, 1, 128)])
 def test_decode_attention_shared_prefix(hq, hkv, dh):
     """Forks of two parents (255 and 40 shared full pages) decoding together with an
     unrelated sequence: the shared pages are read once per group of rows, and every
@@ -320,7 +322,7 @@ def _prefill_case(chunks, hq, hkv, dh, seed):
         np.testing.assert_allclose(got[row0[s]:row0[s] + n], ref, rtol=1e-2, atol=1e-2, err_msg=f"chunk {s}")
 
 
-@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128)])
+@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128), (64, 8, 128), (8, 1, 128)])
 def test_prefill_attention_chunks(hq, hkv, dh):
     chunks = [(0, 1), (0, 17), (0, 64), (16, 16), (40, 9), (100, 77), (0, 300), (513, 130)]
     _prefill_case(chunks, hq, hkv, dh, seed=dh + hq)
