@@ -77,10 +77,12 @@ typedef struct hxf_sched_cfg {
   /* Compute-cost estimate of a request, Section 4.1 (t_prefill(L_in) + t_decode(L_out)):
    * t_comp_us = floor((c0 + c1*L_in + c2*L_in^2 + d1*L_out) / 1e6), coefficients in ps. */
   int64_t cost_ps[4];     /* c0, c1, c2, d1 */
-  /* Virtual iteration cost: floor((i0 + i1*T + i2*sum_decode_ctx + i3*prefill_attn) / 1e6) us,
-   * T = tokens in the batch, sum_decode_ctx = sum of decode context lengths,
-   * prefill_attn = sum over prefill chunks of chunk_len * (chunk_start + chunk_len). */
-  int64_t iter_ps[4];
+  /* Virtual iteration cost:
+   * floor((i0 + i1*T_prefill + i2*sum_decode_ctx + i3*prefill_attn + i4*n_decode) / 1e6) us,
+   * T_prefill = prefill tokens in the batch, n_decode = decode rows, sum_decode_ctx = sum of
+   * the decode rows' context lengths, prefill_attn = sum over prefill chunks of
+   * chunk_len * (chunk_start + chunk_len).  i4 = i1 charges every token alike. */
+  int64_t iter_ps[5];
 } hxf_sched_cfg;
 
 /* (L_in, L_out) of one later stage on the workflow's critical path. */

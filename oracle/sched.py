@@ -85,10 +85,14 @@ def urgency(t_comp_us, t_slo_us, tau_us):
     return t_comp_us - (t_slo_us - tau_us)
 
 
-def t_iter(it, n_tokens, sum_ctx_decode, attn_pf):
-    """Virtual-clock duration of one iteration (us)."""
-    i0, i1, i2, i3 = it
-    return floor_div(i0 + i1 * n_tokens + i2 * sum_ctx_decode + i3 * attn_pf, PS)
+def t_iter(it, n_prefill, n_decode, sum_ctx_decode, attn_pf):
+    """Virtual-clock duration of one iteration (us): a fixed part, prefill tokens,
+    decode rows, the decode rows' context and the prefill attention pairs, each with
+    its own coefficient (ps).  A 4-coefficient model charges a decode row like a
+    prefill token."""
+    i0, i1, i2, i3 = it[:4]
+    i4 = it[4] if len(it) == 5 else i1
+    return floor_div(i0 + i1 * n_prefill + i2 * sum_ctx_decode + i3 * attn_pf + i4 * n_decode, PS)
 
 
 def fake_token(req_id, pos, vocab):
@@ -258,7 +262,8 @@ class Scheduler:
             sampled = [fake_token(r.id, len(r.context) + len(r.generated), self.vocab) for r in rows]
         else:
             sampled = executor(batch, rows)
-        dt = t_iter(self.iter_cost, n_tok, sum_ctx, attn) if measured_us is None else measured_us
+        n_dec = sum(1 for b in batch if b[1] == "d")
+        dt = t_iter(self.iter_cost, n_tok - n_dec, n_dec, sum_ctx, attn) if measured_us is None else measured_us
         t_end = now + dt
         finished = []
         k = 0

@@ -175,15 +175,16 @@ int hxf_step(hxf_instance* inst, int64_t now_us, hxf_step_info* out) {
     if (out) *out = info;
     return HXF_IDLE;
   }
-  int64_t n_tok, sum_ctx, attn;
+  int64_t n_tok, sum_ctx, attn, n_dec = 0;
   S.batch_cost_terms(inst->batch, &n_tok, &sum_ctx, &attn);
+  for (const auto& e : inst->batch) n_dec += e.decode ? 1 : 0;
   const auto t0 = std::chrono::steady_clock::now();
   int rc = inst->exec->run(inst->batch, inst->sampled, inst->err);
   if (rc) return rc;
   const auto t1 = std::chrono::steady_clock::now();
   int64_t dt = (S.scfg.clock == HXF_CLOCK_MEASURED)
                    ? std::chrono::duration_cast<std::chrono::microseconds>(t1 - t0).count()
-                   : t_iter_us(S.scfg.iter_ps, n_tok, sum_ctx, attn);
+                   : t_iter_us(S.scfg.iter_ps, n_tok - n_dec, n_dec, sum_ctx, attn);
   for (const auto& e : inst->batch) {
     info.n_decode += e.decode ? 1 : 0;
     info.n_prefill_tokens += e.decode ? 0 : e.n;

@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <unordered_set>
 
 #include "decode_plan.hpp"
 #include "kernels/kernels.hpp"
@@ -180,12 +181,19 @@ class HipExecutor : public Executor {
   std::vector<hipEvent_t> ev_pool_, ev_merge_;
   // Decode-only iterations replay a captured HIP graph of the whole forward (metadata
   // upload, every kernel, sampled ids back), keyed by the batch's launch shape; the
-  // graph reads the per-iteration metadata from the pinned staging buffer.
+  // graph reads the per-iteration metadata from the pinned staging buffer.  A shape is
+  // captured the second time it occurs (a capture costs more than an eager launch, and
+  // under continuous batching many shapes occur once); at most kMaxGraphs are kept,
+  // the least recently used one is replaced.
+  static constexpr size_t kMaxGraphs = 16, kMaxSeen = 4096;
   struct GraphRec {
     int64_t key = 0;
     hipGraphExec_t exec = nullptr;
+    int64_t last_use = 0;
   };
   std::vector<GraphRec> graphs_;
+  std::unordered_set<int64_t> seen_;   // shapes met once, not captured yet
+  int64_t graph_clock_ = 0;
   bool use_graphs_ = true;
   // The legacy null stream cannot be captured: graphs then run on a stream of our own
   // (blocking, default priority), which the null stream orders against.
@@ -194,6 +202,7 @@ class HipExecutor : public Executor {
     for (auto& g : graphs_)
       if (g.exec) (void)hipGraphExecDestroy(g.exec);
     graphs_.clear();
+    seen_.clear();
   }
 };
 
@@ -448,8 +457,16 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     GraphRec* g = nullptr;
     for (auto& x : graphs_)
       if (x.key == key) g = &x;
-    if (!g) {
-      if (graphs_.size() >= 16) drop_graphs();
+    const bool capture = !g && !seen_.insert(key).second;   // second occurrence of the shape
+    if (capture) {
+      seen_.erase(key);
+      if (seen_.size() > kMaxSeen) seen_.clear();
+      if (graphs_.size() >= kMaxGraphs) {
+        auto lru = std::min_element(graphs_.begin(), graphs_.end(),
+                                    [](const GraphRec& a, const GraphRec& b) { return a.last_use < b.last_use; });
+        if (lru->exec) (void)hipGraphExecDestroy(lru->exec);
+        graphs_.erase(lru);
+      }
       GraphRec rec;
       rec.key = key;
       HXF_HIP(hipStreamBeginCapture(st_, hipStreamCaptureModeThreadLocal));
@@ -471,6 +488,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
       }
     }
     if (g) {
+      g->last_use = ++graph_clock_;
       HXF_HIP(hipGraphLaunch(g->exec, st_));
     } else if (int rc = forward()) {
       return rc;

@@ -24,8 +24,8 @@ i64 slo_budget_us(i64 slo_e2e, i64 elapsed, i64 c_j, const std::vector<i64>& res
   return (i64)floor_div(remaining * c_j, denom);
 }
 
-i64 t_iter_us(const i64 it[4], i64 n_tokens, i64 sum_ctx, i64 attn) {
-  i128 ps = (i128)it[0] + (i128)it[1] * n_tokens + (i128)it[2] * sum_ctx + (i128)it[3] * attn;
+i64 t_iter_us(const i64 it[5], i64 n_prefill, i64 n_decode, i64 sum_ctx, i64 attn) {
+  i128 ps = (i128)it[0] + (i128)it[1] * n_prefill + (i128)it[2] * sum_ctx + (i128)it[3] * attn + (i128)it[4] * n_decode;
   return (i64)floor_div(ps, kPsPerUs);
 }
 

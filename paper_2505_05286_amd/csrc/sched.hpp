@@ -42,7 +42,7 @@ i64 slo_budget_us(i64 slo_e2e, i64 elapsed, i64 c_j, const std::vector<i64>& res
 i64 t_comp_mean_us(const i64 cost_sum_ps[4], i64 n_instances, i64 l_in, i64 l_out);
 
 // Iteration duration of the virtual clock.
-i64 t_iter_us(const i64 iter_ps[4], i64 n_tokens, i64 sum_ctx_decode, i64 prefill_attn);
+i64 t_iter_us(const i64 iter_ps[5], i64 n_prefill, i64 n_decode, i64 sum_ctx_decode, i64 prefill_attn);
 
 enum State : int32_t { QUEUED = 0, PREFILL = 1, DECODE = 2, DONE = 3, RELEASED = 4, CANCELLED = 5 };
 

@@ -36,7 +36,7 @@ class ModelCfg(C.Structure):
 class SchedCfg(C.Structure):
     _fields_ = [("n_blocks", C.c_int64), ("max_seqs", C.c_int32), ("chunk_tokens", C.c_int32),
                 ("policy", C.c_int32), ("clock", C.c_int32), ("executor", C.c_int32), ("reserved", C.c_int32),
-                ("cost_ps", C.c_int64 * 4), ("iter_ps", C.c_int64 * 4)]
+                ("cost_ps", C.c_int64 * 4), ("iter_ps", C.c_int64 * 5)]
 
 
 class StageShape(C.Structure):
@@ -194,7 +194,10 @@ def sched_cfg(n_blocks, max_seqs, chunk_tokens, cost_ps, iter_ps, policy=POLICY_
     s.policy, s.clock, s.executor = policy, clock, executor
     for i in range(4):
         s.cost_ps[i] = int(cost_ps[i])
-        s.iter_ps[i] = int(iter_ps[i])
+    # (i0, i1, i2, i3[, i4]): without i4 a decode row costs what a prefill token does
+    it = tuple(iter_ps) if len(iter_ps) == 5 else tuple(iter_ps) + (iter_ps[1],)
+    for i in range(5):
+        s.iter_ps[i] = int(it[i])
     return s
 
 

@@ -10,7 +10,7 @@ Token ids are uniform in [0, vocab).  Times are integer microseconds.
 End-to-end SLOs are ``slo_scale`` times a reference isolated latency
 ``REF_US(L_in, L_out)`` summed over the workflow's critical path.  The
 reference figures below are fixed data: a lone request's latency on one MI355X
-(chunked prefill, batch-1 decode at ~4k context), as measured for each 8B/32B
+(chunked prefill, batch-1 decode at ~4k context), as measured for each 8B/32B/70B
 shape by ``bench.py --calibrate``; the tiny shape's are nominal.
 """
 from dataclasses import dataclass, field
@@ -23,7 +23,7 @@ REF_LATENCY = {
     "tiny": (200, 0.05, 150),
     "llama8b": (3855, 18.8, 3949),
     "qwen32b": (13126, 75.6, 13368),
-    "llama70b": (33700, 165.0, 34500),
+    "llama70b": (25850, 157.0, 26181),
 }
 
 

@@ -282,3 +282,16 @@ def _run_exec(s, ex):
         if st == S.IDLE:
             return
         now += info["t_iter_us"]
+
+
+def test_iteration_cost_terms():
+    # hand value: 1 ms fixed, 2 us per prefill token, 3 ns per decode context token,
+    # 5 ps per attention pair, 0.5 us per decode row
+    it = (1000 * S.PS, 2 * S.PS, 3000, 5, S.PS // 2)
+    assert S.t_iter(it, 100, 8, 40_000, 1_000_000) == 1000 + 200 + 120 + 5 + 4
+    # four coefficients: a decode row costs what a prefill token does
+    it4 = it[:4]
+    for n_pf, n_dec in ((0, 64), (2048, 32), (17, 0)):
+        assert S.t_iter(it4, n_pf, n_dec, 12345, 678) == S.t_iter(it4 + (it4[1],), n_pf, n_dec, 12345, 678)
+    # floor toward minus infinity of the picosecond sum
+    assert S.t_iter((S.PS - 1, 0, 0, 0, 0), 0, 0, 0, 0) == 0

@@ -87,14 +87,16 @@ class Pair:
 
 COST = (300 * S.PS, 2 * S.PS, 1, 40 * S.PS)
 ITER = (800 * S.PS, 3 * S.PS, S.PS // 50, 1)
+ITER5 = (800 * S.PS, 3 * S.PS, S.PS // 50, 1, S.PS // 7)     # decode rows priced apart
 
 
+@pytest.mark.parametrize("it", [ITER, ITER5])
 @pytest.mark.parametrize("policy", [S.POLICY_PQ, S.POLICY_FCFS, S.POLICY_LLF])
 @pytest.mark.parametrize("seed", [0, 1, 2])
-def test_random_streams_match(policy, seed):
+def test_random_streams_match(policy, seed, it):
     rng = np.random.default_rng(100 + seed)
     p = Pair(n_blocks=int(rng.integers(40, 120)), max_seqs=int(rng.integers(2, 9)), chunk=int(rng.integers(16, 200)),
-             cost=COST, it=ITER, policy=policy)
+             cost=COST, it=it, policy=policy)
     now = 0
     retained = []
     for k in range(60):
