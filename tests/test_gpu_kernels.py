@@ -72,7 +72,7 @@ def test_gemm(M_, N, K, epi):
                                     (20, 2 * 4096, 4096), (64, 2 * 96, 8192), (2080, 2 * 4096, 200),
                                     (300, 2 * 1376, 512), (128, 2 * 14336, 4096), (700, 2 * 688, 256),
                                     (2080, 2 * 2080, 512), (1040, 2 * 5504, 72), (520, 2 * 3584, 72),
-                                    (64, 2 * 28672, 8192)])
+                                    (64, 2 * 28672, 8192), (1024, 2 * 5632, 1000), (2080, 2 * 7168, 1000)])
 def test_gemm_swiglu(M_, N, K):
     _gemm_case(M_, N, K, hxf.EPI_SWIGLU, seed=M_ + N + K)
 
