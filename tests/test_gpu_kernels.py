@@ -18,7 +18,8 @@ from .gpu_util import dev_bits, dev_packed, empty_i16, host_f64, i32, log, rand_
 pytestmark = pytest.mark.gpu
 
 
-def _gemm_case(M_, N, K, epi, seed):
+def _gemm_case(M_, N, K, epi, seed, rows=None):
+    """rows: compare only these output rows (the reference is computed for them alone)."""
     t = torch()
     rng = np.random.default_rng(seed)
     ab, af = rand_bf16(rng, (M_, K))
@@ -41,15 +42,17 @@ def _gemm_case(M_, N, K, epi, seed):
     hxf.op_gemm(A.data_ptr(), K, B.data_ptr(), B2.data_ptr() if B2 is not None else 0, C.data_ptr(), n_out, M_, N, K,
                 epi, ws.data_ptr(), ws.numel())
     t.cuda.synchronize()
+    sel = np.arange(M_) if rows is None else np.asarray(rows)
+    a_s = af[sel]
     if epi == hxf.EPI_SWIGLU:
-        ref = M.silu(af @ bf.T) * (af @ b2f.T)
-        got = host_f64(C).reshape(M_, n_out)
+        ref = M.silu(a_s @ bf.T) * (a_s @ b2f.T)
+        got = host_f64(C).reshape(M_, n_out)[sel]
     elif epi == hxf.EPI_BF16:
-        ref = af @ bf.T
-        got = host_f64(C).reshape(M_, n_out)
+        ref = a_s @ bf.T
+        got = host_f64(C).reshape(M_, n_out)[sel]
     else:
-        ref = af @ bf.T + (base.astype(np.float64) if epi == hxf.EPI_RESID else 0.0)
-        got = C.cpu().numpy().astype(np.float64).reshape(M_, n_out)
+        ref = a_s @ bf.T + (base[sel].astype(np.float64) if epi == hxf.EPI_RESID else 0.0)
+        got = C.cpu().numpy().astype(np.float64).reshape(M_, n_out)[sel]
     scale = np.max(np.abs(ref))
     rtol = 2 ** -7 if epi in (hxf.EPI_BF16, hxf.EPI_SWIGLU) else 1e-5
     np.testing.assert_allclose(got, ref, rtol=rtol, atol=2e-4 * scale)
@@ -75,6 +78,20 @@ def test_gemm(M_, N, K, epi):
                                     (64, 2 * 28672, 8192), (1024, 2 * 5632, 1000), (2080, 2 * 7168, 1000)])
 def test_gemm_swiglu(M_, N, K):
     _gemm_case(M_, N, K, hxf.EPI_SWIGLU, seed=M_ + N + K)
+
+
+@pytest.mark.parametrize("name,M_,N,K,epi", [
+    ("8B qkv", 2080, 6144, 4096, hxf.EPI_BF16), ("8B o", 2080, 4096, 4096, hxf.EPI_RESID),
+    ("8B gate/up", 2080, 2 * 14336, 4096, hxf.EPI_SWIGLU), ("8B down", 2080, 4096, 14336, hxf.EPI_RESID),
+    ("70B qkv", 2080, 10240, 8192, hxf.EPI_BF16), ("70B down", 2080, 8192, 28672, hxf.EPI_RESID),
+    ("8B lm head", 64, 128256, 4096, hxf.EPI_F32)])
+def test_gemm_full_size_sampled(name, M_, N, K, epi):
+    """Mixed-iteration projections at their full sizes (2048 prefill + 32 decode rows) in the
+    launch configuration the forward uses; the reference is computed for sampled rows: the
+    first and last of every 32-row tile boundary region and the ragged tail."""
+    rows = sorted(r for r in set(list(range(0, M_, 97)) + [31, 32, 255, 256, M_ - 33, M_ - 32, M_ - 1]) if r < M_)
+    log(f"gemm full size {name}: {len(rows)} sampled rows")
+    _gemm_case(M_, N, K, epi, seed=M_ + N + K, rows=rows)
 
 
 def test_gemm_split_repeatable():
@@ -320,6 +337,12 @@ def _prefill_case(chunks, hq, hkv, dh, seed):
     for s, (p0, n) in enumerate(chunks):
         ref = P.paged_attention(qf[row0[s]:row0[s] + n], np.arange(p0, p0 + n), Kl, Vl, bts[s], p0 + n)
         np.testing.assert_allclose(got[row0[s]:row0[s] + n], ref, rtol=1e-2, atol=1e-2, err_msg=f"chunk {s}")
+
+
+def test_prefill_attention_cfg3_full_size():
+    """Workload-3 chunks at full size, 8B heads: the first 2048-token chunk of a prompt
+    and the last chunk of an 8192-token prompt (queries at 6144-8191), in one launch."""
+    _prefill_case([(0, 2048), (6144, 2048)], 32, 8, 128, seed=3)
 
 
 @pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128), (64, 8, 128), (8, 1, 128)])
