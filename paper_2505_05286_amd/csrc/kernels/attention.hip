@@ -313,7 +313,11 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   const int kend = pos0 + it.q0 + it.nq;       // keys [0, kend) are visible to some pair
   const int ntiles = (kend + 31) / 32;
   const int last_page = (kend - 1) / kPage;
-  const int32_t* bt = a.bt + (size_t)it.entry * a.bt_stride;
+  // the block table does not change during the kernel: read it through the constant
+  // address space, so that its (wavefront-uniform) entries come by scalar loads, which
+  // are counted apart from the vector loads and do not wait for the DMAs in flight
+  const __attribute__((address_space(4))) int32_t* bt =
+      (const __attribute__((address_space(4))) int32_t*)(a.bt + (size_t)it.entry * a.bt_stride);
   const int h = lane >> 5;
 
   // this lane's two pairs (columns lane % 32 of the wavefront's two pair tiles)
