@@ -354,7 +354,9 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
       const int pg = blk / (KT / 1024);
       const int page = min(tt * 2 + pg, last_page);
       const size_t tile = kv_tile(it.kvh, a.n_blocks, bt[page], DH);
-      dma16(a.v_pool + tile + (blk % (KT / 1024)) * 512 + lane * 8, base + KT + blk * 512);
+      // the two 16-byte halves of dims 8..15 (mod 16) of a block swap places in LDS, so that
+      // the 16 lanes of one V^T read pass hit distinct banks
+      dma16(a.v_pool + tile + (blk % (KT / 1024)) * 512 + (lane ^ ((lane >> 4) & 1)) * 8, base + KT + blk * 512);
     }
   };
 
@@ -375,7 +377,7 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   // operand offsets inside a stage: K for key lane%32 (page (lane%32)/16), dims chunk ks*2 + h;
   // V^T for dim dt*32 + lane%32, page s, positions 8h..8h+7
   const int k_off = ((lane & 31) >> 4) * (KT / 2) + (lane & 15) * 8 + h * 128;
-  const int v_off = KT + (lane & 31) * 16 + h * 8;
+  const int v_off = KT + (lane & 31) * 16 + (h ^ ((lane >> 3) & 1)) * 8;
 
   auto compute = [&](const bf16_t* base, int t) __attribute__((always_inline)) {
     f32x16 s[PT];
