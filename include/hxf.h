@@ -18,6 +18,10 @@
  *    buffer (weights, KV pool, workspace) and the HIP stream; see hxf_bind.
  *    It allocates only host memory (request state, pinned metadata staging).
  *  - An instance is single-threaded: calls on one instance must not overlap.
+ *  - Tracing: if the environment variable HXF_TRACE names a file when an instance is
+ *    created, every hxf_step that runs an iteration appends one JSON line to it
+ *    (instance, iteration, now_us, t_iter_us, batch token/row counts, cost-model terms,
+ *    finished count, free pages, ids admitted).
  */
 #ifndef HXF_H
 #define HXF_H

@@ -1,6 +1,8 @@
 // C ABI of the serving instance (include/hxf.h).
 #include <algorithm>
 #include <chrono>
+#include <cstdio>
+#include <cstdlib>
 #include <memory>
 #include <new>
 #include <string>
@@ -39,7 +41,11 @@ class NullExecutor : public Executor {
 
 struct hxf_instance {
   hxf_instance(const hxf_model_cfg& m, const hxf_sched_cfg& s) : sched(m, s) {}
+  ~hxf_instance() {
+    if (trace) std::fclose(trace);
+  }
   Scheduler sched;
+  std::FILE* trace = nullptr;   // HXF_TRACE: one JSON line per iteration
   std::unique_ptr<Executor> exec;
   std::string err;
   std::vector<BatchEntry> batch;
@@ -79,6 +85,7 @@ int hxf_create(const hxf_model_cfg* model, const hxf_sched_cfg* sched, hxf_insta
   try {
     inst = new hxf_instance(*model, *sched);
     if (sched->executor == HXF_EXEC_NULL) inst->exec = std::make_unique<NullExecutor>(model->vocab);
+    if (const char* path = std::getenv("HXF_TRACE"); path && path[0]) inst->trace = std::fopen(path, "a");
   } catch (...) {
     delete inst;
     return HXF_ENOMEM;
@@ -199,6 +206,19 @@ int hxf_step(hxf_instance* inst, int64_t now_us, hxf_step_info* out) {
   info.t_iter_us = dt;
   S.commit(inst->batch, inst->sampled, now_us + dt, &info.n_finished);
   info.free_blocks = S.alloc.n_free();
+  if (inst->trace) {
+    std::fprintf(inst->trace,
+                 "{\"instance\":\"%p\",\"iteration\":%lld,\"now_us\":%lld,\"t_iter_us\":%lld,\"n_tokens\":%d,"
+                 "\"n_decode\":%d,\"n_prefill_tokens\":%d,\"n_logit_rows\":%d,\"sum_decode_ctx\":%lld,"
+                 "\"prefill_attn\":%lld,\"n_finished\":%d,\"free_blocks\":%lld,\"admitted\":[",
+                 (void*)inst, (long long)info.iteration, (long long)now_us, (long long)dt, info.n_tokens, info.n_decode,
+                 info.n_prefill_tokens, info.n_logit_rows, (long long)sum_ctx, (long long)attn, info.n_finished,
+                 (long long)info.free_blocks);
+    for (size_t i = 0; i < inst->admitted.size(); ++i)
+      std::fprintf(inst->trace, i ? ",%llu" : "%llu", (unsigned long long)inst->admitted[i]);
+    std::fprintf(inst->trace, "]}\n");
+    std::fflush(inst->trace);
+  }
   if (out) *out = info;
   return HXF_OK;
   GUARD_END

@@ -10,7 +10,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libhxf.so")
+# HXF_LIBRARY selects another build of the library (e.g. one with instrumented host code)
+LIB_PATH = os.environ.get("HXF_LIBRARY") or os.path.join(_HERE, "libhxf.so")
 
 OK, IDLE = 0, 1
 EINVAL, ENOMEM, ENOTFOUND, ESTATE, EDEVICE = -1, -2, -3, -4, -5

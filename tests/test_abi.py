@@ -60,3 +60,34 @@ def test_ops_reject_bad_arguments_without_launching():
     assert e.value.code == hxf.EINVAL
     with pytest.raises(hxf.HxfError):
         hxf.op_decode_attention(1, 1, 1, 8, 1, 1, [0], 1, 1, 4, 3, 128, 1, 1)   # Hq % Hkv
+
+
+def test_iteration_trace_log(tmp_path, monkeypatch):
+    """HXF_TRACE: one JSON line per iteration, matching what hxf_step returned."""
+    import json
+
+    import numpy as np
+    ensure_built()
+    path = tmp_path / "trace.jsonl"
+    monkeypatch.setenv("HXF_TRACE", str(path))
+    shape = synth.ModelShape("sched", 1, 64, 1, 1, 64, 64, 2048, 0)
+    inst = hxf.Instance(hxf.model_cfg(shape, 4096),
+                        hxf.sched_cfg(64, 4, 32, (1000 * 10**6, 10**6, 0, 10**6), (500 * 10**6, 10**6, 0, 0),
+                                      executor=hxf.EXEC_NULL))
+    ids = [inst.submit(0, k, 0, 0, 10**9, np.arange(20 + k, dtype=np.int32), 3) for k in range(3)]
+    infos, now = [], 0
+    while True:
+        st, info = inst.step(now)
+        if st == hxf.IDLE:
+            break
+        infos.append((now, info))
+        now += info["t_iter_us"]
+    inst.close()
+    lines = [json.loads(l) for l in open(path)]
+    assert len(lines) == len(infos) > 1
+    for (t, info), rec in zip(infos, lines):
+        assert rec["now_us"] == t
+        for k in ("iteration", "t_iter_us", "n_tokens", "n_decode", "n_prefill_tokens", "n_logit_rows",
+                  "sum_decode_ctx", "prefill_attn", "n_finished", "free_blocks"):
+            assert rec[k] == info[k], k
+    assert sorted(i for rec in lines for i in rec["admitted"]) == sorted(ids)
