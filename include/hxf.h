@@ -22,6 +22,10 @@
  *    created, every hxf_step that runs an iteration appends one JSON line to it
  *    (instance, iteration, now_us, t_iter_us, batch token/row counts, cost-model terms,
  *    finished count, free pages, ids admitted).
+ *  - Checked mode: with HXF_CHECK=1 in the environment when hxf_bind runs, every
+ *    iteration's indices (token ids, positions, KV slots, block tables, attention work
+ *    items) are validated on the host before any kernel is launched; a violation makes
+ *    hxf_step return HXF_EINVAL with the reason in hxf_last_error.
  */
 #ifndef HXF_H
 #define HXF_H

@@ -130,6 +130,8 @@ class HipExecutor : public Executor {
     ws_ = reinterpret_cast<uint8_t*>(b.workspace);
     const char* ng = std::getenv("HXF_NO_GRAPHS");
     use_graphs_ = !(ng && ng[0] && ng[0] != '0');
+    const char* ck = std::getenv("HXF_CHECK");
+    check_ = ck && ck[0] && ck[0] != '0';
   }
 
   ~HipExecutor() override {
@@ -195,6 +197,7 @@ class HipExecutor : public Executor {
   std::unordered_set<int64_t> seen_;   // shapes met once, not captured yet
   int64_t graph_clock_ = 0;
   bool use_graphs_ = true;
+  bool check_ = false;   // HXF_CHECK: validate every index the kernels will follow before launching
   // The legacy null stream cannot be captured: graphs then run on a stream of our own
   // (blocking, default priority), which the null stream orders against.
   hipStream_t graph_st_ = nullptr;
@@ -316,6 +319,52 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   std::memcpy(hm + o_ditems, ditems.data(), ditems.size() * sizeof(DecodeItem));
   std::memcpy(hm + o_merges, merges.data(), merges.size() * sizeof(MergeItem));
   std::memcpy(hm + o_pitems, pitems.data(), pitems.size() * sizeof(PrefillItem));
+  if (check_) {
+    // every index a kernel follows, checked on the host against the buffers it addresses
+    auto fail = [&](const char* what, int64_t i) {
+      err = std::string("check: ") + what + " (index " + std::to_string(i) + ")";
+      return HXF_EINVAL;
+    };
+    const int64_t slots = s_.n_blocks * kPage;
+    for (int64_t i = 0; i < T; ++i) {
+      if (hm[o_ids + i] < 0 || hm[o_ids + i] >= m_.vocab) return fail("token id outside the vocabulary", i);
+      if (hm[o_pos + i] < 0 || hm[o_pos + i] >= m_.max_context) return fail("position outside max_context", i);
+      if (hm[o_slot + i] < 0 || hm[o_slot + i] >= slots) return fail("KV slot outside the pool", i);
+    }
+    for (int i = 0; i < R; ++i)
+      if (hm[o_lrow + i] < 0 || hm[o_lrow + i] >= T) return fail("logits row outside the batch", i);
+    std::vector<int32_t> ctx(E);
+    for (int e = 0; e < E; ++e) {
+      ctx[e] = batch[e].pos0 + batch[e].n;
+      const int64_t np = ceil_div((int64_t)ctx[e], kPage);
+      if (np > bt_w) return fail("block table wider than its stride", e);
+      for (int64_t j = 0; j < np; ++j) {
+        const int32_t b = hm[o_bt + (int64_t)e * bt_w + j];
+        if (b < 0 || b >= s_.n_blocks) return fail("block-table entry outside the pool", e);
+      }
+    }
+    for (size_t i = 0; i < ditems.size(); ++i) {
+      const DecodeItem& d = ditems[i];
+      if (d.kvh < 0 || d.kvh >= hkv || d.t0 < 0 || d.t0 >= d.t1 || d.n_rows < 1 || d.n_rows > kDecodeRows)
+        return fail("decode item", (int64_t)i);
+      for (int k = 0; k < d.n_rows; ++k)
+        if (d.entry[k] < 0 || d.entry[k] >= E || !batch[d.entry[k]].decode || d.t1 > ctx[d.entry[k]] ||
+            d.part[k] < 0 || d.part[k] >= dplan_.n_parts)
+          return fail("decode item row", (int64_t)i);
+    }
+    for (size_t i = 0; i < merges.size(); ++i) {
+      const MergeItem& mi = merges[i];
+      if (mi.entry < 0 || mi.entry >= E || mi.kvh < 0 || mi.kvh >= hkv || mi.n_part < 1 || mi.part0 < 0 ||
+          mi.part0 + mi.n_part > dplan_.n_parts)
+        return fail("merge item", (int64_t)i);
+    }
+    for (size_t i = 0; i < pitems.size(); ++i) {
+      const PrefillItem& pi = pitems[i];
+      if (pi.entry < 0 || pi.entry >= E || batch[pi.entry].decode || pi.kvh < 0 || pi.kvh >= hkv || pi.q0 < 0 ||
+          pi.nq < 1 || pi.q0 + pi.nq > batch[pi.entry].n)
+        return fail("prefill item", (int64_t)i);
+    }
+  }
   int32_t* dm = dev<int32_t>(plan_.off_meta);
 
   // ---------------------------------------------------------- forward

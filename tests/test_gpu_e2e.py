@@ -294,3 +294,32 @@ def test_graph_replays_match_eager_steps_with_forks(monkeypatch):
     assert steps > 390
     for ra, rb in zip(ka, kb):
         assert ga.inst.tokens(ra) == gb.inst.tokens(rb)
+
+
+def test_checked_mode_runs_clean(monkeypatch):
+    """HXF_CHECK=1 validates every index the kernels follow (tokens, positions, KV slots,
+    block tables, attention work items) on the host before each launch: a run with forks
+    (shared-prefix decode items), chunked prefill and plain decode raises nothing and gives
+    the tokens of an unchecked run."""
+    shape, dm, w = device_model("tiny")
+    rng = np.random.default_rng(31)
+    prompt = rng.integers(0, shape.vocab, 70)
+    others = [rng.integers(0, shape.vocab, n) for n in (20, 130)]
+    apps = [rng.integers(0, shape.vocab, n) for n in (0, 5, 17)]
+
+    def run():
+        eng = Engine(dm, max_context=512, n_blocks=96, max_seqs=8, chunk_tokens=64, cost_ps=COST, iter_ps=ITER)
+        par = eng.inst.submit(0, 0, 0, 0, 10 ** 7, prompt, 3, retain=True)
+        now = 0
+        while eng.inst.step(now)[0] != hxf.IDLE:
+            now += 1000
+        ids = [eng.inst.submit(now, 0, 1, 0, 10 ** 7, a, 6, parent=par) for a in apps]
+        ids += [eng.inst.submit(now, 1 + k, 0, 0, 10 ** 7, p, 6) for k, p in enumerate(others)]
+        while eng.inst.step(now)[0] != hxf.IDLE:
+            now += 1000
+        return [eng.inst.tokens(r) for r in ids]
+
+    plain = run()
+    monkeypatch.setenv("HXF_CHECK", "1")
+    checked = run()
+    assert checked == plain
