@@ -283,7 +283,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeAttnArgs a) {
 //   S^T[32 keys x 32 pairs] = K[32 x dh] . Q^T[dh x 32]       (v_mfma_f32_32x32x16_bf16)
 //   O^T[32 dims x 32 pairs] += V^T[32 x 32 keys] . P^T[32 x 32]
 // (64 pairs per wavefront, two 32-pair tiles).  Tiles of 32 keys (two pages)
-// of K and V are moved into LDS by the DMA path, four tiles in flight, and
+// of K and V are moved into LDS by the DMA path, five tiles in flight, and
 // shared by the four wavefronts.  A lane of the S^T accumulator holds keys
 // 8m + 4h + i (h = lane / 32) of its pair; taken in the order m = 2s, 2s + 1
 // these are the 8 keys of the P^T operand for the 16-key step s (page s of the
@@ -299,11 +299,12 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   constexpr int K_W = KT / 512 / 4;            // 16-byte DMA instructions per wavefront for K
   constexpr int V_W = KT / 512 / 4;            // and for V
   constexpr int PER_W = K_W + V_W;
-  __shared__ __attribute__((aligned(1024))) bf16_t L0[STAGE], L1[STAGE], L2[STAGE], L3[STAGE];
+  constexpr int NS = 5;                        // key tiles in flight: NS - 1 ahead of the one computed
+  __shared__ __attribute__((aligned(1024))) bf16_t L0[STAGE], L1[STAGE], L2[STAGE], L3[STAGE], L4[STAGE];
   auto slot = [&](auto ic) -> bf16_t* {
-    constexpr int I = decltype(ic)::value % 4;
+    constexpr int I = decltype(ic)::value % NS;
     if constexpr (I == 0) return L0; else if constexpr (I == 1) return L1; else if constexpr (I == 2) return L2;
-    else return L3;
+    else if constexpr (I == 3) return L3; else return L4;
   };
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const PrefillItem it = a.items[blockIdx.x];
@@ -466,20 +467,20 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
     }
   };
 
-  static_for<3>([&](auto ic) { issue(decltype(ic)::value, slot(ic)); });
+  static_for<NS - 1>([&](auto ic) { issue(decltype(ic)::value, slot(ic)); });
   int t0 = 0;
-  for (; t0 + 4 <= ntiles; t0 += 4) {
-    static_for<4>([&](auto ic) {
+  for (; t0 + NS <= ntiles; t0 += NS) {
+    static_for<NS>([&](auto ic) {
       constexpr int J = decltype(ic)::value;
-      wait_vmcnt<2 * PER_W>();
+      wait_vmcnt<(NS - 2) * PER_W>();
       __builtin_amdgcn_s_barrier();
-      issue(t0 + J + 3, slot(std::integral_constant<int, J + 3>{}));
+      issue(t0 + J + NS - 1, slot(std::integral_constant<int, J + NS - 1>{}));
       compute(slot(ic), t0 + J);
     });
   }
   wait_vmcnt<0>();
   __builtin_amdgcn_s_barrier();
-  static_for<3>([&](auto ic) {
+  static_for<NS - 1>([&](auto ic) {
     constexpr int J = decltype(ic)::value;
     if (t0 + J < ntiles) compute(slot(ic), t0 + J);
   });
