@@ -187,13 +187,11 @@ def cpu_baselines():
 # t_iter = (i0 + i1*T + i2*sum_decode_ctx + i3*prefill_attention_pairs) / 1e6 us
 COST_PS = {
     # (c0, c1, c2, d1) of t_comp and (i0, i1, i2, i3) of the virtual iteration, picoseconds:
-    # fitted to measured iterations on one MI355X by `bench.py --calibrate <model>`; the 8B and
-    # 32B pairs come from the earlier four-term procedure (a decode row priced like a prefill
-    # token, decode-only iterations only at small batches), which fitted their data to 0.3-0.6%
-    # median error and is kept because the workload-5 runs and the policy ablation use it
-    "llama8b": ((3_855_276_245, 17_641_835, 286, 3_948_937_446), (3_855_276_245, 15_173_800, 19_162, 572)),
-    "qwen32b": ((13_126_065_958, 71_492_740, 997, 13_368_178_414), (13_126_065_958, 63_041_887, 43_718, 1_994)),
-    # five-term iteration model (decode rows priced apart), fitted by the current procedure
+    # fitted to measured iterations on one MI355X by `bench.py --calibrate <model>` (five-term
+    # iteration model, decode rows priced apart)
+    "llama8b": ((4_383_794_963, 16_710_429, 234, 4_470_257_482), (4_383_794_963, 14_089_711, 20_149, 469, 3_934_053)),
+    "qwen32b": ((13_843_718_843, 69_707_878, 806, 14_035_778_677),
+                (13_843_718_843, 61_297_098, 38_500, 1_612, 34_363_125)),
     "llama70b": ((25_849_666_649, 154_627_611, 572, 26_181_289_978), (25_849_666_649, 140_833_739, 80_963, 1_144, 0)),
 }
 

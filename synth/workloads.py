@@ -21,8 +21,8 @@ import numpy as np
 # Reference isolated latency per shape: base + per-prompt-token + per-output-token (us).
 REF_LATENCY = {
     "tiny": (200, 0.05, 150),
-    "llama8b": (3855, 18.8, 3949),
-    "qwen32b": (13126, 75.6, 13368),
+    "llama8b": (4384, 17.7, 4470),
+    "qwen32b": (13844, 73.0, 14036),
     "llama70b": (25850, 157.0, 26181),
 }
 
