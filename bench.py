@@ -12,11 +12,15 @@ upload, 32 layers of GEMMs / RoPE / paged attention, LM head, argmax, and the
 sampled ids back on the host.
 
 Prints one JSON line.  `value` is decode tokens/s over the K timed steps.
-`roofline` is the paged decode-attention kernel (the largest single kernel of
-the step): algorithmic K+V bytes per launch over its average duration, timed
-with HIP events that the launch itself stamps with the kernel's start and end
-(hipExtLaunchKernel) on the instance's stream.  `cpu_baseline` times the CPU
-oracle on a bounded sample of the same step.
+`roofline` is the paged decode attention (the largest single item of the
+step): its split-K kernel plus the log-sum-exp merge that follows it, the
+algorithmic K+V bytes per layer over their summed average duration, timed with
+HIP events that each launch itself stamps with the kernel's start and end
+(hipExtLaunchKernel) on the instance's stream; `attention_only` is the split-K
+kernel alone.  `gemm_roofline` is the MFMA roofline of the prefill projections
+(2080 rows: workload 3's 2048-token chunk plus 32 decodes), timed the same way
+over profiled mixed iterations.  `cpu_baseline` times the CPU oracle on a
+bounded sample of the decode step.
 """
 import argparse
 import json
@@ -273,6 +277,62 @@ def kv_pages_that_fit(shape, reserve_gb=8.0, frac=0.9):
     free, _ = torch.cuda.mem_get_info()
     page = 2 * shape.n_kv_heads * shape.head_dim * 2 * 16 * shape.n_layers
     return int(max(free - reserve_gb * 1e9, 0) * frac // page)
+
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def mixed_iteration_profile(dm, shape, n_profiled=3):
+    """Kernel-stamped timing of workload-3 mixed iterations (a 2048-token prefill chunk
+    co-batched with 32 decode rows: 2080-row projections).  The 32 decodes are prefilled
+    first (untimed), the 16 prompts submitted, then `n_profiled` mixed iterations run with
+    profiling on (eager launches, HIP events stamped by every GEMM and prefill-attention
+    launch).  Returns the MFMA roofline of each projection and of a whole layer's four,
+    2*M*N*K / kernel time / 2.5 PFLOP/s, and of the prefill attention."""
+    import synth
+    from paper_2505_05286_amd import hxf
+    from paper_2505_05286_amd.device import Engine
+    decodes, prompts = synth.workloads.cfg3(shape.vocab)
+    cost, it = COST_PS.get(shape.name, COST_PS["llama8b"])
+    total = sum(-(-(len(s.prompt) + 4096) // 16) for s in decodes) + sum(-(-len(s.prompt) // 16) for s in prompts)
+    eng = Engine(dm, max_context=8192 + 4096, n_blocks=total + 256, max_seqs=64, chunk_tokens=2048, cost_ps=cost,
+                 iter_ps=it, clock=hxf.CLOCK_MEASURED)
+    inst = eng.inst
+    for s in decodes:
+        inst.submit(0, s.workflow, 0, 0, s.wf_slo_us, s.prompt, s.max_new_tokens)
+    now, *_ = step_until(inst, 0, lambda i: i["n_prefill_tokens"] == 0)
+    for s in prompts:
+        inst.submit(now, s.workflow, 0, now, s.wf_slo_us, s.prompt, s.max_new_tokens)
+    inst.profile_enable(True)
+    rows = []
+    now, iters, pf, dec, dt = step_until(inst, now, lambda i: len(rows) >= n_profiled,
+                                         per_step=lambda i: rows.append(i["n_tokens"]))
+    prof = inst.profile()
+    inst.profile_enable(False)
+    del eng, inst
+    peak = MFMA_BF16_PEAK_TFLOPS
+    per = {}
+    for k in ("qkv", "o", "gate_up", "down"):
+        ms, fl, n = prof["gemm_ms"][k], prof["gemm_flops"][k], prof["gemm_launches"][k]
+        ach = fl / (ms * 1e-3) / 1e12
+        per[k] = {"launches": n, "avg_us": round(ms / n * 1e3, 1), "tflops": round(ach, 1),
+                  "frac": round(ach / peak, 4)}
+    fl = sum(prof["gemm_flops"][k] for k in per)
+    ms = sum(prof["gemm_ms"][k] for k in per)
+    layer = fl / (ms * 1e-3) / 1e12
+    pa = prof["prefill_attn_flops"] / (prof["prefill_attn_ms"] * 1e-3) / 1e12
+    return {"bound": "mfma", "achieved": round(layer, 1), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(layer / peak, 4), "traffic": None,
+            "kernels": "gemm_big_kernel (QKV, O, gate/up + SwiGLU, down) of every layer",
+            "workload": "3: mixed iterations, 2048-token prefill chunk + 32 decode rows",
+            "rows_per_iteration": rows, "iterations_profiled": iters,
+            "ms_per_iteration_profiled": round(dt / iters * 1e3, 2),
+            "timing": "kernel-stamped HIP events, 2*M*N*K per launch over its duration",
+            "per_projection": per,
+            "prefill_attention": {"launches": prof["prefill_attn_launches"], "tflops": round(pa, 1),
+                                  "frac": round(pa / peak, 4),
+                                  "avg_us": round(prof["prefill_attn_ms"] / max(prof["prefill_attn_launches"], 1)
+                                                  * 1e3, 1)}}
 
 
 def workload3(model="llama8b"):
@@ -746,6 +806,8 @@ def main():
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemm-roofline", action="store_true",
+                    help="skip the profiled workload-3 iterations that give gemm_roofline")
     ap.add_argument("--workload", type=int, default=2, choices=(1, 2, 3, 4, 5),
                     help="2 (default) prints the benchmark line; 1, 3-5 print per-workload measurements")
     ap.add_argument("--n-workflows", type=int, default=16, help="workload 5: workflows replayed")
@@ -890,23 +952,29 @@ def main():
         "data": "synthetic",
         "config": {"workload": (f"decode iteration, {describe(shape)}, 64 sequences, contexts lognormal(median "
                                 "3000, sigma 0.5) clipped to [1024, 8192], 16-token KV pages"),
+                   "value_is": "decode tokens/s of the timed steps (64 sequences x steps / seconds)",
                    "batch": BATCH, "layers": shape.n_layers, "sum_context_tokens": int(sum_ctx_now)},
         "prefill_tokens_per_s": round(pf_tokens / t_pf, 1),
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "roofline": {"bound": "hbm", "achieved": round(achieved_merged, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved_merged / HBM_PEAK_GBS, 4),
                      "traffic": DECODE_ATTN_TRAFFIC["bytes_per_launch"] if default_shape else None,
                      "traffic_sample": DECODE_ATTN_TRAFFIC if default_shape else None,
-                     "kernel": "decode_attn_kernel<128>", "avg_launch_us": round(avg_ms * 1e3, 2),
-                     "timing": (f"kernel-stamped HIP events on the {int(launches)} decode-attention launches of "
-                                f"{roof_steps} eager decode steps run right after the timed (graph-replayed) steps"),
+                     "kernel": "decode_attn_kernel<128> + decode_merge_kernel<128> (split-K attention and its "
+                               "log-sum-exp merge, one layer per launch pair)",
+                     "avg_launch_us": round((avg_ms + merge_ms) * 1e3, 2),
+                     "timing": (f"kernel-stamped HIP events on the {int(launches)} decode-attention and merge launch "
+                                f"pairs of {roof_steps} eager decode steps run right after the timed (graph-replayed) "
+                                "steps"),
                      "bytes_per_launch": int(bytes_per_launch),
-                     "with_merge": {"kernels": "decode_attn_kernel<128> + decode_merge_kernel<128>",
-                                    "avg_us": round((avg_ms + merge_ms) * 1e3, 2),
-                                    "achieved": round(achieved_merged, 1),
-                                    "frac": round(achieved_merged / HBM_PEAK_GBS, 4)}},
+                     "attention_only": {"kernel": "decode_attn_kernel<128>", "avg_us": round(avg_ms * 1e3, 2),
+                                        "achieved": round(achieved, 1),
+                                        "frac": round(achieved / HBM_PEAK_GBS, 4)}},
     }
     out["hbm_copy_probe"] = hbm_copy_probe()
     del eng, inst
+    if not args.no_gemm_roofline:
+        progress("workload-3 mixed iterations, profiled: MFMA roofline of the 2080-row projections")
+        out["gemm_roofline"] = mixed_iteration_profile(dm, shape)
     if not args.no_cpu_baseline:
         progress("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(shape, ctxs)

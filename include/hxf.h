@@ -230,14 +230,25 @@ int hxf_last_batch(hxf_instance* inst, uint64_t* ids, int32_t cap, int32_t* n,
 /* fp32 logits (vocab floats) of the request's row in the last iteration; HXF_ENOTFOUND if it had none. */
 int hxf_last_logits(hxf_instance* inst, uint64_t id, float* dst, int32_t cap);
 
-/* Kernel timing of the decode-attention launches (HIP events stamped with the
- * kernels' own start and end on the bound stream), for roofline reporting.
- * Enabling resets the counters. */
+/* Kernel timing for roofline reporting: HIP events stamped with the kernels' own
+ * start and end on the bound stream.  While profiling is on, iterations launch
+ * eagerly (no graph replay).  Enabling resets the counters. */
+enum { HXF_PROF_QKV = 0, HXF_PROF_O = 1, HXF_PROF_GATE_UP = 2, HXF_PROF_DOWN = 3, HXF_PROF_LM_HEAD = 4 };
 typedef struct hxf_profile {
   int64_t decode_attn_launches;  /* split-K attention kernel launches timed */
   int64_t decode_attn_bytes;     /* algorithmic K+V bytes those launches read (context tokens x 2 x dh x 2 B x kv-heads) */
   double decode_attn_ms;         /* summed split-K kernel time */
   double decode_merge_ms;        /* summed time of the log-sum-exp merge kernels that follow them */
+  /* GEMMs by projection (HXF_PROF_*): launches, 2*M*N*K flops, time from the first
+   * kernel's start to the last one's end (a split-K reduction pass included). */
+  int64_t gemm_launches[5];
+  double gemm_flops[5];
+  double gemm_ms[5];
+  /* chunked-prefill attention: launches, 4*dh flops per (query, key, q-head) inside the
+   * causal mask, summed kernel time */
+  int64_t prefill_attn_launches;
+  double prefill_attn_flops;
+  double prefill_attn_ms;
 } hxf_profile;
 
 int hxf_profile_enable(hxf_instance* inst, int32_t on);

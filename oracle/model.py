@@ -102,19 +102,34 @@ class Weights:
     be run layer by layer.
     """
 
-    def __init__(self, shape, seed=None, keep_layers=True):
+    def __init__(self, shape, seed=None, keep_layers=True, norm_gains=None, layer_bits=None, embed_bits=None,
+                 lm_head_bits=None):
+        """norm_gains: None (every RMSNorm gain is 1, as in the workloads) or a dict of
+        bf16 bits with one gain per norm: attn [L, d], ffn [L, d], final [d].
+        layer_bits(l), embed_bits, lm_head_bits: the synthetic bf16 bits, when the
+        caller already holds them (default: drawn from ``synth`` with the seed)."""
         self.shape = shape
         self.seed = shape.weight_seed if seed is None else seed
         self.keep = keep_layers
+        self._layer_bits = layer_bits
         self._layers = {}
-        self._embed_bits = None
-        self._lm = None
-        self.norm = synth.bf16_bits_to_f32(synth.norm_weight(shape)).astype(F)
+        self._embed_bits = embed_bits
+        self._lm = None if lm_head_bits is None else synth.bf16_bits_to_f32(lm_head_bits)
+        L = shape.n_layers
+        if norm_gains is None:
+            ones = synth.bf16_bits_to_f32(synth.norm_weight(shape)).astype(F)
+            self.attn_norm = [ones] * L
+            self.ffn_norm = [ones] * L
+            self.final_norm = ones
+        else:
+            self.attn_norm = [synth.bf16_bits_to_f32(norm_gains["attn"][l]).astype(F) for l in range(L)]
+            self.ffn_norm = [synth.bf16_bits_to_f32(norm_gains["ffn"][l]).astype(F) for l in range(L)]
+            self.final_norm = synth.bf16_bits_to_f32(norm_gains["final"]).astype(F)
 
     def layer(self, l):
         if l in self._layers:
             return self._layers[l]
-        raw = synth.gen_layer(self.shape, l, self.seed)
+        raw = synth.gen_layer(self.shape, l, self.seed) if self._layer_bits is None else self._layer_bits(l)
         w = {k: synth.bf16_bits_to_f32(v).astype(F) for k, v in raw.items()}
         if self.keep:
             self._layers[l] = w
@@ -149,6 +164,19 @@ class Sequence:
         self.v = [None] * n_layers
         self.n = 0          # tokens whose KV is stored
 
+    def fork(self, n_keep):
+        """A new sequence holding a copy of this one's KV for positions [0, n_keep):
+        the context a forked request continues from (KV of earlier positions
+        depends only on earlier tokens)."""
+        assert 0 <= n_keep <= self.n
+        s = Sequence(len(self.k))
+        for l in range(len(self.k)):
+            if self.k[l] is not None and n_keep > 0:
+                s.k[l] = self.k[l][:n_keep].copy()
+                s.v[l] = self.v[l][:n_keep].copy()
+        s.n = n_keep
+        return s
+
     def append(self, layer, k, v):
         if self.k[layer] is None:
             self.k[layer], self.v[layer] = k, v
@@ -173,7 +201,7 @@ def forward(weights, seqs, chunks, logit_rows=None):
     x = weights.embed_rows(np.concatenate([np.asarray(c) for c in chunks]))
     for l in range(sh.n_layers):
         w = weights.layer(l)
-        h = rmsnorm(x, weights.norm, sh.rms_eps)
+        h = rmsnorm(x, weights.attn_norm[l], sh.rms_eps)
         q = (h @ w["wq"].T).reshape(-1, hq, dh)
         k = (h @ w["wk"].T).reshape(-1, hkv, dh)
         v = (h @ w["wv"].T).reshape(-1, hkv, dh)
@@ -186,7 +214,7 @@ def forward(weights, seqs, chunks, logit_rows=None):
             kpos = np.arange(s.k[l].shape[0])
             att[a:b] = attention(qi, s.k[l], s.v[l], pos[i], kpos)
         x = x + att.reshape(-1, hq * dh) @ w["wo"].T
-        h = rmsnorm(x, weights.norm, sh.rms_eps)
+        h = rmsnorm(x, weights.ffn_norm[l], sh.rms_eps)
         x = x + (silu(h @ w["w_gate"].T) * (h @ w["w_up"].T)) @ w["w_down"].T
     for s, c in zip(seqs, chunks):
         s.n += len(c)
@@ -195,7 +223,7 @@ def forward(weights, seqs, chunks, logit_rows=None):
         sel = [lens[i] - 1] if logit_rows is None else logit_rows[i]
         rows.append(offs[i] + np.asarray(sel, dtype=int))
     flat = np.concatenate(rows) if rows else np.zeros(0, int)
-    hf = rmsnorm(x[flat], weights.norm, sh.rms_eps)
+    hf = rmsnorm(x[flat], weights.final_norm, sh.rms_eps)
     lg = weights.logits(hf) if len(flat) else np.zeros((0, sh.vocab))
     out, o = [], 0
     for r in rows:

@@ -347,6 +347,14 @@ int hxf_profile_get(hxf_instance* inst, hxf_profile* out) {
   out->decode_attn_bytes = p->decode_attn_bytes;
   out->decode_attn_ms = p->decode_attn_ms;
   out->decode_merge_ms = p->decode_merge_ms;
+  for (int i = 0; i < 5; ++i) {
+    out->gemm_launches[i] = p->gemm_launches[i];
+    out->gemm_flops[i] = p->gemm_flops[i];
+    out->gemm_ms[i] = p->gemm_ms[i];
+  }
+  out->prefill_attn_launches = p->prefill_attn_launches;
+  out->prefill_attn_flops = p->prefill_attn_flops;
+  out->prefill_attn_ms = p->prefill_attn_ms;
   return HXF_OK;
 }
 

@@ -165,8 +165,18 @@ class HipExecutor : public Executor {
   T* dev(int64_t off) { return reinterpret_cast<T*>(ws_ + off); }
   // With `pending` set, a split-K plan leaves its partials in the workspace and
   // *pending = its split count (0 when the GEMM finished its own epilogue).
+  // `kind` (HXF_PROF_*) names the projection for profiling.
   int gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M, int N, int K,
-           int epi, std::string& err, int* pending = nullptr);
+           int epi, int kind, std::string& err, int* pending = nullptr);
+  // A pair of events for a profiled launch of `kind` (0-4 GEMMs, 5 prefill attention)
+  // doing `flops`; null events when profiling is off.
+  int prof_events(int kind, double flops, hipEvent_t* e0, hipEvent_t* e1, std::string& err);
+  struct ProfEv {
+    int kind;
+    hipEvent_t e0, e1;
+    double flops;
+  };
+  std::vector<ProfEv> prof_ev_;
 
   hxf_model_cfg m_;
   hxf_sched_cfg s_;
@@ -209,8 +219,17 @@ class HipExecutor : public Executor {
   }
 };
 
+int HipExecutor::prof_events(int kind, double flops, hipEvent_t* e0, hipEvent_t* e1, std::string& err) {
+  *e0 = *e1 = nullptr;
+  if (!prof.on) return HXF_OK;
+  HXF_HIP(hipEventCreate(e0));
+  HXF_HIP(hipEventCreate(e1));
+  prof_ev_.push_back(ProfEv{kind, *e0, *e1, flops});
+  return HXF_OK;
+}
+
 int HipExecutor::gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M,
-                      int N, int K, int epi, std::string& err, int* pending) {
+                      int N, int K, int epi, int kind, std::string& err, int* pending) {
   GemmArgs a{};
   a.A = A;
   a.B = B;
@@ -229,7 +248,9 @@ int HipExecutor::gemm(const uint16_t* A, int lda, const uint16_t* B, const uint1
     return HXF_EINVAL;
   }
   const bool defer = pending && p.splits > 1;
-  HXF_HIP(gemm_launch(a, epi, p, st_, !defer));
+  hipEvent_t e0, e1;
+  if (int rc = prof_events(kind, 2.0 * M * N * K, &e0, &e1, err)) return rc;
+  HXF_HIP(gemm_launch(a, epi, p, st_, !defer, e0, e1));
   if (pending) *pending = defer ? p.splits : 0;
   return HXF_OK;
 }
@@ -416,6 +437,10 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   pa.scale_log2 = scale_log2;
 
   const int64_t kv_tokens = dplan_.kv_tokens;
+  // prefill attention work: 4*dh flops per (query, visible key, q-head)
+  double pf_attn_flops = 0;
+  for (const auto& be : batch)
+    if (!be.decode) pf_attn_flops += ((double)be.n * be.pos0 + 0.5 * be.n * (be.n + 1.0)) * hq * 4.0 * dh;
   uint16_t* hr = dev<uint16_t>(plan_.off_hr);
   float* logits = dev<float>(plan_.off_logits);
   int32_t* samp = dev<int32_t>(plan_.off_sampled);
@@ -437,7 +462,8 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
         HXF_HIP(resid_rmsnorm_launch(resid, part, pend_down, T, nullptr, (const uint16_t*)L.attn_norm, h, T, d,
                                      m_.rms_eps, st_));
       int pend_qkv = 0;
-      if (int rc = gemm(h, d, (const uint16_t*)L.wqkv, nullptr, qkv, qkv_w, T, qkv_w, d, EPI_BF16, err, &pend_qkv))
+      if (int rc = gemm(h, d, (const uint16_t*)L.wqkv, nullptr, qkv, qkv_w, T, qkv_w, d, EPI_BF16, HXF_PROF_QKV, err,
+                        &pend_qkv))
         return rc;
       if (pend_qkv)
         HXF_HIP(rope_kv_partials_launch(qkv, part, pend_qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq,
@@ -463,24 +489,32 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
           ev_merge_.push_back(e3);
         }
       }
-      HXF_HIP(prefill_attn_launch(pa, st_));
+      if (pa.n_items) {
+        hipEvent_t e0, e1;
+        if (int rc = prof_events(5, pf_attn_flops, &e0, &e1, err)) return rc;
+        HXF_HIP(prefill_attn_launch(pa, st_, e0, e1));
+      }
       int pend_o = 0;
       if (int rc =
-              gemm(attn, hq * dh, (const uint16_t*)L.wo, nullptr, resid, d, T, d, hq * dh, EPI_RESID, err, &pend_o))
+              gemm(attn, hq * dh, (const uint16_t*)L.wo, nullptr, resid, d, T, d, hq * dh, EPI_RESID, HXF_PROF_O, err,
+                   &pend_o))
         return rc;
       HXF_HIP(resid_rmsnorm_launch(resid, part, pend_o, T, nullptr, (const uint16_t*)L.ffn_norm, h, T, d, m_.rms_eps,
                                    st_));
       if (int rc =
-              gemm(h, d, (const uint16_t*)L.w_gate, (const uint16_t*)L.w_up, act, f, T, 2 * f, d, EPI_SWIGLU, err))
+              gemm(h, d, (const uint16_t*)L.w_gate, (const uint16_t*)L.w_up, act, f, T, 2 * f, d, EPI_SWIGLU,
+                   HXF_PROF_GATE_UP, err))
         return rc;
-      if (int rc = gemm(act, f, (const uint16_t*)L.w_down, nullptr, resid, d, T, d, f, EPI_RESID, err, &pend_down))
+      if (int rc = gemm(act, f, (const uint16_t*)L.w_down, nullptr, resid, d, T, d, f, EPI_RESID, HXF_PROF_DOWN, err,
+                        &pend_down))
         return rc;
     }
     if (R > 0) {
       // (rows without logits never need the last down projection's partials)
       HXF_HIP(resid_rmsnorm_launch(resid, part, pend_down, T, dm + o_lrow, (const uint16_t*)b_.final_norm, hr, R, d,
                                    m_.rms_eps, st_));
-      if (int rc = gemm(hr, d, (const uint16_t*)b_.lm_head, nullptr, logits, m_.vocab, R, m_.vocab, d, EPI_F32, err))
+      if (int rc = gemm(hr, d, (const uint16_t*)b_.lm_head, nullptr, logits, m_.vocab, R, m_.vocab, d, EPI_F32,
+                           HXF_PROF_LM_HEAD, err))
         return rc;
       HXF_HIP(argmax_launch(logits, samp, R, m_.vocab, st_));
       HXF_HIP(hipMemcpyAsync(host_sampled_, samp, (size_t)R * 4, hipMemcpyDeviceToHost, st_));
@@ -565,6 +599,22 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
       (void)hipEventDestroy(ev_merge_[i + 1]);
     }
     ev_merge_.clear();
+    for (const ProfEv& pe : prof_ev_) {
+      float ms = 0.f;
+      HXF_HIP(hipEventElapsedTime(&ms, pe.e0, pe.e1));
+      if (pe.kind < 5) {
+        prof.gemm_launches[pe.kind] += 1;
+        prof.gemm_flops[pe.kind] += pe.flops;
+        prof.gemm_ms[pe.kind] += ms;
+      } else {
+        prof.prefill_attn_launches += 1;
+        prof.prefill_attn_flops += pe.flops;
+        prof.prefill_attn_ms += ms;
+      }
+      (void)hipEventDestroy(pe.e0);
+      (void)hipEventDestroy(pe.e1);
+    }
+    prof_ev_.clear();
   }
   sampled.assign(host_sampled_, host_sampled_ + R);
   return HXF_OK;

@@ -33,6 +33,12 @@ struct Profile {
   int64_t decode_attn_launches = 0;
   int64_t decode_attn_bytes = 0; // algorithmic KV bytes read by those launches
   double decode_merge_ms = 0;    // log-sum-exp merge kernel time of the same iterations
+  int64_t gemm_launches[5] = {};  // by projection: QKV, O, gate/up, down, LM head
+  double gemm_flops[5] = {};      // 2*M*N*K
+  double gemm_ms[5] = {};
+  int64_t prefill_attn_launches = 0;
+  double prefill_attn_flops = 0;  // 4*dh per (query, key, q-head) pair inside the causal mask
+  double prefill_attn_ms = 0;
 };
 
 std::unique_ptr<Executor> make_hip_executor(const hxf_model_cfg& m, const hxf_sched_cfg& s,

@@ -541,12 +541,16 @@ hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent
   return hipErrorInvalidValue;
 }
 
-hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st) {
+hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (a.n_items <= 0) return hipSuccess;
-  if (a.dh == 128) hipLaunchKernelGGL((prefill_flash_kernel<128, kPrefillPT>), dim3(a.n_items), dim3(256), 0, st, a);
-  else if (a.dh == 64) hipLaunchKernelGGL((prefill_flash_kernel<64, kPrefillPT>), dim3(a.n_items), dim3(256), 0, st, a);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
+  auto go = [&](auto kernel) {
+    if (ev_start || ev_stop) hipExtLaunchKernelGGL(kernel, dim3(a.n_items), dim3(256), 0, st, ev_start, ev_stop, 0, a);
+    else hipLaunchKernelGGL(kernel, dim3(a.n_items), dim3(256), 0, st, a);
+    return hipGetLastError();
+  };
+  if (a.dh == 128) return go(prefill_flash_kernel<128, kPrefillPT>);
+  if (a.dh == 64) return go(prefill_flash_kernel<64, kPrefillPT>);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace hxf

@@ -9,6 +9,8 @@
 //                by LDS DMA, four or eight wavefronts, tile shape chosen per GEMM.
 // Workgroups are renumbered so that consecutive output tiles (which share a
 // weight slice) land on the same XCD and its L2.
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 #include <utility>
 
@@ -50,6 +52,14 @@ __device__ __forceinline__ int xcd_remap(int i, int nb) {
   const int xcd = i & 7, local = i >> 3;
   const int per = nb >> 3, rem = nb & 7;
   return (xcd < rem) ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
+}
+
+// Launch; with events, the kernel itself records its start (e0) and end (e1).
+template <typename K, typename... Args>
+hipError_t launch_ev(K kernel, dim3 grid, dim3 block, hipStream_t st, hipEvent_t e0, hipEvent_t e1, Args... args) {
+  if (e0 || e1) hipExtLaunchKernelGGL(kernel, grid, block, 0, st, e0, e1, 0, args...);
+  else hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+  return hipGetLastError();
 }
 
 template <int BM, int BN, int BK, int NS, int EPI, bool SPLIT>
@@ -389,18 +399,18 @@ __global__ __launch_bounds__(64 * ST_WV) void gemm_stream_kernel(GemmArgs a) {
 }
 
 template <int MT, int EPI>
-hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st, bool reduce) {
+hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st, bool reduce, hipEvent_t e0, hipEvent_t e1) {
   const int nb = (a.N + ST_WV * ST_NTW * 16 - 1) / (ST_WV * ST_NTW * 16);
   if (S > 1) {
-    hipLaunchKernelGGL((gemm_stream_kernel<MT, EPI, true>), dim3(nb, S), dim3(64 * ST_WV), 0, st, a);
-    if (!reduce) return hipGetLastError();
+    if (hipError_t e = launch_ev(gemm_stream_kernel<MT, EPI, true>, dim3(nb, S), dim3(64 * ST_WV), st, e0,
+                                 reduce ? nullptr : e1, a))
+      return e;
+    if (!reduce) return hipSuccess;
     const int n_out = (EPI == EPI_SWIGLU) ? a.N / 2 : a.N;
     const size_t tot = (size_t)a.M * n_out;
-    hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((tot + 255) / 256), dim3(256), 0, st, a, S);
-  } else {
-    hipLaunchKernelGGL((gemm_stream_kernel<MT, EPI, false>), dim3(nb, 1), dim3(64 * ST_WV), 0, st, a);
+    return launch_ev(splitk_reduce_kernel<EPI>, dim3((tot + 255) / 256), dim3(256), st, nullptr, e1, a, S);
   }
-  return hipGetLastError();
+  return launch_ev(gemm_stream_kernel<MT, EPI, false>, dim3(nb, 1), dim3(64 * ST_WV), st, e0, e1, a);
 }
 
 // Prefill-sized M: BM x BN macro tiles on the 32x32x16 bf16 MFMA, fed by the
@@ -617,60 +627,57 @@ constexpr BigCfg kBig[] = {
 constexpr int kNumBig = sizeof(kBig) / sizeof(kBig[0]);
 
 template <int BM, int BN, int WM, int WN, int EPI>
-hipError_t launch_big(const GemmArgs& a, hipStream_t st) {
+hipError_t launch_big(const GemmArgs& a, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   constexpr int STAGE_BYTES = (BM + BN) * 64;
   constexpr int NSTG = std::min(5, 160 * 1024 / STAGE_BYTES);
   const int nb = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_big_kernel<BM, BN, WM, WN, NSTG, EPI>), dim3(nb), dim3(64 * WM * WN), 0, st, a);
-  return hipGetLastError();
+  return launch_ev(gemm_big_kernel<BM, BN, WM, WN, NSTG, EPI>, dim3(nb), dim3(64 * WM * WN), st, e0, e1, a);
 }
 
 template <int EPI>
-hipError_t launch_big_cfg(const GemmArgs& a, int cfg, hipStream_t st) {
+hipError_t launch_big_cfg(const GemmArgs& a, int cfg, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   switch (cfg) {
-    case 0: return launch_big<256, 256, 4, 2, EPI>(a, st);
-    case 2: return launch_big<192, 256, 2, 4, EPI>(a, st);
-    case 4: return launch_big<128, 256, 2, 4, EPI>(a, st);
-    case 5: return launch_big<128, 128, 2, 2, EPI>(a, st);
+    case 0: return launch_big<256, 256, 4, 2, EPI>(a, st, e0, e1);
+    case 2: return launch_big<192, 256, 2, 4, EPI>(a, st, e0, e1);
+    case 4: return launch_big<128, 256, 2, 4, EPI>(a, st, e0, e1);
+    case 5: return launch_big<128, 128, 2, 2, EPI>(a, st, e0, e1);
     default: break;
   }
   if constexpr (EPI != EPI_SWIGLU) {
-    if (cfg == 1) return launch_big<224, 256, 1, 8, EPI>(a, st);
-    if (cfg == 3) return launch_big<160, 256, 1, 8, EPI>(a, st);
+    if (cfg == 1) return launch_big<224, 256, 1, 8, EPI>(a, st, e0, e1);
+    if (cfg == 3) return launch_big<160, 256, 1, 8, EPI>(a, st, e0, e1);
   }
   return hipErrorInvalidValue;
 }
 
 template <int BM, int BN, int BK, int NS, int EPI>
-hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st, bool reduce = true) {
+hipError_t launch_tile(const GemmArgs& a, int S, hipStream_t st, bool reduce, hipEvent_t e0, hipEvent_t e1) {
   const int nb = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  if (S <= 1) {
-    hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, BK, NS, EPI, false>), dim3(nb), dim3(256), 0, st, a);
-  } else {
-    hipLaunchKernelGGL((gemm_nt_kernel<BM, BN, BK, NS, EPI, true>), dim3(nb, 1, S), dim3(256), 0, st, a);
-    if (!reduce) return hipGetLastError();
-    const int n_out = (EPI == EPI_SWIGLU) ? a.N / 2 : a.N;
-    const size_t tot = (size_t)a.M * n_out;
-    hipLaunchKernelGGL((splitk_reduce_kernel<EPI>), dim3((tot + 255) / 256), dim3(256), 0, st, a, S);
-  }
-  return hipGetLastError();
+  if (S <= 1) return launch_ev(gemm_nt_kernel<BM, BN, BK, NS, EPI, false>, dim3(nb), dim3(256), st, e0, e1, a);
+  if (hipError_t e = launch_ev(gemm_nt_kernel<BM, BN, BK, NS, EPI, true>, dim3(nb, 1, S), dim3(256), st, e0,
+                               reduce ? nullptr : e1, a))
+    return e;
+  if (!reduce) return hipSuccess;
+  const int n_out = (EPI == EPI_SWIGLU) ? a.N / 2 : a.N;
+  const size_t tot = (size_t)a.M * n_out;
+  return launch_ev(splitk_reduce_kernel<EPI>, dim3((tot + 255) / 256), dim3(256), st, nullptr, e1, a, S);
 }
 
 template <int EPI>
-hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st, bool reduce) {
+hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st, bool reduce, hipEvent_t e0, hipEvent_t e1) {
   a.k_chunk = p.k_chunk;
   if (p.stream) {
-    if (p.bm <= 32) return launch_stream<2, EPI>(a, p.splits, st, reduce);
-    if (p.bm <= 64) return launch_stream<4, EPI>(a, p.splits, st, reduce);
-    if (p.bm <= 128) return launch_stream<8, EPI>(a, p.splits, st, reduce);
-    return launch_stream<16, EPI>(a, p.splits, st, reduce);
+    if (p.bm <= 32) return launch_stream<2, EPI>(a, p.splits, st, reduce, e0, e1);
+    if (p.bm <= 64) return launch_stream<4, EPI>(a, p.splits, st, reduce, e0, e1);
+    if (p.bm <= 128) return launch_stream<8, EPI>(a, p.splits, st, reduce, e0, e1);
+    return launch_stream<16, EPI>(a, p.splits, st, reduce, e0, e1);
   }
   if (p.big) {
     // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0
-    if (EPI == EPI_SWIGLU && a.N % 64 != 0) return launch_tile<128, 128, 64, 2, EPI>(a, 1, st);
-    return launch_big_cfg<EPI>(a, p.cfg, st);
+    if (EPI == EPI_SWIGLU && a.N % 64 != 0) return launch_tile<128, 128, 64, 2, EPI>(a, 1, st, true, e0, e1);
+    return launch_big_cfg<EPI>(a, p.cfg, st, e0, e1);
   }
-  return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce);
+  return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce, e0, e1);
 }
 
 // One 16-byte chunk of the packed layout per thread: chunk q is tile q / 64 and,
@@ -744,12 +751,13 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu) {
   return p;
 }
 
-hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st, bool reduce) {
+hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st, bool reduce, hipEvent_t e0,
+                       hipEvent_t e1) {
   switch (epi) {
-    case EPI_BF16: return launch_epi<EPI_BF16>(a, p, st, reduce);
-    case EPI_RESID: return launch_epi<EPI_RESID>(a, p, st, reduce);
-    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, p, st, reduce);
-    default: return launch_epi<EPI_F32>(a, p, st, reduce);
+    case EPI_BF16: return launch_epi<EPI_BF16>(a, p, st, reduce, e0, e1);
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, p, st, reduce, e0, e1);
+    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, p, st, reduce, e0, e1);
+    default: return launch_epi<EPI_F32>(a, p, st, reduce, e0, e1);
   }
 }
 

@@ -51,8 +51,10 @@ struct GemmPlan {
 // swiglu: the plan is for the SwiGLU epilogue (N = 2F logical columns)
 GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu = false);
 // With reduce == false a split-K plan leaves its fp32 partials [splits][M][N] in
-// a.partial for the consumer to sum (no reduction launch).
-hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st, bool reduce = true);
+// a.partial for the consumer to sum (no reduction launch).  e0 / e1 (may be null):
+// events recorded at the first kernel's start and the last kernel's end.
+hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st, bool reduce = true,
+                       hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // Weight packing: W bf16 [N, K] row-major -> tiles of 16 rows x 32 columns in MFMA
 // operand order, zero padded to ceil(N/16)*16 rows and ceil(K/32)*32 columns.
 size_t packed_weight_elems(int N, int K);
@@ -186,7 +188,8 @@ struct PrefillAttnArgs {
   int Hq, Hkv, dh;
   float scale_log2;
 };
-hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st);
+hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st, hipEvent_t ev_start = nullptr,
+                               hipEvent_t ev_stop = nullptr);
 // Queries covered by one prefill work item for a given GQA group size.
 int prefill_queries_per_item(int group);
 

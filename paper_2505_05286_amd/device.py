@@ -29,6 +29,8 @@ class DeviceModel:
     wq, wk, wv, wo, w_gate, w_up, w_down; ``embed``, ``lm_head`` and ``norm``
     are host bf16 bits.  Wq, Wk and Wv are stacked row-wise into one QKV matrix.
     Projection matrices and the LM head are held packed (hxf_op_pack_weight).
+    ``norm`` is one bf16 gain [d] used by every RMSNorm, or a dict with one gain
+    per norm: attn [L, d], ffn [L, d], final [d].
     """
 
     def __init__(self, shape, layer_fn, embed, lm_head, norm, device="cuda"):
@@ -36,7 +38,15 @@ class DeviceModel:
         self.device = device
         self.embed = _dev_u16(embed, device)
         self.lm_head = _dev_packed(lm_head, device)
-        self.norm = _dev_u16(norm, device)
+        L = shape.n_layers
+        if isinstance(norm, dict):
+            self.norm = _dev_u16(norm["final"], device)
+            self.attn_norm = [_dev_u16(norm["attn"][l], device) for l in range(L)]
+            self.ffn_norm = [_dev_u16(norm["ffn"][l], device) for l in range(L)]
+        else:
+            self.norm = _dev_u16(norm, device)
+            self.attn_norm = [self.norm] * L
+            self.ffn_norm = [self.norm] * L
         self.layers = []
         for l in range(shape.n_layers):
             w = layer_fn(l)
@@ -49,8 +59,8 @@ class DeviceModel:
         torch.cuda.current_stream(device).synchronize()
 
     def layer_ptrs(self):
-        n = self.norm.data_ptr()
-        return [{"attn_norm": n, "ffn_norm": n, **{k: t.data_ptr() for k, t in L.items()}} for L in self.layers]
+        return [{"attn_norm": a.data_ptr(), "ffn_norm": f.data_ptr(), **{k: t.data_ptr() for k, t in L.items()}}
+                for a, f, L in zip(self.attn_norm, self.ffn_norm, self.layers)]
 
 
 class Engine:

@@ -88,9 +88,15 @@ class RequestState(C.Structure):
                 ("t_submit_us", C.c_int64)]
 
 
+PROF_GEMMS = ("qkv", "o", "gate_up", "down", "lm_head")
+
+
 class Profile(C.Structure):
     _fields_ = [("decode_attn_launches", C.c_int64), ("decode_attn_bytes", C.c_int64),
-                ("decode_attn_ms", C.c_double), ("decode_merge_ms", C.c_double)]
+                ("decode_attn_ms", C.c_double), ("decode_merge_ms", C.c_double),
+                ("gemm_launches", C.c_int64 * 5), ("gemm_flops", C.c_double * 5), ("gemm_ms", C.c_double * 5),
+                ("prefill_attn_launches", C.c_int64), ("prefill_attn_flops", C.c_double),
+                ("prefill_attn_ms", C.c_double)]
 
 
 _lib = None
@@ -348,7 +354,11 @@ class Instance:
     def profile(self):
         p = Profile()
         self._check(self.L.hxf_profile_get(self.h, C.byref(p)), "hxf_profile_get")
-        return {k: getattr(p, k) for k, _ in p._fields_}
+        out = {}
+        for k, _ in p._fields_:
+            v = getattr(p, k)
+            out[k] = dict(zip(PROF_GEMMS, list(v))) if k.startswith("gemm_") else v
+        return out
 
 
 # ------------------------------------------------------------------ ops

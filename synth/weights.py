@@ -96,3 +96,19 @@ def gen_lm_head(shape, seed=None):
 def norm_weight(shape):
     """RMSNorm gain: all ones, as bf16 bits."""
     return np.full(shape.d_model, BF16_ONE, dtype=np.uint16)
+
+
+NORM_STREAM = 7_000_001
+
+
+def gen_norm_gains(shape, seed=None, spread=0.5):
+    """Distinct RMSNorm gains for every norm, for tests that must tell the norms
+    apart (the workloads themselves use all-ones gains).  Each element is
+    1 + spread * U(-1, 1), rounded to bf16; one stream per seed.
+    Returns a dict of bf16 bits: attn [L, d], ffn [L, d], final [d]."""
+    seed = shape.weight_seed if seed is None else seed
+    rng = np.random.default_rng(np.random.SeedSequence([seed, NORM_STREAM]))
+    L, d = shape.n_layers, shape.d_model
+    g = 1.0 + spread * rng.uniform(-1.0, 1.0, (2 * L + 1, d)).astype(np.float32)
+    bits = f32_to_bf16_bits(g.astype(np.float32)).reshape(2 * L + 1, d)
+    return {"attn": bits[:L].copy(), "ffn": bits[L:2 * L].copy(), "final": bits[2 * L].copy()}

@@ -35,9 +35,10 @@ def device_model(name, n_layers=None):
         _models.clear()
         shape = synth.model_shape(name, n_layers)
         log(f"uploading {shape.name}")
+        gains = synth.gen_norm_gains(shape)       # a distinct gain per norm: miswired norms fail
         _models[key] = (shape, DeviceModel(shape, lambda l: synth.gen_layer(shape, l), synth.gen_embed(shape),
-                                           synth.gen_lm_head(shape), synth.norm_weight(shape), device="cuda:0"),
-                        M.Weights(shape))
+                                           synth.gen_lm_head(shape), gains, device="cuda:0"),
+                        M.Weights(shape, norm_gains=gains))
     return _models[key]
 
 

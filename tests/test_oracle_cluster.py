@@ -228,6 +228,28 @@ def test_tuning_prefers_the_fast_instance_when_the_other_is_much_slower():
     assert all(v > min(vals) for v in vals[:grid.index(best)])
 
 
+def test_beta_from_two_warmup_queries_by_hand():
+    """beta = C_ref * Q_ref (Section 4.1) over warm-up dispatches at alpha = 0
+    (reading: means over the decisions of the instances' mean t_comp and mean
+    t_queue).  Two instances with t_comp = L_in and 2 L_in microseconds, 1 ms
+    iterations, two one-request queries:
+      t = 0:  L_in 100 -> costs (100, 200), queues (0, 0): decision (150, 0); tie -> instance 0
+      t = 10: L_in  50 -> costs (50, 100), instance 0 still runs the first (queue 100):
+              decision (75, 50); 1/100 < 1/1 -> instance 1
+    C_ref = (150 + 75) / 2 = 112.5, Q_ref = (0 + 50) / 2 = 25, beta = 2812.5."""
+    it = (1000 * S.PS, 0, 0, 0)
+    specs = [spec((0, S.PS, 0, 0), it), spec((0, 2 * S.PS, 0, 0), it)]
+    wfs = [_wf(0, 0, 10 ** 7, [[_req(100, 1)]], [(100, 1)]),
+           _wf(1, 10, 10 ** 7, [[_req(50, 1, seed=1)]], [(50, 1)])]
+    assert K.beta_from_warmup(specs, wfs) == 2812.5
+    co = K.Coordinator(specs, "wb", 0.0, 1.0, record=True)
+    co.simulate(wfs)
+    assert co.decisions == [(150.0, 0.0), (75.0, 50.0)]
+    assert [p[4] for p in co.placements] == [0, 1]
+    # with the queue mean below 1 us it counts as 1: one query alone gives C_ref * 1
+    assert K.beta_from_warmup(specs, wfs[:1]) == 150.0
+
+
 def test_tuning_is_indifferent_with_one_instance():
     trace = [_two_stage(w, 3_000 * w) for w in range(8)]
     best, vals = K.grid_search([spec(COST)], trace, 1e6, tuple(k / 10 for k in range(11)))

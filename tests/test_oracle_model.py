@@ -170,6 +170,71 @@ def test_uniform_attention_closed_form():
         np.testing.assert_allclose(lg[i], expect, rtol=1e-12, atol=1e-14)
 
 
+def test_ffn_closed_form_with_distinct_norm_gains():
+    """Pins the FFN half of a layer and which gain each RMSNorm uses.  Wq = Wk = 0
+    (uniform causal attention), Wv and Wo permutations, W_gate and W_up scaled
+    row selections (a * e_sel_g[f], b * e_sel_u[f]), W_down a row selection
+    (e_sel_d[j]), an identity LM head and a different random gain for the
+    attention, FFN and final norms.  Position i then has the closed form
+        y = x_i + (mean_{t<=i} n(x_t, g_a)[perm_v])[perm_o]
+        u = n(y, g_f)
+        z = y + (silu(a u[sel_g]) * (b u[sel_u]))[sel_d]
+        logits_i = n(z, g_out),   n(v, g) = v / sqrt(mean(v^2) + eps) * g,
+    which a slip such as SiLU on the up projection, the FFN norm fed the layer
+    input, a swapped gain or the second residual added to u instead of y breaks."""
+    d, F = 32, 48
+    sh = synth.ModelShape("ffn", 1, d, 2, 2, 16, F, d, weight_seed=0)
+    gains = synth.gen_norm_gains(sh, seed=3)
+    w = M.Weights(sh, norm_gains=gains)
+    rng = np.random.default_rng(17)
+    perm_v, perm_o = rng.permutation(d), rng.permutation(d)
+    sel_g, sel_u = rng.integers(0, d, F), rng.integers(0, d, F)
+    sel_d = rng.permutation(F)[:d]
+    a, b = 1.5, -0.75
+    lay = {k: np.zeros_like(v) for k, v in w.layer(0).items()}
+    lay["wv"][np.arange(d), perm_v] = 1.0
+    lay["wo"][np.arange(d), perm_o] = 1.0
+    lay["w_gate"][np.arange(F), sel_g] = a
+    lay["w_up"][np.arange(F), sel_u] = b
+    lay["w_down"][np.arange(d), sel_d] = 1.0
+    w._layers[0] = lay
+    w._lm = np.eye(d, dtype=np.float32)
+    g_a, g_f, g_o = (synth.bf16_bits_to_f32(x).astype(np.float64)
+                     for x in (gains["attn"][0], gains["ffn"][0], gains["final"]))
+    assert not np.allclose(g_a, g_f) and not np.allclose(g_f, g_o)
+    ids = np.array([5, 11, 30, 2, 19, 7])
+    x = w.embed_rows(ids)
+    eps = sh.rms_eps
+
+    def n(v, g):
+        return v / math.sqrt(float(np.mean(v * v)) + eps) * g
+
+    lg = M.forward(w, [M.Sequence(1)], [ids], logit_rows=[list(range(len(ids)))])[0]
+    for i in range(len(ids)):
+        att = np.mean([n(x[t], g_a) for t in range(i + 1)], axis=0)[perm_v][perm_o]
+        y = x[i] + att
+        u = n(y, g_f)
+        gate, up = a * u[sel_g], b * u[sel_u]
+        f = gate / (1.0 + np.exp(-gate)) * up
+        z = y + f[sel_d]
+        np.testing.assert_allclose(lg[i], n(z, g_o), rtol=1e-12, atol=1e-14)
+
+
+def test_fork_copies_the_parents_kv_prefix(tiny):
+    """A forked sequence continued from the parent's first n tokens of KV gives the
+    logits of processing its whole context at once."""
+    rng = np.random.default_rng(23)
+    ctx = rng.integers(0, 2048, 57)
+    app = rng.integers(0, 2048, 6)
+    par = M.Sequence(2)
+    M.forward(tiny, [par], [ctx])
+    kid = par.fork(48)
+    got = M.forward(tiny, [kid], [np.concatenate([ctx[48:], app])])[0]
+    ref = M.forward(tiny, [M.Sequence(2)], [np.concatenate([ctx, app])])[0]
+    np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-10)
+    assert par.n == 57 and kid.n == 63
+
+
 def test_causal_mask_future_tokens_do_not_matter(tiny):
     rng = np.random.default_rng(8)
     ids = rng.integers(0, 2048, 40)

@@ -115,6 +115,58 @@ def test_single_instance_average_cost_is_own_cost():
     assert S.t_comp((7 * S.PS, 3 * S.PS, 0, 5 * S.PS), 10, 4) == 7 + 30 + 20
 
 
+def test_t_comp_hand_values_with_quadratic_term():
+    """Section 4.1's t_comp = t_prefill(L_in) + t_decode(L_out) with the quadratic
+    prefill term, worked by hand (picosecond coefficients, floored microseconds)."""
+    cost = (1_500_000, 2_000_000, 300, 4_000_000)
+    # 1.5e6 + 2e6*1000 + 300*1000^2 + 4e6*10 = 2_341_500_000 ps = 2341.5 us -> 2341
+    assert S.t_comp(cost, 1000, 10) == 2341
+    # quadratic term alone: 806 * 8192^2 = 54_089_744_384 ps -> 54089 us
+    assert S.t_comp((0, 0, 806, 0), 8192, 0) == 54089
+    # 234 * 3000^2 + 17 * 1e6 * 256 = 2_106_000_000 + 4_352_000_000 = 6_458_000_000 ps -> 6458 us
+    assert S.t_comp((0, 0, 234, 17_000_000), 3000, 256) == 6458
+    # one picosecond short of a whole microsecond floors down: 999_999 + 1 * 1^2 ... = 999_999 + 0
+    assert S.t_comp((999_998, 0, 1, 0), 1, 0) == 0
+    assert S.t_comp((999_999, 0, 1, 0), 1, 0) == 1
+    # the same costs through a scheduler's submit
+    s = S.Scheduler(4096, 8, 2048, cost, ITER)
+    rid = s.submit(0, 0, 0, 0, 10 ** 7, [1] * 1000, 10)
+    assert s.reqs[rid].t_comp == 2341
+
+
+def test_llf_key_and_order_differ_from_pq_by_hand():
+    """LLF (Section 5.1's least-laxity baseline, reading: key = workflow arrival +
+    end-to-end SLO - (own cost + the later stages' costs)) against PQ (key =
+    enqueue + budget - own cost), three requests submitted at t = 0 with
+    t_comp = L_in microseconds:
+        A: arrival    0, SLO 1000, L_in 100, later stage L_in 400
+           LLF 0 + 1000 - 500 = 500;   PQ budget 1000*100/500 = 200, key 200 - 100 = 100
+        B: arrival    0, SLO  610, L_in 300, no later stage
+           LLF 610 - 300 = 310;        PQ budget 610, key 610 - 300 = 310
+        C: arrival -150, SLO  900, L_in 200, later stage L_in 100
+           LLF -150 + 900 - 300 = 450; PQ budget (900-150)*200/300 = 500, key 300
+    PQ order A, C, B; LLF order B, C, A.  Leaving out the later stages' costs in
+    LLF would give B (310), C (550), A (900) -> still B first but C keyed 550;
+    using the enqueue time instead of the workflow arrival would key C at 600,
+    after A."""
+    keys = {}
+    for pol in (S.POLICY_PQ, S.POLICY_LLF):
+        s = S.Scheduler(64, 1, 4096, UNIT_PREFILL, ITER, policy=pol)
+        a = s.submit(0, 1, 0, 0, 1000, [1] * 100, 1, rest=[(400, 1)])
+        b = s.submit(0, 2, 0, 0, 610, [1] * 300, 1)
+        c = s.submit(0, 3, 0, -150, 900, [1] * 200, 1, rest=[(100, 1)])
+        keys[pol] = [s.reqs[r].key for r in (a, b, c)]
+        order = s.queue_order()
+        if pol == S.POLICY_PQ:
+            assert order == [a, c, b]
+        else:
+            assert order == [b, c, a]
+        st, info = s.step(0)
+        assert info["admitted"] == [order[0]]
+    assert keys[S.POLICY_PQ] == [100, 310, 300]
+    assert keys[S.POLICY_LLF] == [500, 310, 450]
+
+
 def test_urgency_is_negative_laxity_and_static_key():
     s = S.Scheduler(64, 8, 512, (0, 2 * S.PS, 0, 3 * S.PS), ITER)
     rid = s.submit(1000, 0, 0, 0, 50_000, list(range(40)), 5, rest=[(100, 10)])
