@@ -185,13 +185,14 @@ class Sequence:
             self.v[layer] = np.concatenate([self.v[layer], v])
 
 
-def forward(weights, seqs, chunks, logit_rows=None):
+def forward(weights, seqs, chunks, logit_rows=None, progress=None):
     """Run one forward pass over several independent sequences.
 
     seqs: list of Sequence; chunks: list of int arrays of new token ids (one per
     sequence), placed at positions seq.n .. seq.n + len - 1.  Appends their KV.
     logit_rows: per sequence, the local row indices whose logits are wanted
-    (default: the last row).  Returns a list of float64 logit arrays.
+    (default: the last row).  progress(layer), if given, is called after each
+    layer (long runs report liveness).  Returns a list of float64 logit arrays.
     """
     sh = weights.shape
     dh, hq, hkv = sh.head_dim, sh.n_q_heads, sh.n_kv_heads
@@ -216,6 +217,8 @@ def forward(weights, seqs, chunks, logit_rows=None):
         x = x + att.reshape(-1, hq * dh) @ w["wo"].T
         h = rmsnorm(x, weights.ffn_norm[l], sh.rms_eps)
         x = x + (silu(h @ w["w_gate"].T) * (h @ w["w_up"].T)) @ w["w_down"].T
+        if progress is not None:
+            progress(l)
     for s, c in zip(seqs, chunks):
         s.n += len(c)
     rows = []

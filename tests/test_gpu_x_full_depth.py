@@ -65,6 +65,12 @@ def load(name):
     return shape, dm, gains, bits, embed, lm
 
 
+def tick(layer):
+    """Oracle progress: a line every 8 layers, so a long float64 pass shows it is alive."""
+    if layer % 8 == 7:
+        log(f"  oracle layer {layer + 1}")
+
+
 def compare_rows(name, gpu_tok, gpu_rows, ref_rows):
     """Logits of every row within TOL; ids equal or near ties.  Returns (worst, ties)."""
     assert len(gpu_rows) == len(ref_rows), (name, len(gpu_rows), len(ref_rows))
@@ -132,7 +138,8 @@ def ref8b(m8b):
     par = M.Sequence(shape.n_layers)
     prompts = [cfg2[i].prompt.astype(np.int64) for i in s2] + [prompts3[p3].prompt.astype(np.int64), parent]
     log(f"full depth oracle pass 1: prefill of {sum(len(p) for p in prompts)} tokens")
-    out = M.forward(w, seq2 + [seq3, par], prompts, logit_rows=[[len(p) - 1] for p in prompts[:3]] + [[]])
+    out = M.forward(w, seq2 + [seq3, par], prompts, logit_rows=[[len(p) - 1] for p in prompts[:3]] + [[]],
+                    progress=tick)
     lg2 = [[o[0]] for o in out[:2]]
     tok2 = [[int(np.argmax(o[0]))] for o in out[:2]]
     lg3 = out[2][0]
@@ -141,7 +148,7 @@ def ref8b(m8b):
     lg4, tok4 = [[] for _ in APPEND4], [[] for _ in APPEND4]
     log(f"full depth oracle pass 2 after {time.time() - t0:.0f} s")
     chunks = [np.array([t[-1]]) for t in tok2] + [np.concatenate([parent[shared:], a]) for a in apps]
-    out = M.forward(w, seq2 + forks, chunks)
+    out = M.forward(w, seq2 + forks, chunks, progress=tick)
     for k in range(2):
         lg2[k].append(out[k][0])
         tok2[k].append(int(np.argmax(out[k][0])))
@@ -150,7 +157,7 @@ def ref8b(m8b):
         tok4[b].append(int(np.argmax(out[2 + b][0])))
     log(f"full depth oracle pass 3 after {time.time() - t0:.0f} s")
     chunks = [np.array([t[-1]]) for t in tok2] + [np.array([t[-1]]) for t in tok4]
-    out = M.forward(w, seq2 + forks, chunks)
+    out = M.forward(w, seq2 + forks, chunks, progress=tick)
     for k in range(2):
         lg2[k].append(out[k][0])
         tok2[k].append(int(np.argmax(out[k][0])))

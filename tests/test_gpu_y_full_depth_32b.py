@@ -18,7 +18,7 @@ from paper_2505_05286_amd import hxf
 from paper_2505_05286_amd.device import Engine
 
 from .gpu_util import log
-from .test_gpu_x_full_depth import COST, ITER, collect, compare_rows, load
+from .test_gpu_x_full_depth import COST, ITER, collect, compare_rows, load, tick
 
 pytestmark = pytest.mark.gpu
 
@@ -38,18 +38,18 @@ def test_cfg5_full_depth_32b():
     t0 = time.time()
     par = M.Sequence(shape.n_layers)
     lgp, tokp = [], []
-    out = M.forward(w, [par], [prompt])[0][0]
+    out = M.forward(w, [par], [prompt], progress=tick)[0][0]
     lgp.append(out)
     tokp.append(int(np.argmax(out)))
     log(f"cfg5 32B oracle: prompt pass {time.time() - t0:.0f} s")
-    out = M.forward(w, [par], [np.array([tokp[0]])])[0][0]
+    out = M.forward(w, [par], [np.array([tokp[0]])], progress=tick)[0][0]
     lgp.append(out)
     tokp.append(int(np.argmax(out)))
     S_ = np.concatenate([prompt, tokp])
     n = len(S_)
     shared = (n - 1) // 16 * 16
     forks = [par.fork(shared) for _ in apps]
-    outs = M.forward(w, forks, [np.concatenate([S_[shared:], a]) for a in apps])
+    outs = M.forward(w, forks, [np.concatenate([S_[shared:], a]) for a in apps], progress=tick)
     lgf = [[o[0]] for o in outs]
     tokf = [[int(np.argmax(o[0]))] for o in outs]
     log(f"cfg5 32B oracle done in {time.time() - t0:.0f} s")
