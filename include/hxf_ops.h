@@ -47,6 +47,20 @@ int64_t hxf_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
 int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void* C, int32_t ldc, int32_t M, int32_t N,
                 int32_t K, int32_t epilogue, void* workspace, int64_t workspace_bytes, void* stream);
 
+/* hxf_op_gemm without a workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid it).
+ * Same arguments and result as hxf_op_gemm; the split-K partials go to a device
+ * array of HXF_GEMM_NOALLOC_MAX_BYTES that the library holds on each GPU it runs on
+ * until the process ends (its address is looked up on the first call on a device,
+ * which must be the current device).  Nothing is allocated.  HXF_ENOMEM (nothing
+ * enqueued) when the plan's partials, splits * M * N * 4 bytes, exceed that size:
+ * every plan with M <= 128 fits.  Calls on one GPU share the array: calls that
+ * overlap on one GPU (several streams, several threads) race and must be serialised
+ * by the caller. */
+#define HXF_GEMM_NOALLOC_MAX_BYTES (16LL << 20)
+int hxf_op_gemm_noalloc(const void* A, int32_t lda, const void* B, const void* B2, void* C, int32_t ldc, int32_t M,
+                        int32_t N, int32_t K, int32_t epilogue, void* stream);
+
 /* Packed weight layout, used for every GEMM weight: W [N,K] bf16 row-major becomes
  * tiles of 16 rows x 32 columns (1 KB), row-tiles outermost, zero padded to
  * ceil(N/16)*16 rows and ceil(K/32)*32 columns; inside a tile the 8-element chunks

@@ -22,6 +22,7 @@ SOURCES = [
     "coord.cpp",
     "api.cpp",
     "ops.cpp",
+    "noalloc.hip",
     "executor.hip",
     "kernels/gemm.hip",
     "kernels/norm.hip",

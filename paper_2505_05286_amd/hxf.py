@@ -139,6 +139,8 @@ _SIGS = {
     "hxf_op_pack_weight": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]),
     "hxf_op_gemm": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32,
                               C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p]),
+    "hxf_op_gemm_noalloc": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                      C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_void_p]),
     "hxf_op_rmsnorm": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_float,
                                  C.c_void_p]),
     "hxf_op_embed_rmsnorm": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
@@ -398,6 +400,15 @@ def op_gemm_workspace_bytes(M, N, K):
 def op_gemm(A, lda, B, B2, Cp, ldc, M, N, K, epi, ws=0, ws_bytes=0, stream=0):
     _op(lib().hxf_op_gemm(A, lda, B, B2 or None, Cp, ldc, M, N, K, epi, ws or None, ws_bytes, stream or None),
         "hxf_op_gemm")
+
+
+GEMM_NOALLOC_MAX_BYTES = 16 << 20
+
+
+def op_gemm_noalloc(A, lda, B, B2, Cp, ldc, M, N, K, epi, stream=0):
+    """hxf_op_gemm with its split-K partials in the library's own device array."""
+    _op(lib().hxf_op_gemm_noalloc(A, lda, B, B2 or None, Cp, ldc, M, N, K, epi, stream or None),
+        "hxf_op_gemm_noalloc")
 
 
 def packed_weight_bytes(N, K):
