@@ -970,6 +970,15 @@ def main():
                                         "achieved": round(achieved, 1),
                                         "frac": round(achieved / HBM_PEAK_GBS, 4)}},
     }
+    # weight-streaming GEMMs of the same profiled steps: weight bytes per launch / duration
+    wbytes = {"qkv": shape.qkv_dim * shape.d_model, "o": shape.d_model * shape.q_dim,
+              "gate_up": 2 * shape.ffn_dim * shape.d_model, "down": shape.d_model * shape.ffn_dim,
+              "lm_head": shape.vocab * shape.d_model}
+    out["decode_gemms"] = {}
+    for k, nbytes in wbytes.items():
+        n = max(prof["gemm_launches"][k], 1)
+        us = prof["gemm_ms"][k] / n * 1e3
+        out["decode_gemms"][k] = {"avg_us": round(us, 2), "weight_tb_s": round(2 * nbytes / (us * 1e-6) / 1e12, 3)}
     out["hbm_copy_probe"] = hbm_copy_probe()
     del eng, inst
     if not args.no_gemm_roofline:

@@ -113,8 +113,10 @@ typedef struct hxf_stage_req {
   const hxf_stage_shape* rest;  /* host; later stages of the workflow (budget denominator) */
   int32_t n_rest;
   int32_t n_forced;             /* 0, or max_new_tokens: teacher forcing */
-  const int32_t* forced_ids;    /* host; token fed back after generated token k (k < n_forced);
-                                   the sampled argmax is still what hxf_completion_tokens returns */
+  const int32_t* forced_ids;    /* host; token fed back after generated token k (k < n_forced):
+                                   the request's sequence holds the forced tokens (a fork of it
+                                   continues from them); the sampled argmax is still what
+                                   hxf_completion_tokens returns */
 } hxf_stage_req;
 
 /* Device pointers of one decoder layer.  Every matrix is bf16, row-major

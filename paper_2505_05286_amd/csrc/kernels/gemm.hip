@@ -255,64 +255,96 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int S) {
 
 // Decode-sized M (at most 16 * MT rows): a weight-streaming kernel fed by the
 // LDS DMA path (global_load_lds, 16 bytes per lane, no registers).  Each of
-// the WV wavefronts owns NTW 16-column tiles; a stage holds 64 K-elements of
-// the A rows (MT x 2 MFMA blocks, loaded by all wavefronts together) and of
-// each wavefront's weight tiles (NTW x 2 blocks), each block 1 KB laid out in
+// the WV wavefronts owns NTW 16-column tiles; a stage holds 32*KB K-elements of
+// the A rows (MT x KB MFMA blocks, loaded by all wavefronts together) and of
+// each wavefront's weight tiles (NTW x KB blocks), each block 1 KB laid out in
 // MFMA operand order.  NSTG stages are in flight: a wavefront waits for its
 // own DMAs of the oldest stage (vmcnt), one barrier makes everybody's visible
 // and frees the slot consumed one step earlier, which is refilled before the
 // multiplies.  Stages live in distinct LDS arrays and the loop is unrolled by
 // NSTG so the compiler can see that the LDS reads of a stage do not alias the
 // DMAs in flight (otherwise it waits for all of them).  Split K (grid.y)
-// writes fp32 partials; a reduction kernel finishes them.
-constexpr int ST_WV = 4, ST_NTW = 2, ST_NSTG = 3;   // 4 wavefronts x 2 tiles = 128 columns per workgroup
+// writes fp32 partials; a reduction kernel (or the consumer) finishes them.
+#ifndef HXF_ST_WV
+#define HXF_ST_WV 4
+#endif
+#ifndef HXF_ST_NTW
+#define HXF_ST_NTW 2
+#endif
+#ifndef HXF_ST_KB
+#define HXF_ST_KB 2
+#endif
+#ifndef HXF_ST_NSTG
+#define HXF_ST_NSTG 3
+#endif
+#ifndef HXF_ST_WG_PER_CU
+#define HXF_ST_WG_PER_CU 1
+#endif
+constexpr int ST_WV = HXF_ST_WV, ST_NTW = HXF_ST_NTW, ST_KB = HXF_ST_KB, ST_NSTG = HXF_ST_NSTG;
+constexpr int ST_COLS = ST_WV * ST_NTW * 16;          // output columns per workgroup
+constexpr int ST_KS = 32 * ST_KB;                     // K per stage
+
+// Stages of the streaming kernel with MT row tiles: as many as asked for that fit 160 KB
+// of LDS (wide row tiles may get fewer; below 2 the kernel is not used).
+template <int MT>
+constexpr int stream_stages() {
+  constexpr int bytes = (MT * ST_KB + ST_WV * ST_NTW * ST_KB) * 1024;
+  return ST_NSTG < 160 * 1024 / bytes ? ST_NSTG : 160 * 1024 / bytes;
+}
 
 template <int MT, int EPI, bool SPLIT>
 __global__ __launch_bounds__(64 * ST_WV) void gemm_stream_kernel(GemmArgs a) {
-  constexpr int WV = ST_WV, NTW = ST_NTW, NSTG = ST_NSTG;
-  constexpr int A_BLK = MT * 2, B_BLK_W = NTW * 2;
+  constexpr int WV = ST_WV, NTW = ST_NTW, KB = ST_KB, KS = ST_KS;
+  constexpr int A_BLK = MT * KB, B_BLK_W = NTW * KB;
   constexpr int STAGE = (A_BLK + WV * B_BLK_W) * 512;       // bf16 elements per stage
-  constexpr int A_PER_W = A_BLK / WV;                       // A blocks each wavefront moves
+  constexpr int NSTG = stream_stages<MT>();
+  constexpr int A_PER_W = (A_BLK + WV - 1) / WV;            // A blocks each wavefront moves (last one repeated)
   constexpr int PER_STAGE = A_PER_W + B_BLK_W;              // DMA instructions per wavefront per stage
   constexpr bool SW = (EPI == EPI_SWIGLU);
-  static_assert(A_BLK % WV == 0, "A blocks are split evenly over the wavefronts");
-  static_assert(NSTG == 3, "three stage arrays");
-  __shared__ __attribute__((aligned(1024))) bf16_t L0[STAGE], L1[STAGE], L2[STAGE];
+  static_assert(NSTG >= 2 && NSTG <= 6, "stage layout");
+  static_assert((NSTG - 2) * PER_STAGE < 64, "vmcnt range");
+  __shared__ __attribute__((aligned(1024))) bf16_t L0[STAGE], L1[STAGE], L2[NSTG > 2 ? STAGE : 8],
+      L3[NSTG > 3 ? STAGE : 8], L4[NSTG > 4 ? STAGE : 8], L5[NSTG > 5 ? STAGE : 8];
   auto slot = [&](auto ic) -> bf16_t* {
     constexpr int I = decltype(ic)::value;
-    if constexpr (I == 0) return L0; else if constexpr (I == 1) return L1; else return L2;
+    if constexpr (I == 0) return L0; else if constexpr (I == 1) return L1; else if constexpr (I == 2) return L2;
+    else if constexpr (I == 3) return L3; else if constexpr (I == 4) return L4; else return L5;
   };
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, g = lane >> 4;
   const int c0 = (blockIdx.x * WV + w) * NTW * 16;          // first logical column of this wavefront
   const int kb = blockIdx.y * a.k_chunk;
   const int ke = min(a.K, kb + a.k_chunk);
   const int kend = a.kt * 32;                               // packed K (zero padded past K)
-  const int nst = (ke - kb + 63) / 64;
+  const int nst = (ke - kb + KS - 1) / KS;
 
-  // weight tile sources (lane offset included); tiles past the end repeat the last one (dropped)
   // weight tile sources, lane offset included (tiles past the end repeat the last one; dropped)
   const bf16_t* bsrc[NTW];
 #pragma unroll
   for (int j = 0; j < NTW; ++j) bsrc[j] = b_row(a, min(c0 + j * 16, a.N - 1) & ~15, SW) + lane * 8;
-  // A block b = (row tile i, 32-column half kk): lane reads row 16i + r (rows past M repeat M-1)
+  // A block b = (row tile b / KB, 32-column block b % KB): lane reads row 16 (b / KB) + r
+  // (rows past M repeat M-1)
   const bf16_t* arow[A_PER_W];
+  int ablk[A_PER_W];
 #pragma unroll
-  for (int u = 0; u < A_PER_W; ++u) arow[u] = a.A + (size_t)min(((w * A_PER_W + u) >> 1) * 16 + r, a.M - 1) * a.lda;
+  for (int u = 0; u < A_PER_W; ++u) {
+    ablk[u] = min(w * A_PER_W + u, A_BLK - 1);
+    arow[u] = a.A + (size_t)min((ablk[u] / KB) * 16 + r, a.M - 1) * a.lda;
+  }
   auto issue = [&](int s, bf16_t* base) {
-    const int k0 = kb + min(s, nst - 1) * 64;               // past the last stage: reload it (never read)
+    const int k0 = kb + min(s, nst - 1) * KS;               // past the last stage: reload it (never read)
 #pragma unroll
     for (int u = 0; u < A_PER_W; ++u) {
-      const int kk = (w * A_PER_W + u) & 1;
+      const int kk = ablk[u] % KB;
       const int k = min(k0 + kk * 32 + g * 8, a.K - 8);      // stays in the row; the weights are zero past K
-      dma16(arow[u] + k, base + (w * A_PER_W + u) * 512);
+      dma16(arow[u] + k, base + ablk[u] * 512);
     }
 #pragma unroll
     for (int j = 0; j < NTW; ++j)
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
+      for (int kk = 0; kk < KB; ++kk) {
         const int t = min(k0 / 32 + kk, a.kt - 1);
-        dma16(bsrc[j] + (size_t)t * 512, base + (A_BLK + w * B_BLK_W + j * 2 + kk) * 512);
+        dma16(bsrc[j] + (size_t)t * 512, base + (A_BLK + w * B_BLK_W + j * KB + kk) * 512);
       }
   };
   f32x4 acc[MT][NTW];
@@ -321,17 +353,17 @@ __global__ __launch_bounds__(64 * ST_WV) void gemm_stream_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < NTW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto compute = [&](const bf16_t* base, int s) {
-    const int k0 = kb + s * 64;
+    const int k0 = kb + s * KS;
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+    for (int kk = 0; kk < KB; ++kk) {
       if (k0 + kk * 32 >= kend) break;                      // a 32-block wholly past the packed K
       bf16x8 fa[MT], fb[NTW];
 #pragma unroll
       for (int i = 0; i < MT; ++i)
-        fa[i] = as_bf16x8(*reinterpret_cast<const uint4*>(base + (i * 2 + kk) * 512 + lane * 8));
+        fa[i] = as_bf16x8(*reinterpret_cast<const uint4*>(base + (i * KB + kk) * 512 + lane * 8));
 #pragma unroll
       for (int j = 0; j < NTW; ++j)
-        fb[j] = as_bf16x8(*reinterpret_cast<const uint4*>(base + (A_BLK + w * B_BLK_W + j * 2 + kk) * 512 + lane * 8));
+        fb[j] = as_bf16x8(*reinterpret_cast<const uint4*>(base + (A_BLK + w * B_BLK_W + j * KB + kk) * 512 + lane * 8));
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -381,9 +413,14 @@ __global__ __launch_bounds__(64 * ST_WV) void gemm_stream_kernel(GemmArgs a) {
       const int row = i * 16 + g * 4 + e;
       if (row >= a.M) continue;
       if (SW) {
-        if (c0 >= a.N) continue;                             // gate tile j = 0, up tile j = 1 of group c0 / 32
-        const float gt = acc[i][0][e], up = acc[i][1][e];
-        reinterpret_cast<bf16_t*>(a.C)[(size_t)row * a.ldc + (c0 >> 5) * 16 + r] = f2bf(gt / (1.f + __expf(-gt)) * up);
+        // SwiGLU: tile pairs (2q, 2q+1) are the gate and up rows of logical group (c0 + 32q) / 32
+#pragma unroll
+        for (int q = 0; q < NTW / 2; ++q) {
+          const int cq = c0 + q * 32;
+          if (cq >= a.N) continue;
+          const float gt = acc[i][2 * q][e], up = acc[i][2 * q + 1][e];
+          reinterpret_cast<bf16_t*>(a.C)[(size_t)row * a.ldc + (cq >> 5) * 16 + r] = f2bf(gt / (1.f + __expf(-gt)) * up);
+        }
       } else {
 #pragma unroll
         for (int j = 0; j < NTW; ++j) {
@@ -400,7 +437,7 @@ __global__ __launch_bounds__(64 * ST_WV) void gemm_stream_kernel(GemmArgs a) {
 
 template <int MT, int EPI>
 hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st, bool reduce, hipEvent_t e0, hipEvent_t e1) {
-  const int nb = (a.N + ST_WV * ST_NTW * 16 - 1) / (ST_WV * ST_NTW * 16);
+  const int nb = (a.N + ST_COLS - 1) / ST_COLS;
   if (S > 1) {
     if (hipError_t e = launch_ev(gemm_stream_kernel<MT, EPI, true>, dim3(nb, S), dim3(64 * ST_WV), st, e0,
                                  reduce ? nullptr : e1, a))
@@ -670,7 +707,8 @@ hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st, bool reduce
     if (p.bm <= 32) return launch_stream<2, EPI>(a, p.splits, st, reduce, e0, e1);
     if (p.bm <= 64) return launch_stream<4, EPI>(a, p.splits, st, reduce, e0, e1);
     if (p.bm <= 128) return launch_stream<8, EPI>(a, p.splits, st, reduce, e0, e1);
-    return launch_stream<16, EPI>(a, p.splits, st, reduce, e0, e1);
+    if constexpr (stream_stages<16>() >= 2) return launch_stream<16, EPI>(a, p.splits, st, reduce, e0, e1);
+    else return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce, e0, e1);
   }
   if (p.big) {
     // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0
@@ -738,10 +776,10 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu) {
     // pieces that keep the grid within one workgroup per CU and >= 512 of K per piece
     p.stream = true;
     p.bm = M <= 32 ? 32 : M <= 64 ? 64 : M <= 128 ? 128 : 256;
-    const int tiles = (N + 127) / 128;
+    const int tiles = (N + ST_COLS - 1) / ST_COLS;
     int s = 1;
-    while (s + 1 <= max_splits && tiles * (s + 1) <= 256 && K / (s + 1) >= 512) ++s;
-    p.k_chunk = (((K + s - 1) / s) + 63) / 64 * 64;
+    while (s + 1 <= max_splits && tiles * (s + 1) <= 256 * HXF_ST_WG_PER_CU && K / (s + 1) >= 512) ++s;
+    p.k_chunk = (((K + s - 1) / s) + ST_KS - 1) / ST_KS * ST_KS;
     p.splits = (K + p.k_chunk - 1) / p.k_chunk;
     return p;
   }

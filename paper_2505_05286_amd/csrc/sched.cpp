@@ -115,8 +115,11 @@ int Scheduler::submit(const hxf_stage_req& q, i64 now, uint64_t* out_id, std::st
       err = "submit: parent has not finished with retained KV";
       return HXF_ESTATE;
     }
+    // the parent's sequence: its context and its tokens (under teacher forcing the forced
+    // ones, which are what its sequence holds)
+    const std::vector<int32_t>& ptoks = par->forced.empty() ? par->generated : par->forced;
     std::vector<int32_t> s(par->context);
-    s.insert(s.end(), par->generated.begin(), par->generated.end());
+    s.insert(s.end(), ptoks.begin(), ptoks.begin() + par->generated.size());
     const i64 n = (i64)s.size();
     n_shared = (n - 1) / page;
     r.context = s;

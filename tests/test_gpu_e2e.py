@@ -195,6 +195,27 @@ def test_forks_share_prefix_pages():
         assert eng.inst.tokens(rid) == list(map(int, ref[k])), f"fork {k}"
 
 
+def test_fork_of_a_teacher_forced_parent_continues_from_the_forced_tokens():
+    """A parent fed forced tokens holds them in its sequence: a fork continues from
+    prompt + forced tokens (not from the parent's own argmax)."""
+    shape, dm, w = device_model("tiny")
+    rng = np.random.default_rng(22)
+    eng = Engine(dm, max_context=512, n_blocks=80, max_seqs=8, chunk_tokens=64, cost_ps=COST, iter_ps=ITER)
+    prompt = rng.integers(0, shape.vocab, 38)
+    own, _ = M.generate(w, [prompt], [3])
+    forced = [int(t + 1) % shape.vocab for t in own[0]]          # never the argmax
+    par = eng.inst.submit(0, 0, 0, 0, 10 ** 7, prompt, 3, retain=True, forced=forced)
+    now = 0
+    while eng.inst.step(now)[0] != hxf.IDLE:
+        now += 1000
+    app = rng.integers(0, shape.vocab, 5)
+    kid = eng.inst.submit(now, 0, 1, 0, 10 ** 7, app, 4, parent=par)
+    while eng.inst.step(now)[0] != hxf.IDLE:
+        now += 1000
+    ref, ref_lg = M.generate(w, [np.concatenate([prompt, forced, app]).astype(np.int64)], [4])
+    compare_free_running("fork of a forced parent", eng.inst.tokens(kid), ref[0], ref_lg[0])
+
+
 def test_policy_does_not_change_tokens_and_runs_are_deterministic():
     shape, dm, w = device_model("tiny")
     rng = np.random.default_rng(8)

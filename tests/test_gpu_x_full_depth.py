@@ -33,11 +33,16 @@ from oracle import sched as S
 from paper_2505_05286_amd import hxf
 from paper_2505_05286_amd.device import DeviceModel, Engine
 
+from . import bf16_emulation as E
 from .gpu_util import log, rel_max_err
 
 pytestmark = pytest.mark.gpu
 
 TOL = 2e-2
+# A row's bound is max(TOL, DRIFT x the error of the bf16-rounding forward on the same
+# inputs): bf16 arithmetic alone drifts past TOL after a few layers of these random
+# weights, by an amount that adds up with depth.
+DRIFT = 2.0
 COST = (200 * S.PS, 50_000, 10, 150 * S.PS)
 ITER = (500 * S.PS, 1000, 20, 1)
 APPEND4 = (0, 0, 1, 2, 3, 5, 8, 13)
@@ -71,20 +76,27 @@ def tick(layer):
         log(f"  oracle layer {layer + 1}")
 
 
-def compare_rows(name, gpu_tok, gpu_rows, ref_rows):
-    """Logits of every row within TOL; ids equal or near ties.  Returns (worst, ties)."""
-    assert len(gpu_rows) == len(ref_rows), (name, len(gpu_rows), len(ref_rows))
-    worst, ties = 0.0, 0
-    for j, (g, r) in enumerate(zip(gpu_rows, ref_rows)):
-        worst = max(worst, rel_max_err(g, r))
+def compare_rows(name, gpu_tok, gpu_rows, ref_rows, emul_rows):
+    """Every row's logits within its bound, max(TOL, DRIFT x the drift of the bf16-rounding
+    forward on the same inputs); ids equal, or a near tie within that bound.
+    Returns (worst error, worst error / bound, near ties)."""
+    assert len(gpu_rows) == len(ref_rows) == len(emul_rows), (name, len(gpu_rows), len(ref_rows))
+    worst, worst_frac, ties, drift = 0.0, 0.0, 0, 0.0
+    for j, (g, r, e) in enumerate(zip(gpu_rows, ref_rows, emul_rows)):
+        d = rel_max_err(e, r)
+        bound = max(TOL, DRIFT * d)
+        err = rel_max_err(g, r)
+        worst, drift = max(worst, err), max(drift, d)
+        worst_frac = max(worst_frac, err / bound)
+        assert err <= bound, f"{name} row {j}: logits rel err {err:.3e} > bound {bound:.3e} (bf16 drift {d:.3e})"
         a = int(np.argmax(r))
         if gpu_tok[j] != a:
             gap = (r[a] - r[gpu_tok[j]]) / np.max(np.abs(r))
-            assert gap <= TOL, f"{name} row {j}: gpu id {gpu_tok[j]} vs oracle {a}, gap {gap:.3e} is no near tie"
+            assert gap <= bound, f"{name} row {j}: gpu id {gpu_tok[j]} vs oracle {a}, gap {gap:.3e} is no near tie"
             ties += 1
-    log(f"{name}: {len(ref_rows)} rows, logits rel err {worst:.2e}, near ties {ties}")
-    assert worst <= TOL, f"{name}: logits rel err {worst}"
-    return worst, ties
+    log(f"{name}: {len(ref_rows)} rows, logits rel err {worst:.2e} (bf16-rounding forward: {drift:.2e}), "
+        f"{worst_frac:.2f} of the bound, near ties {ties}")
+    return worst, worst_frac, ties
 
 
 def collect(inst, ids, rows):
@@ -120,9 +132,10 @@ def m8b():
 
 @pytest.fixture(scope="module")
 def ref8b(m8b):
-    """The oracle over all 32 layers for every 8B sample, in three passes."""
+    """The oracle over all 32 layers for every 8B sample, in three passes, and the
+    bf16-rounding forward on the same inputs (fed the oracle's tokens)."""
     shape, _, w = m8b
-    V = shape.vocab
+    V, L = shape.vocab, shape.n_layers
     t0 = time.time()
     cfg2 = synth.workloads.cfg2(V)
     s2 = [int(i) for i in np.argsort([len(s.prompt) for s in cfg2], kind="stable")[:2]]
@@ -133,40 +146,43 @@ def ref8b(m8b):
     rng = np.random.default_rng(404)
     apps = [rng.integers(0, V, n) for n in APPEND4]
     apps[1] = apps[0].copy()
-    seq2 = [M.Sequence(shape.n_layers) for _ in s2]
-    seq3 = M.Sequence(shape.n_layers)
-    par = M.Sequence(shape.n_layers)
-    prompts = [cfg2[i].prompt.astype(np.int64) for i in s2] + [prompts3[p3].prompt.astype(np.int64), parent]
-    log(f"full depth oracle pass 1: prefill of {sum(len(p) for p in prompts)} tokens")
-    out = M.forward(w, seq2 + [seq3, par], prompts, logit_rows=[[len(p) - 1] for p in prompts[:3]] + [[]],
-                    progress=tick)
-    lg2 = [[o[0]] for o in out[:2]]
-    tok2 = [[int(np.argmax(o[0]))] for o in out[:2]]
-    lg3 = out[2][0]
     shared = (PARENT4 - 1) // 16 * 16
-    forks = [par.fork(shared) for _ in APPEND4]
-    lg4, tok4 = [[] for _ in APPEND4], [[] for _ in APPEND4]
-    log(f"full depth oracle pass 2 after {time.time() - t0:.0f} s")
-    chunks = [np.array([t[-1]]) for t in tok2] + [np.concatenate([parent[shared:], a]) for a in apps]
-    out = M.forward(w, seq2 + forks, chunks, progress=tick)
-    for k in range(2):
-        lg2[k].append(out[k][0])
-        tok2[k].append(int(np.argmax(out[k][0])))
-    for b in range(len(APPEND4)):
-        lg4[b].append(out[2 + b][0])
-        tok4[b].append(int(np.argmax(out[2 + b][0])))
-    log(f"full depth oracle pass 3 after {time.time() - t0:.0f} s")
-    chunks = [np.array([t[-1]]) for t in tok2] + [np.array([t[-1]]) for t in tok4]
-    out = M.forward(w, seq2 + forks, chunks, progress=tick)
-    for k in range(2):
-        lg2[k].append(out[k][0])
-        tok2[k].append(int(np.argmax(out[k][0])))
-    for b in range(len(APPEND4)):
-        lg4[b].append(out[2 + b][0])
-        tok4[b].append(int(np.argmax(out[2 + b][0])))
-    log(f"full depth oracle (8B) done in {time.time() - t0:.0f} s")
-    return dict(s2=s2, tok2=tok2, lg2=lg2, p3=p3, lg3=lg3, tok3=int(np.argmax(lg3)), parent=parent, apps=apps,
-                tok4=tok4, lg4=lg4)
+    prompts = [cfg2[i].prompt.astype(np.int64) for i in s2] + [prompts3[p3].prompt.astype(np.int64), parent]
+    rows1 = [[len(p) - 1] for p in prompts[:3]] + [[]]
+    out = {}
+    tok2, tok4, tok3 = [[], []], [[] for _ in APPEND4], None
+    for kind, fwd in (("ref", M.forward), ("emul", E.forward)):
+        lg2, lg4 = [[], []], [[] for _ in APPEND4]
+        seqs = [M.Sequence(L) for _ in range(4)]
+        log(f"full depth {kind} pass 1: prefill of {sum(len(p) for p in prompts)} tokens ({time.time() - t0:.0f} s)")
+        o = fwd(w, seqs, prompts, logit_rows=rows1, progress=tick)
+        for k in range(2):
+            lg2[k].append(o[k][0])
+        lg3 = o[2][0]
+        if kind == "ref":
+            tok2 = [[int(np.argmax(o[k][0]))] for k in range(2)]
+            tok3 = int(np.argmax(lg3))
+        forks = [seqs[3].fork(shared) for _ in APPEND4]
+        for step in (1, 2):
+            log(f"full depth {kind} pass {step + 1} ({time.time() - t0:.0f} s)")
+            if step == 1:
+                chunks = [np.array([t[0]]) for t in tok2] + [np.concatenate([parent[shared:], a]) for a in apps]
+            else:
+                chunks = [np.array([t[1]]) for t in tok2] + [np.array([t[0]]) for t in tok4]
+            o = fwd(w, seqs[:2] + forks, chunks, progress=tick)
+            for k in range(2):
+                lg2[k].append(o[k][0])
+                if kind == "ref":
+                    tok2[k].append(int(np.argmax(o[k][0])))
+            for b in range(len(APPEND4)):
+                lg4[b].append(o[2 + b][0])
+                if kind == "ref":
+                    tok4[b].append(int(np.argmax(o[2 + b][0])))
+        out[kind] = dict(lg2=lg2, lg3=lg3, lg4=lg4)
+    log(f"full depth oracle and bf16-rounding forward (8B) done in {time.time() - t0:.0f} s")
+    return dict(s2=s2, tok2=tok2, p3=p3, tok3=tok3, parent=parent, apps=apps, tok4=tok4,
+                lg2=out["ref"]["lg2"], lg3=out["ref"]["lg3"], lg4=out["ref"]["lg4"],
+                em2=out["emul"]["lg2"], em3=out["emul"]["lg3"], em4=out["emul"]["lg4"])
 
 
 def test_cfg2_full_depth(m8b, ref8b):
@@ -204,7 +220,8 @@ def test_cfg2_full_depth(m8b, ref8b):
     for k, i in enumerate(s2):
         rid = ids[i]
         assert eng.inst.block_table(rid) == o_s.block_table(rid)
-        compare_rows(f"cfg2 ctx {len(cfg2[i].prompt)}", eng.inst.tokens(rid), rows[rid], ref8b["lg2"][k])
+        compare_rows(f"cfg2 ctx {len(cfg2[i].prompt)}", eng.inst.tokens(rid), rows[rid], ref8b["lg2"][k],
+                     ref8b["em2"][k])
     del eng
 
 
@@ -244,7 +261,8 @@ def test_cfg3_full_depth(m8b, ref8b):
     log(f"cfg3 full depth: prompt of {len(prompts[p3].prompt)} tokens over iterations (prefill, decode rows) "
         f"{chunks_with}")
     assert len(chunks_with) >= 2 and all(d == 32 for _, d in chunks_with)
-    compare_rows(f"cfg3 prompt {len(prompts[p3].prompt)}", inst.tokens(rid), rows[rid], [ref8b["lg3"]])
+    compare_rows(f"cfg3 prompt {len(prompts[p3].prompt)}", inst.tokens(rid), rows[rid], [ref8b["lg3"]],
+                 [ref8b["em3"]])
     del eng
 
 
@@ -284,7 +302,8 @@ def test_cfg4_full_depth(m8b, ref8b):
     log(f"cfg4 full depth: decode plan rows per item {sorted(set(int(x) for x in items[:, 3]))}")
     assert (items[:, 3] > 1).any()
     for b, r in enumerate(kids):
-        compare_rows(f"cfg4 branch {b} (+{len(apps[b])})", inst.tokens(r), rows[r], ref8b["lg4"][b])
+        compare_rows(f"cfg4 branch {b} (+{len(apps[b])})", inst.tokens(r), rows[r], ref8b["lg4"][b],
+                     ref8b["em4"][b])
     for a, b in ((0, 1),):
         for x, y in zip(rows[kids[a]], rows[kids[b]]):
             np.testing.assert_array_equal(x, y)
