@@ -625,6 +625,51 @@ def policy_ablation(n_wf=300):
             "scenarios": out}
 
 
+def measured_ablation(n_wf, rate, policies=("pq", "fcfs", "llf"), slo_scale=10, model="qwen32b"):
+    """The local-queue policy ablation on the GPU with the measured clock: the same
+    workload-5 workflows (arrivals rescaled to `rate` per second, SLO = slo_scale x the
+    isolated latency) replayed through the HIP instance once per policy; every
+    iteration's duration is its measured wall time (idle gaps are skipped to the next
+    arrival), so latencies and SLO attainment are served times, not cost-model times."""
+    import torch
+
+    import synth
+    from paper_2505_05286_amd import hxf
+    from paper_2505_05286_amd.device import Engine
+    from paper_2505_05286_amd.workflows import Driver
+    shape, dm = load_model(model)
+    cost, it = COST_PS[model]
+    pols = {"pq": hxf.POLICY_PQ, "fcfs": hxf.POLICY_FCFS, "llf": hxf.POLICY_LLF}
+    n_blocks = min(40_000, kv_pages_that_fit(shape))
+    out = []
+    for name in policies:
+        wfs = cfg5_workflows(n_wf, shape.vocab, model)
+        for w in wfs:
+            w.arrival_us = int(w.arrival_us * 0.5 / rate)
+            w.slo_us = w.slo_us * slo_scale // 10
+        eng = Engine(dm, max_context=8192 + 64 + 256 + 512 + 256 + 16, n_blocks=n_blocks, max_seqs=128,
+                     chunk_tokens=2048, cost_ps=cost, iter_ps=it, policy=pols[name], clock=hxf.CLOCK_MEASURED)
+        d = Driver(eng.inst, wfs, measured=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        d.run(report=lambda i, now, fin: progress(f"{name}: {i} iterations, clock {now / 1e6:.0f} s, {fin}/{n_wf} "
+                                                  f"workflows done, {time.perf_counter() - t0:.0f} s"),
+              report_every=1000)
+        torch.cuda.synchronize()
+        st = d.stats()
+        rnd = lambda v: None if v is None else round(v, 2)
+        res = {"policy": name, "slo_attainment": round(st["slo_attainment"], 4),
+               "p95_latency_s": rnd(st["p95_latency_s"]), "mean_latency_s": rnd(st["mean_latency_s"]),
+               "finished": st["finished"], "iterations": st["iterations"],
+               "gpu_seconds": round(time.perf_counter() - t0, 1)}
+        progress(json.dumps(res))
+        out.append(res)
+        del d, eng
+    return {"ablation": f"local queue policy on the GPU, measured clock, {MODEL_NAMES[model]} shape",
+            "workflows": n_wf, "rate_wf_per_s": rate, "slo_scale": slo_scale, "kv_pages": n_blocks,
+            "results": out}
+
+
 CLUSTER_SPEEDS = (1.0, 1.0, 2.0, 2.0)
 CLUSTER_SCENARIOS = [
     # (name, [(workflows, arrival rate in workflows/s), ...] in sequence)
@@ -820,6 +865,11 @@ def main():
                     help="run only the four 2080-row prefill GEMMs (for MFMA counter runs)")
     ap.add_argument("--policy-ablation", action="store_true",
                     help="PQ / FCFS / LLF on config-5 workflows, virtual clock, scheduler only (CPU)")
+    ap.add_argument("--measured-ablation", action="store_true",
+                    help="PQ / FCFS / LLF on workload-5 workflows on the GPU with the measured clock "
+                         "(--n-workflows, --rate, --slo-scale)")
+    ap.add_argument("--slo-scale", type=int, default=10, help="--measured-ablation: SLO as a multiple of the "
+                                                               "isolated latency")
     ap.add_argument("--cluster-sim", action="store_true",
                     help="coordinator across 4 heterogeneous scheduler-only instances: dispatch and alpha tuning (CPU)")
     ap.add_argument("--calibration-rows", help="--calibrate: also write the measured iterations (JSON) here")
@@ -848,6 +898,11 @@ def main():
 
     if args.calibrate:
         print(json.dumps(calibrate(args.calibrate, args.calibration_rows)), flush=True)
+        return
+
+    if args.measured_ablation:
+        print(json.dumps(measured_ablation(args.n_workflows, args.rate, slo_scale=args.slo_scale,
+                                           model=args.model or "qwen32b")), flush=True)
         return
 
     if args.cluster_sim:

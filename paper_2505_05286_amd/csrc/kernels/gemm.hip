@@ -265,22 +265,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int S) {
 // NSTG so the compiler can see that the LDS reads of a stage do not alias the
 // DMAs in flight (otherwise it waits for all of them).  Split K (grid.y)
 // writes fp32 partials; a reduction kernel (or the consumer) finishes them.
-#ifndef HXF_ST_WV
-#define HXF_ST_WV 4
-#endif
-#ifndef HXF_ST_NTW
-#define HXF_ST_NTW 2
-#endif
-#ifndef HXF_ST_KB
-#define HXF_ST_KB 2
-#endif
-#ifndef HXF_ST_NSTG
-#define HXF_ST_NSTG 3
-#endif
-#ifndef HXF_ST_WG_PER_CU
-#define HXF_ST_WG_PER_CU 1
-#endif
-constexpr int ST_WV = HXF_ST_WV, ST_NTW = HXF_ST_NTW, ST_KB = HXF_ST_KB, ST_NSTG = HXF_ST_NSTG;
+constexpr int ST_WV = 4, ST_NTW = 2, ST_KB = 2, ST_NSTG = 3;
 constexpr int ST_COLS = ST_WV * ST_NTW * 16;          // output columns per workgroup
 constexpr int ST_KS = 32 * ST_KB;                     // K per stage
 
@@ -660,6 +645,7 @@ struct BigCfg {
 constexpr BigCfg kBig[] = {
     {256, 256, 4, 2, 1.02, true}, {224, 256, 1, 8, 1.10, false}, {192, 256, 2, 4, 1.0, true},
     {160, 256, 1, 8, 1.17, false}, {128, 256, 2, 4, 1.3, true},    {128, 128, 2, 2, 1.6, true},
+    {256, 256, 2, 2, 1.02, true}, {192, 256, 2, 2, 1.0, true},     {256, 128, 2, 2, 1.3, true},
 };
 constexpr int kNumBig = sizeof(kBig) / sizeof(kBig[0]);
 
@@ -778,7 +764,7 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu) {
     p.bm = M <= 32 ? 32 : M <= 64 ? 64 : M <= 128 ? 128 : 256;
     const int tiles = (N + ST_COLS - 1) / ST_COLS;
     int s = 1;
-    while (s + 1 <= max_splits && tiles * (s + 1) <= 256 * HXF_ST_WG_PER_CU && K / (s + 1) >= 512) ++s;
+    while (s + 1 <= max_splits && tiles * (s + 1) <= 256 && K / (s + 1) >= 512) ++s;
     p.k_chunk = (((K + s - 1) / s) + ST_KS - 1) / ST_KS * ST_KS;
     p.splits = (K + p.k_chunk - 1) / p.k_chunk;
     return p;
