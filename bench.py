@@ -625,12 +625,13 @@ def policy_ablation(n_wf=300):
             "scenarios": out}
 
 
-def measured_ablation(n_wf, rate, policies=("pq", "fcfs", "llf"), slo_scale=10, model="qwen32b"):
+def measured_ablation(n_wf, rate, policies=("pq", "fcfs", "llf"), slo_scale=10, model="qwen32b", tenants=None):
     """The local-queue policy ablation on the GPU with the measured clock: the same
     workload-5 workflows (arrivals rescaled to `rate` per second, SLO = slo_scale x the
     isolated latency) replayed through the HIP instance once per policy; every
     iteration's duration is its measured wall time (idle gaps are skipped to the next
-    arrival), so latencies and SLO attainment are served times, not cost-model times."""
+    arrival), so latencies and SLO attainment are served times, not cost-model times.
+    tenants=(a, b): even workflows get SLO a x, odd ones b x (two tenants)."""
     import torch
 
     import synth
@@ -646,7 +647,7 @@ def measured_ablation(n_wf, rate, policies=("pq", "fcfs", "llf"), slo_scale=10, 
         wfs = cfg5_workflows(n_wf, shape.vocab, model)
         for w in wfs:
             w.arrival_us = int(w.arrival_us * 0.5 / rate)
-            w.slo_us = w.slo_us * slo_scale // 10
+            w.slo_us = w.slo_us * (slo_scale if tenants is None else tenants[w.wid % 2]) // 10
         eng = Engine(dm, max_context=8192 + 64 + 256 + 512 + 256 + 16, n_blocks=n_blocks, max_seqs=128,
                      chunk_tokens=2048, cost_ps=cost, iter_ps=it, policy=pols[name], clock=hxf.CLOCK_MEASURED)
         d = Driver(eng.inst, wfs, measured=True)
@@ -662,11 +663,17 @@ def measured_ablation(n_wf, rate, policies=("pq", "fcfs", "llf"), slo_scale=10, 
                "p95_latency_s": rnd(st["p95_latency_s"]), "mean_latency_s": rnd(st["mean_latency_s"]),
                "finished": st["finished"], "iterations": st["iterations"],
                "gpu_seconds": round(time.perf_counter() - t0, 1)}
+        if tenants is not None:
+            for t, sc in enumerate(tenants):
+                sel = [w for w in d.wf if w.wid % 2 == t]
+                res[f"slo_attainment_{sc}x"] = round(sum(0 <= w.finish_us - w.arrival_us <= w.slo_us
+                                                         for w in sel) / max(len(sel), 1), 4)
         progress(json.dumps(res))
         out.append(res)
         del d, eng
     return {"ablation": f"local queue policy on the GPU, measured clock, {MODEL_NAMES[model]} shape",
-            "workflows": n_wf, "rate_wf_per_s": rate, "slo_scale": slo_scale, "kv_pages": n_blocks,
+            "workflows": n_wf, "rate_wf_per_s": rate, "slo_scale": slo_scale if tenants is None else list(tenants),
+            "kv_pages": n_blocks,
             "results": out}
 
 
@@ -868,6 +875,8 @@ def main():
     ap.add_argument("--measured-ablation", action="store_true",
                     help="PQ / FCFS / LLF on workload-5 workflows on the GPU with the measured clock "
                          "(--n-workflows, --rate, --slo-scale)")
+    ap.add_argument("--tenants", help="--measured-ablation: two tenants' SLO multiples, e.g. 5,20 (even / odd "
+                                      "workflows)")
     ap.add_argument("--slo-scale", type=int, default=10, help="--measured-ablation: SLO as a multiple of the "
                                                                "isolated latency")
     ap.add_argument("--cluster-sim", action="store_true",
@@ -901,8 +910,9 @@ def main():
         return
 
     if args.measured_ablation:
+        tenants = tuple(int(x) for x in args.tenants.split(",")) if args.tenants else None
         print(json.dumps(measured_ablation(args.n_workflows, args.rate, slo_scale=args.slo_scale,
-                                           model=args.model or "qwen32b")), flush=True)
+                                           model=args.model or "qwen32b", tenants=tenants)), flush=True)
         return
 
     if args.cluster_sim:

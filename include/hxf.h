@@ -209,11 +209,22 @@ int hxf_bind(hxf_instance* inst, const hxf_device_buffers* bufs, void* hip_strea
  * per-request SLO budget, assigns an id (1, 2, ...), and queues it. */
 int hxf_submit(hxf_instance* inst, const hxf_stage_req* req, int64_t now_us, uint64_t* out_id);
 
-/* One batch boundary and one forward iteration.  Synchronous: returns after
- * the sampled token ids have reached the host.  HXF_IDLE if nothing ran. */
+/* One batch boundary and one forward iteration.  The batch is formed by the
+ * selection rule of Section 4.2: the queue is re-ranked at this boundary (the
+ * urgency U = t_comp - (t_SLO - tau) of every queued request, taken in decreasing
+ * order, i.e. the argmax over the local queue first, which the static key
+ * enq + t_SLO - t_comp ranks identically); running decodes take one token each,
+ * running prefills take chunk tokens in that order, then queued requests are
+ * admitted in that order while a sequence slot, their page reservation and the
+ * chunk budget allow, stopping at the first that does not fit.  now_us is the
+ * caller's clock.  Synchronous: returns after the sampled token ids have reached
+ * the host.  HXF_IDLE if nothing ran. */
 int hxf_step(hxf_instance* inst, int64_t now_us, hxf_step_info* out);
 
-/* Move up to cap completion records (in finishing order) to out. */
+/* Move up to cap completion records (in finishing order) to out.  A completion
+ * frees its request's place in the queue, after which Section 4.2's selection
+ * takes the next most urgent request at the next hxf_step; each record carries
+ * the request's budget t_SLO and whether it finished within it. */
 int hxf_drain(hxf_instance* inst, hxf_completion* out, int32_t cap, int32_t* n);
 /* Generated (sampled) tokens of a request so far.  HXF_ENOMEM if cap is too small (n is set). */
 int hxf_completion_tokens(hxf_instance* inst, uint64_t id, int32_t* buf, int32_t cap, int32_t* n);

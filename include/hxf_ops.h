@@ -100,16 +100,18 @@ int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k
  * bt_host (may be NULL): the same block table on the host.  When given, sequences whose tables start
  * with the same physical pages (forks of one retained parent, e.g. the parallel candidate requests
  * of one query, Section 2.1) are grouped and their common full pages are read once for up to
- * min(4, 16 / (Hq/Hkv)) of them; the result is the same attention.  Each (sequence, kv-head) stream is
+ * min(8, 32 / (Hq/Hkv)) of them (a second 16-column MFMA tile reuses every K/V read when more
+ * than 16 / (Hq/Hkv) rows share an item); the result is the same attention.  Each (sequence, kv-head) stream is
  * split into equal page-aligned partitions (at least 256 tokens, sized so that the work items fill
  * the wavefronts the chip holds at once), merged by log-sum-exp.
  * workspace: hxf_op_decode_attention_workspace_bytes(...) bytes (same ctx_host, bt_host, bt_stride). */
 int64_t hxf_op_decode_attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
                                                 const int32_t* ctx_host, const int32_t* bt_host, int32_t bt_stride);
 /* Introspection (host only, no device work): the decode-attention work list the two calls above
- * build.  items: n_items records of 16 int32 {kvh, t0, t1, n_rows, entry[4], part[4], pad[4]}
+ * build.  items: n_items records of 24 int32 {kvh, t0, t1, n_rows, entry[8], part[8], pad[4]}
  * (tokens [t0, t1) of kv-head kvh through the pages of entry[0], attended by the first n_rows
- * entries, partial of row r in slot part[r]); merges: n_merges records of 4 int32
+ * entries, partial of row r in slot part[r]); the one-tile items (n_rows <= max(1, 16 / G)) come
+ * first, then the two-tile items, each longest first; merges: n_merges records of 4 int32
  * {entry, kvh, part0, n_part}.  Returns HXF_ENOMEM (with the counts set) when a capacity is short. */
 int hxf_op_decode_plan(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* ctx_host, const int32_t* bt_host,
                        int32_t bt_stride, int32_t* items, int32_t items_cap, int32_t* n_items, int32_t* merges,

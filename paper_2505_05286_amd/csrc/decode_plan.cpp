@@ -1,4 +1,5 @@
-// Decode-attention work list: prefix groups, partitions, partial slots.
+// Attention work lists: decode (prefix groups, partitions, partial slots) and
+// chunked prefill (query blocks, key-range splits).
 #include "decode_plan.hpp"
 
 #include <algorithm>
@@ -18,13 +19,16 @@ struct Stream {
 }  // namespace
 
 void plan_decode(const std::vector<DecodeSeq>& seqs, int hkv, int G, DecodePlan& out) {
+  // every field is overwritten: the caller reuses one plan across iterations, and a stale
+  // count of wide items with no items behind it would send the two-tile kernel past them
   out.items.clear();
   out.merges.clear();
   out.n_parts = 0;
   out.kv_tokens = 0;
+  out.n_wide = 0;
   const int n = (int)seqs.size();
   if (n == 0) return;
-  const int R = std::max(1, std::min(kDecodeRows, 16 / G));
+  const int R1 = decode_rows_narrow(G), R = decode_rows_wide(G);
 
   // prefix groups: equal first page, shared length = the shortest common run of full pages
   std::vector<int> order, shared(n, 0);
@@ -92,6 +96,7 @@ void plan_decode(const std::vector<DecodeSeq>& seqs, int hkv, int G, DecodePlan&
       out.merges.push_back(MergeItem{seqs[i].entry, h, (int32_t)(base[i] + (int64_t)h * nslots[i]), nslots[i]});
   }
   out.n_parts = slot;
+  std::vector<DecodeItem> wide;
   for (size_t k = 0; k < streams.size(); ++k) {
     const Stream& st = streams[k];
     for (int h = 0; h < hkv; ++h)
@@ -107,10 +112,52 @@ void plan_decode(const std::vector<DecodeSeq>& seqs, int hkv, int G, DecodePlan&
           it.part[r] = (int32_t)(base[i] + (int64_t)h * nslots[i] + st.slot_off + p);
         }
         out.kv_tokens += it.t1 - it.t0;
-        out.items.push_back(it);
+        (st.n_rows > R1 ? wide : out.items).push_back(it);
       }
   }
+  // one-tile items first, then the wide ones, each longest first
   order_decode_items(out.items.data(), out.items.size());
+  order_decode_items(wide.data(), wide.size());
+  out.n_wide = (int64_t)wide.size();
+  out.items.insert(out.items.end(), wide.begin(), wide.end());
+}
+
+void plan_prefill(const std::vector<PrefillEntry>& entries, int hkv, int qpi, PrefillPlan& out) {
+  out.items.clear();
+  out.merges.clear();
+  out.n_parts = 0;
+  out.tiles = 0;
+  std::vector<PrefillItem> whole;
+  for (const PrefillEntry& e : entries)
+    for (int h = 0; h < hkv; ++h)
+      for (int q0 = 0; q0 < e.n; q0 += qpi) {
+        const int nq = std::min(qpi, e.n - q0);
+        const int t1 = (e.pos0 + q0 + nq + 31) / 32;
+        whole.push_back(PrefillItem{e.entry, h, q0, nq, 0, t1, -1, 0});
+        out.tiles += t1;
+      }
+  // the per-slot share of one pass over the resident workgroups
+  const int64_t share = std::max<int64_t>((out.tiles + kPrefillResident - 1) / kPrefillResident, kPrefillMinTiles);
+  for (const PrefillItem& it : whole) {
+    if (it.t1 <= share) {
+      out.items.push_back(it);
+      continue;
+    }
+    const int np = (int)((it.t1 + share - 1) / share);
+    const int len = (it.t1 + np - 1) / np;
+    const int part0 = (int)out.n_parts;
+    int k = 0;
+    for (int t0 = 0; t0 < it.t1; t0 += len, ++k) {
+      PrefillItem p = it;
+      p.t0 = t0;
+      p.t1 = std::min(it.t1, t0 + len);
+      p.part = part0 + k;
+      out.items.push_back(p);
+    }
+    out.n_parts += k;
+    out.merges.push_back(PrefillMerge{it.entry, it.kvh, it.q0, it.nq, part0, k, 0, 0});
+  }
+  order_prefill_items(out.items.data(), out.items.size());
 }
 
 }  // namespace hxf

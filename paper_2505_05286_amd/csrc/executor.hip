@@ -70,13 +70,15 @@ WsPlan plan_workspace(const hxf_model_cfg& m, const hxf_sched_cfg& s) {
   p.dec_items_max = decode_parts_bound(s.max_seqs, hkv, m.max_context);
   p.merges_max = (int64_t)s.max_seqs * hkv;
   const int qpi = prefill_queries_per_item((int)G);
-  p.pf_items_max = hkv * (ceil_div(s.chunk_tokens, qpi) + s.max_seqs);
+  p.pf_merges_max = hkv * (ceil_div(s.chunk_tokens, qpi) + s.max_seqs);   // whole prefill items
+  p.pf_parts_max = prefill_parts_bound(p.pf_merges_max);
+  p.pf_items_max = p.pf_merges_max + kPrefillResident;                    // with the parts of split items
   // metadata (int32 words), sections packed in this order, each 64-word aligned
   auto words = [](int64_t n) { return (n + 63) & ~int64_t(63); };
   const int64_t meta_words = words(1) + words(p.t_max) * 3 + words(p.r_max) + words(p.e_max) * 2 +
                              words(p.e_max * p.bt_w) + words(p.dec_items_max * (int64_t)(sizeof(DecodeItem) / 4)) +
-                             words(p.merges_max * 4) +
-                             words(p.pf_items_max * 4);
+                             words(p.merges_max * 4) + words(p.pf_items_max * (int64_t)(sizeof(PrefillItem) / 4)) +
+                             words(p.pf_merges_max * (int64_t)(sizeof(PrefillMerge) / 4));
   p.meta_bytes = meta_words * 4;
   // split-K partials: largest splits*M*N over the GEMM shapes at M <= 256
   int64_t part = 0;
@@ -99,6 +101,8 @@ WsPlan plan_workspace(const hxf_model_cfg& m, const hxf_sched_cfg& s) {
   p.off_part = take(std::max<int64_t>(part, 256));
   p.off_attn_o = take(p.dec_items_max * G * dh * 4);
   p.off_attn_ml = take(p.dec_items_max * G * 2 * 4);
+  p.off_pf_o = take(p.pf_parts_max * kPrefillPairs * dh * 4);
+  p.off_pf_ml = take(p.pf_parts_max * kPrefillPairs * 2 * 4);
   p.off_logits = take(p.r_max * m.vocab * 4);
   p.off_hr = take(p.r_max * d * 2);
   p.off_sampled = take(p.r_max * 4);
@@ -189,6 +193,7 @@ class HipExecutor : public Executor {
   int32_t* host_sampled_ = nullptr;
   std::vector<uint64_t> last_rows_;   // request id per logits row of the last iteration
   DecodePlan dplan_;                  // decode-attention work list of the current iteration
+  PrefillPlan pplan_;                 // prefill-attention work list of the current iteration
   bool ev_ = false;
   std::vector<hipEvent_t> ev_pool_, ev_merge_;
   // Decode-only iterations replay a captured HIP graph of the whole forward (metadata
@@ -286,13 +291,13 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   int32_t* hm = reinterpret_cast<int32_t*>(host_meta_);
   int64_t w = 0;
   auto sec = [&](int64_t n) { int64_t at = w; w += (n + 63) & ~int64_t(63); return at; };
-  const int64_t o_nitems = sec(1);
+  const int64_t o_nitems = sec(2);
   const int64_t o_ids = sec(T), o_pos = sec(T), o_slot = sec(T), o_lrow = sec(R), o_row0 = sec(E), o_pos0 = sec(E),
                 o_bt = sec((int64_t)E * bt_w);
   int row = 0, r = 0;
   std::vector<DecodeSeq> dseqs;
   dseqs.reserve(n_dec);
-  std::vector<PrefillItem> pitems;
+  std::vector<PrefillEntry> pentries;
   const int qpi = prefill_queries_per_item(G);
   last_rows_.clear();
   for (int e = 0; e < E; ++e) {
@@ -315,31 +320,42 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     if (be.decode) {
       dseqs.push_back(DecodeSeq{e, be.pos0 + 1, bt.data()});
     } else {
-      for (int h = 0; h < hkv; ++h)
-        for (int q0 = 0; q0 < be.n; q0 += qpi) pitems.push_back(PrefillItem{e, h, q0, std::min(qpi, be.n - q0)});
+      pentries.push_back(PrefillEntry{e, be.pos0, be.n});
     }
     row += be.n;
   }
-  order_prefill_items(pitems.data(), pitems.size(), hm + o_pos0);
+  plan_prefill(pentries, hkv, qpi, pplan_);
+  const std::vector<PrefillItem>& pitems = pplan_.items;
+  const std::vector<PrefillMerge>& pmerges = pplan_.merges;
   plan_decode(dseqs, hkv, G, dplan_);
   const std::vector<DecodeItem>& ditems = dplan_.items;
   const std::vector<MergeItem>& merges = dplan_.merges;
+  if (dplan_.n_wide < 0 || dplan_.n_wide > (int64_t)ditems.size()) {
+    err = "run: decode work list counts are inconsistent";
+    return HXF_EINVAL;
+  }
   if ((int64_t)ditems.size() > plan_.dec_items_max || dplan_.n_parts > plan_.dec_items_max ||
-      (int64_t)pitems.size() > plan_.pf_items_max || (graph && (int64_t)ditems.size() > item_cap)) {
+      (int64_t)pitems.size() > plan_.pf_items_max || (int64_t)pmerges.size() > plan_.pf_merges_max ||
+      pplan_.n_parts > plan_.pf_parts_max || (graph && (int64_t)ditems.size() > item_cap)) {
     err = "run: attention work list exceeds the workspace plan";
     return HXF_EINVAL;
   }
   constexpr int64_t kItemWords = sizeof(DecodeItem) / 4;
   const int64_t o_ditems = sec((graph ? item_cap : (int64_t)ditems.size()) * kItemWords),
-                o_merges = sec((int64_t)merges.size() * 4), o_pitems = sec((int64_t)pitems.size() * 4);
+                o_merges = sec((int64_t)merges.size() * 4),
+                o_pitems = sec((int64_t)pitems.size() * (int64_t)(sizeof(PrefillItem) / 4)),
+                o_pmerges = sec((int64_t)pmerges.size() * (int64_t)(sizeof(PrefillMerge) / 4));
   if (w * 4 > plan_.meta_bytes) {
     err = "run: metadata exceeds the workspace plan";
     return HXF_EINVAL;
   }
-  hm[o_nitems] = (int32_t)ditems.size();
+  const int64_t n_wide = dplan_.n_wide, n_narrow = (int64_t)ditems.size() - n_wide;
+  hm[o_nitems] = (int32_t)n_narrow;
+  hm[o_nitems + 1] = (int32_t)n_wide;
   std::memcpy(hm + o_ditems, ditems.data(), ditems.size() * sizeof(DecodeItem));
   std::memcpy(hm + o_merges, merges.data(), merges.size() * sizeof(MergeItem));
   std::memcpy(hm + o_pitems, pitems.data(), pitems.size() * sizeof(PrefillItem));
+  std::memcpy(hm + o_pmerges, pmerges.data(), pmerges.size() * sizeof(PrefillMerge));
   if (check_) {
     // every index a kernel follows, checked on the host against the buffers it addresses
     auto fail = [&](const char* what, int64_t i) {
@@ -366,7 +382,8 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     }
     for (size_t i = 0; i < ditems.size(); ++i) {
       const DecodeItem& d = ditems[i];
-      if (d.kvh < 0 || d.kvh >= hkv || d.t0 < 0 || d.t0 >= d.t1 || d.n_rows < 1 || d.n_rows > kDecodeRows)
+      const int rows_max = (int64_t)i < n_narrow ? decode_rows_narrow(G) : decode_rows_wide(G);
+      if (d.kvh < 0 || d.kvh >= hkv || d.t0 < 0 || d.t0 >= d.t1 || d.n_rows < 1 || d.n_rows > rows_max)
         return fail("decode item", (int64_t)i);
       for (int k = 0; k < d.n_rows; ++k)
         if (d.entry[k] < 0 || d.entry[k] >= E || !batch[d.entry[k]].decode || d.t1 > ctx[d.entry[k]] ||
@@ -382,8 +399,17 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     for (size_t i = 0; i < pitems.size(); ++i) {
       const PrefillItem& pi = pitems[i];
       if (pi.entry < 0 || pi.entry >= E || batch[pi.entry].decode || pi.kvh < 0 || pi.kvh >= hkv || pi.q0 < 0 ||
-          pi.nq < 1 || pi.q0 + pi.nq > batch[pi.entry].n)
+          pi.nq < 1 || pi.nq * G > kPrefillPairs || pi.q0 + pi.nq > batch[pi.entry].n || pi.t0 < 0 ||
+          pi.t0 >= pi.t1 || (int64_t)pi.t1 * 32 > ((int64_t)ctx[pi.entry] + 31) / 32 * 32 ||
+          pi.part >= pplan_.n_parts)
         return fail("prefill item", (int64_t)i);
+    }
+    for (size_t i = 0; i < pmerges.size(); ++i) {
+      const PrefillMerge& pm = pmerges[i];
+      if (pm.entry < 0 || pm.entry >= E || batch[pm.entry].decode || pm.kvh < 0 || pm.kvh >= hkv || pm.nq < 1 ||
+          pm.nq * G > kPrefillPairs || pm.q0 < 0 || pm.q0 + pm.nq > batch[pm.entry].n || pm.n_part < 1 ||
+          pm.part0 < 0 || pm.part0 + pm.n_part > pplan_.n_parts)
+        return fail("prefill merge", (int64_t)i);
     }
   }
   int32_t* dm = dev<int32_t>(plan_.off_meta);
@@ -407,7 +433,8 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   da.bt = dm + o_bt;
   da.bt_stride = bt_w;
   da.items = reinterpret_cast<const DecodeItem*>(dm + o_ditems);
-  da.n_items = graph ? (int)item_cap : (int)ditems.size();
+  da.n_items = graph ? (int)item_cap : (int)n_narrow;
+  da.n_wide = graph ? (n_wide ? (int)item_cap : 0) : (int)n_wide;
   da.n_items_dev = graph ? dm + o_nitems : nullptr;
   da.merges = reinterpret_cast<const MergeItem*>(dm + o_merges);
   da.n_merges = (int)merges.size();
@@ -429,6 +456,10 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   pa.bt_stride = bt_w;
   pa.items = reinterpret_cast<const PrefillItem*>(dm + o_pitems);
   pa.n_items = (int)pitems.size();
+  pa.merges = reinterpret_cast<const PrefillMerge*>(dm + o_pmerges);
+  pa.n_merges = (int)pmerges.size();
+  pa.part_o = dev<float>(plan_.off_pf_o);
+  pa.part_ml = dev<float>(plan_.off_pf_ml);
   pa.out = attn;
   pa.out_stride = hq * dh;
   pa.Hq = hq;
@@ -472,7 +503,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
         HXF_HIP(rope_kv_launch(qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq, hkv, dh, st_));
       da.k_pool = pa.k_pool = kp;
       da.v_pool = pa.v_pool = vp;
-      if (da.n_items) {
+      if (da.n_items || da.n_wide) {
         hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr, e3 = nullptr;
         if (prof.on) {
           HXF_HIP(hipEventCreate(&e0));
@@ -536,7 +567,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
       if (!graph_st_) HXF_HIP(hipStreamCreate(&graph_st_));
       st_ = graph_st_;
     }
-    const int64_t key = ((int64_t)E << 32) | (int64_t)bt_w;
+    const int64_t key = ((int64_t)E << 32) | ((int64_t)bt_w << 1) | (dplan_.n_wide > 0 ? 1 : 0);
     GraphRec* g = nullptr;
     for (auto& x : graphs_)
       if (x.key == key) g = &x;
@@ -578,7 +609,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
     }
     HXF_HIP(hipStreamSynchronize(st_));
   }
-  if (prof.on && da.n_items) {
+  if (prof.on && (da.n_items || da.n_wide)) {
     prof.decode_attn_launches += m_.n_layers;
     prof.decode_attn_bytes += (int64_t)m_.n_layers * kv_tokens * 2 * dh * 2;
   }

@@ -13,12 +13,12 @@ namespace hxf {
 
 struct WsPlan {
   int64_t t_max = 0, r_max = 0, e_max = 0, bt_w = 0;
-  int64_t dec_items_max = 0, merges_max = 0, pf_items_max = 0;
+  int64_t dec_items_max = 0, merges_max = 0, pf_items_max = 0, pf_merges_max = 0, pf_parts_max = 0;
   // byte offsets into the workspace
   int64_t off_meta = 0, meta_bytes = 0;
   int64_t off_rope = 0, off_resid = 0, off_h = 0, off_qkv = 0, off_attn = 0, off_act = 0;
   int64_t off_part = 0, part_bytes = 0;
-  int64_t off_attn_o = 0, off_attn_ml = 0;
+  int64_t off_attn_o = 0, off_attn_ml = 0, off_pf_o = 0, off_pf_ml = 0;
   int64_t off_logits = 0, off_hr = 0, off_sampled = 0;
   int64_t total = 0;
 };

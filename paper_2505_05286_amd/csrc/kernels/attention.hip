@@ -74,78 +74,88 @@ __device__ __forceinline__ uint2 keep_mask(int n) {
   return make_uint2((uint32_t)m, (uint32_t)(m >> 32));
 }
 
-template <int DH, bool CAUSAL>
-__device__ __forceinline__ void compute_pair(AttnState<DH>& S, const PairRegs<DH>& R, const bf16x8* qf, int page,
-                                             int t_end, int lim, float scale_log2, int lane) {
+// Scores, online softmax and PV product of one page pair for NT column tiles of 16
+// (query, head) pairs each; the K/V registers are shared by the tiles.
+template <int DH, bool CAUSAL, int NT>
+__device__ __forceinline__ void compute_pair(AttnState<DH> (&S)[NT], const PairRegs<DH>& R,
+                                             const bf16x8 (&qf)[NT][DH / 32], int page, int t_end, int lim,
+                                             float scale_log2, int lane) {
   const int rq = lane >> 4;
-  f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int s = 0; s < DH / 32; ++s) {
-    sa = mfma16x16x32(as_bf16x8(R.ka[s]), qf[s], sa);
-    sb = mfma16x16x32(as_bf16x8(R.kb[s]), qf[s], sb);
-  }
   const int ta = page * kPage + rq * 4;   // first token of this lane's rows in page a
   const int tb = ta + kPage;
   const bool full = (page + 2) * kPage <= t_end;   // wavefront-uniform
-  float x[8];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    x[e] = sa[e] * scale_log2;
-    x[4 + e] = sb[e] * scale_log2;
-  }
-  if (!full) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (ta + e >= t_end) x[e] = kNegInf;
-      if (tb + e >= t_end) x[4 + e] = kNegInf;
-    }
-  }
-  if (CAUSAL) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (ta + e > lim) x[e] = kNegInf;
-      if (tb + e > lim) x[4 + e] = kNegInf;
-    }
-  }
-  float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-  const float m_new = fmaxf(S.m, mx);
-  const float alpha = exp2f(S.m - m_new);
-  float p[8];
-  float psum = 0.f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    p[e] = exp2f(x[e] - m_new);
-    psum += p[e];
-  }
-  S.l = S.l * alpha + psum;
-  S.m = m_new;
-  const bf16x8 pf = as_bf16x8(make_uint4(pack_bf2(p[0], p[1]), pack_bf2(p[2], p[3]), pack_bf2(p[4], p[5]),
-                                         pack_bf2(p[6], p[7])));
   uint2 ma = make_uint2(~0u, ~0u), mb = make_uint2(~0u, ~0u);
   if (!full) {
     ma = keep_mask(t_end - ta);
     mb = keep_mask(t_end - tb);
   }
 #pragma unroll
-  for (int n = 0; n < DH / 16; ++n) {
-    S.acc[n] *= alpha;
-    const uint4 v = make_uint4(R.va[n].x & ma.x, R.va[n].y & ma.y, R.vb[n].x & mb.x, R.vb[n].y & mb.y);
-    S.acc[n] = mfma16x16x32(as_bf16x8(v), pf, S.acc[n]);
+  for (int t = 0; t < NT; ++t) {
+    f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < DH / 32; ++s) {
+      sa = mfma16x16x32(as_bf16x8(R.ka[s]), qf[t][s], sa);
+      sb = mfma16x16x32(as_bf16x8(R.kb[s]), qf[t][s], sb);
+    }
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[e] = sa[e] * scale_log2;
+      x[4 + e] = sb[e] * scale_log2;
+    }
+    if (!full) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (ta + e >= t_end) x[e] = kNegInf;
+        if (tb + e >= t_end) x[4 + e] = kNegInf;
+      }
+    }
+    if (CAUSAL) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (ta + e > lim) x[e] = kNegInf;
+        if (tb + e > lim) x[4 + e] = kNegInf;
+      }
+    }
+    float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    const float m_new = fmaxf(S[t].m, mx);
+    const float alpha = exp2f(S[t].m - m_new);
+    float p[8];
+    float psum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      p[e] = exp2f(x[e] - m_new);
+      psum += p[e];
+    }
+    S[t].l = S[t].l * alpha + psum;
+    S[t].m = m_new;
+    const bf16x8 pf = as_bf16x8(make_uint4(pack_bf2(p[0], p[1]), pack_bf2(p[2], p[3]), pack_bf2(p[4], p[5]),
+                                           pack_bf2(p[6], p[7])));
+#pragma unroll
+    for (int n = 0; n < DH / 16; ++n) {
+      S[t].acc[n] *= alpha;
+      const uint4 v = make_uint4(R.va[n].x & ma.x, R.va[n].y & ma.y, R.vb[n].x & mb.x, R.vb[n].y & mb.y);
+      S[t].acc[n] = mfma16x16x32(as_bf16x8(v), pf, S[t].acc[n]);
+    }
   }
 }
 
-// Attend the lane's column to tokens [t_begin, t_end) (t_begin page aligned);
-// tokens beyond `lim` are masked for this column.
-template <int DH, bool CAUSAL>
-__device__ __forceinline__ void attn_range(AttnState<DH>& S, const bf16x8* qf, const uint16_t* k_pool,
-                                           const uint16_t* v_pool, const int32_t* bt, int64_t nb, int kvh, int t_begin,
-                                           int t_end, int lim, float scale_log2, int lane) {
+// Attend the lanes' columns (NT tiles) to tokens [t_begin, t_end) (t_begin page
+// aligned); tokens beyond `lim` are masked.
+template <int DH, bool CAUSAL, int NT>
+__device__ __forceinline__ void attn_range(AttnState<DH> (&S)[NT], const bf16x8 (&qf)[NT][DH / 32],
+                                           const uint16_t* k_pool, const uint16_t* v_pool, const int32_t* bt,
+                                           int64_t nb, int kvh, int t_begin, int t_end, int lim, float scale_log2,
+                                           int lane) {
 #pragma unroll
-  for (int n = 0; n < DH / 16; ++n) S.acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  S.m = kNegInf;
-  S.l = 0.f;
+  for (int t = 0; t < NT; ++t) {
+#pragma unroll
+    for (int n = 0; n < DH / 16; ++n) S[t].acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    S[t].m = kNegInf;
+    S[t].l = 0.f;
+  }
   const int p0 = t_begin / kPage, p_end = (t_end + kPage - 1) / kPage;
   // two register buffers used in turn: the loads of the next page pair are in
   // flight while the current one is multiplied
@@ -153,13 +163,16 @@ __device__ __forceinline__ void attn_range(AttnState<DH>& S, const bf16x8* qf, c
   load_pair<DH>(ra, k_pool, v_pool, bt, nb, kvh, p0, t_end, lane);
   for (int p = p0; p < p_end; p += 4) {
     if (p + 2 < p_end) load_pair<DH>(rb, k_pool, v_pool, bt, nb, kvh, p + 2, t_end, lane);
-    compute_pair<DH, CAUSAL>(S, ra, qf, p, t_end, lim, scale_log2, lane);
+    compute_pair<DH, CAUSAL, NT>(S, ra, qf, p, t_end, lim, scale_log2, lane);
     if (p + 2 >= p_end) break;
     if (p + 4 < p_end) load_pair<DH>(ra, k_pool, v_pool, bt, nb, kvh, p + 4, t_end, lane);
-    compute_pair<DH, CAUSAL>(S, rb, qf, p + 2, t_end, lim, scale_log2, lane);
+    compute_pair<DH, CAUSAL, NT>(S, rb, qf, p + 2, t_end, lim, scale_log2, lane);
   }
-  S.l += __shfl_xor(S.l, 16, kWave);
-  S.l += __shfl_xor(S.l, 32, kWave);
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    S[t].l += __shfl_xor(S[t].l, 16, kWave);
+    S[t].l += __shfl_xor(S[t].l, 32, kWave);
+  }
 }
 
 template <int DH>
@@ -170,35 +183,62 @@ __device__ __forceinline__ void load_q(bf16x8* qf, const uint16_t* qrow, bool ok
     qf[s] = ok ? as_bf16x8(*reinterpret_cast<const uint4*>(qrow + s * 32 + rq * 8)) : as_bf16x8(make_uint4(0, 0, 0, 0));
 }
 
-static_assert(kDecodeRows == 4, "the row selects below assume four rows");
+// Element r of a row array of a decode item, r wavefront-varying (a select chain, no
+// scratch indexing).
+__device__ __forceinline__ int32_t item_row(const int32_t (&v)[kDecodeRows], int r) {
+  int32_t x = v[0];
+#pragma unroll
+  for (int k = 1; k < kDecodeRows; ++k) x = (r == k) ? v[k] : x;
+  return x;
+}
 
-template <int DH>
+// One wavefront per work item.  NT = 1: the 16 query columns are (row, head of the
+// group) pairs of up to 16/G rows; NT = 2 (wide items of a shared prefix): 32 columns,
+// up to 32/G rows, the second tile reusing every K/V page read for the first.  The
+// NT = 1 kernel takes the items [0, n_items), the NT = 2 kernel the n_wide items
+// that follow them (counts from device memory in captured launches).
+template <int DH, int NT>
 __global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
   const int lane = threadIdx.x;
-  const int w = blockIdx.x;
-  if (w >= (a.n_items_dev ? *a.n_items_dev : a.n_items)) return;
+  int w = blockIdx.x;
+  if (NT == 1) {
+    if (w >= (a.n_items_dev ? a.n_items_dev[0] : a.n_items)) return;
+  } else {
+    if (w >= (a.n_items_dev ? a.n_items_dev[1] : a.n_wide)) return;
+    w += a.n_items_dev ? a.n_items_dev[0] : a.n_items;
+  }
   const DecodeItem it = a.items[w];
   const int G = a.Hq / a.Hkv;
-  // column (lane % 16) = (row, head of the group); rows past n_rows are idle columns
-  const int col = lane & 15;
-  const int row = col / G, g = col - row * G;
-  const bool ok = row < it.n_rows && row < kDecodeRows;
-  const int r = ok ? row : 0;
-  const int entry = r == 0 ? it.entry[0] : r == 1 ? it.entry[1] : r == 2 ? it.entry[2] : it.entry[3];
-  const int part = r == 0 ? it.part[0] : r == 1 ? it.part[1] : r == 2 ? it.part[2] : it.part[3];
-  const int head = it.kvh * G + (ok ? g : 0);
-  bf16x8 qf[DH / 32];
-  load_q<DH>(qf, a.q + (size_t)a.q_row[entry] * a.q_stride + head * DH, ok, lane);
-  AttnState<DH> S;
-  attn_range<DH, false>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)it.entry[0] * a.bt_stride, a.n_blocks, it.kvh,
-                        it.t0, it.t1, 0x7FFFFFFF, a.scale_log2, lane);
-  if (!ok) return;
-  const int rq = lane >> 4;
-  float* o = a.part_o + ((size_t)part * G + g) * DH;
+  bf16x8 qf[NT][DH / 32];
+  bool ok[NT];
+  int part[NT], g[NT];
 #pragma unroll
-  for (int n = 0; n < DH / 16; ++n)
-    *reinterpret_cast<float4*>(o + n * 16 + rq * 4) = make_float4(S.acc[n][0], S.acc[n][1], S.acc[n][2], S.acc[n][3]);
-  if (rq == 0) *reinterpret_cast<float2*>(a.part_ml + ((size_t)part * G + g) * 2) = make_float2(S.m, S.l);
+  for (int t = 0; t < NT; ++t) {
+    // column (tile t, lane % 16) = (row, head of the group); rows past n_rows are idle columns
+    const int col = t * 16 + (lane & 15);
+    const int row = col / G;
+    g[t] = col - row * G;
+    ok[t] = row < it.n_rows && row < kDecodeRows;
+    const int r = ok[t] ? row : 0;
+    const int entry = item_row(it.entry, r);
+    part[t] = item_row(it.part, r);
+    const int head = it.kvh * G + (ok[t] ? g[t] : 0);
+    load_q<DH>(qf[t], a.q + (size_t)a.q_row[entry] * a.q_stride + head * DH, ok[t], lane);
+  }
+  AttnState<DH> S[NT];
+  attn_range<DH, false, NT>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)it.entry[0] * a.bt_stride, a.n_blocks, it.kvh,
+                            it.t0, it.t1, 0x7FFFFFFF, a.scale_log2, lane);
+  const int rq = lane >> 4;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (!ok[t]) continue;
+    float* o = a.part_o + ((size_t)part[t] * G + g[t]) * DH;
+#pragma unroll
+    for (int n = 0; n < DH / 16; ++n)
+      *reinterpret_cast<float4*>(o + n * 16 + rq * 4) =
+          make_float4(S[t].acc[n][0], S[t].acc[n][1], S[t].acc[n][2], S[t].acc[n][3]);
+    if (rq == 0) *reinterpret_cast<float2*>(a.part_ml + ((size_t)part[t] * G + g[t]) * 2) = make_float2(S[t].m, S[t].l);
+  }
 }
 
 // Log-sum-exp merge of the split-K partials; one wavefront per (entry, q-head).
@@ -312,7 +352,8 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   const int npairs = it.nq * G;
   const int pos0 = a.pos0[it.entry];
   const int kend = pos0 + it.q0 + it.nq;       // keys [0, kend) are visible to some pair
-  const int ntiles = (kend + 31) / 32;
+  const int tbase = it.t0;                     // this item's key tiles: [t0, t1)
+  const int ntiles = it.t1 - it.t0;
   const int last_page = (kend - 1) / kPage;
   // the block table does not change during the kernel: read it through the constant
   // address space, so that its (wavefront-uniform) entries come by scalar loads, which
@@ -340,7 +381,7 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
 
   // DMA of key tile t into a stage: the two K pages, then the two V pages, as stored
   auto issue = [&](int t, bf16_t* base) __attribute__((always_inline)) {
-    const int tt = min(t, ntiles - 1);
+    const int tt = tbase + min(t, ntiles - 1);
 #pragma unroll
     for (int u = 0; u < K_W; ++u) {
       const int blk = w * K_W + u;               // 1 KB block of the K tile
@@ -392,7 +433,7 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
 #pragma unroll
       for (int pt = 0; pt < PT; ++pt) s[pt] = mfma32x32x16(kf, qf[pt][ks], s[pt]);
     }
-    const int k0 = t * 32;
+    const int k0 = (tbase + t) * 32;
     const bool edge = (k0 + 32 > kend) || (k0 + 31 > pos0 + it.q0);   // wavefront-uniform: a mask is needed
     if (edge) {
 #pragma unroll
@@ -489,6 +530,24 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   float lt[PT];
 #pragma unroll
   for (int pt = 0; pt < PT; ++pt) lt[pt] = l[pt] + __shfl_xor(l[pt], 32, kWave);
+  if (it.part >= 0) {
+    // a part of a split item: unnormalized output, max and sum for the merge
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt) {
+      const int p = (w * PT + pt) * 32 + (lane & 31);
+      if (p >= npairs) continue;
+      float* po = a.part_o + ((size_t)it.part * kPrefillPairs + p) * DH;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4)
+          *reinterpret_cast<float4*>(po + dt * 32 + g4 * 8 + h * 4) =
+              make_float4(o[pt][dt][g4 * 4], o[pt][dt][g4 * 4 + 1], o[pt][dt][g4 * 4 + 2], o[pt][dt][g4 * 4 + 3]);
+      if (h == 0)
+        *reinterpret_cast<float2*>(a.part_ml + ((size_t)it.part * kPrefillPairs + p) * 2) = make_float2(m[pt], lt[pt]);
+    }
+    return;
+  }
 #pragma unroll
   for (int pt = 0; pt < PT; ++pt) {
     const int p = (w * PT + pt) * 32 + (lane & 31);
@@ -508,12 +567,54 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   }
 }
 
+// Log-sum-exp merge of the key-range parts of split prefill items: one workgroup per
+// (merge job, 64 pairs), four lanes per pair, each lane DH/4 dims.
+template <int DH>
+__global__ __launch_bounds__(256) void prefill_merge_kernel(PrefillAttnArgs a) {
+  const int job = blockIdx.x >> 1;
+  const PrefillMerge mg = a.merges[job];
+  const int G = a.Hq / a.Hkv;
+  const int p = (blockIdx.x & 1) * 64 + (threadIdx.x >> 2);
+  if (p >= mg.nq * G) return;
+  constexpr int PER = DH / 4;
+  const int d0 = (threadIdx.x & 3) * PER;
+  float M = -__builtin_huge_valf();
+  for (int j = 0; j < mg.n_part; ++j) M = fmaxf(M, a.part_ml[((size_t)(mg.part0 + j) * kPrefillPairs + p) * 2]);
+  float acc[PER];
+#pragma unroll
+  for (int d = 0; d < PER; ++d) acc[d] = 0.f;
+  float L = 0.f;
+  for (int j = 0; j < mg.n_part; ++j) {
+    const size_t slot = (size_t)(mg.part0 + j) * kPrefillPairs + p;
+    const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + slot * 2);
+    const float wgt = __builtin_amdgcn_exp2f(ml.x - M);
+    L += wgt * ml.y;
+    const float4* po = reinterpret_cast<const float4*>(a.part_o + slot * DH + d0);
+#pragma unroll
+    for (int d = 0; d < PER / 4; ++d) {
+      const float4 v = po[d];
+      acc[4 * d] += wgt * v.x;
+      acc[4 * d + 1] += wgt * v.y;
+      acc[4 * d + 2] += wgt * v.z;
+      acc[4 * d + 3] += wgt * v.w;
+    }
+  }
+  const float inv = 1.f / L;
+  const int qi = p / G, hj = p % G;
+  uint16_t* out = a.out + (size_t)(a.row0[mg.entry] + mg.q0 + qi) * a.out_stride + (mg.kvh * G + hj) * DH + d0;
+#pragma unroll
+  for (int d = 0; d < PER / 4; ++d)
+    *reinterpret_cast<uint2*>(out + 4 * d) = make_uint2(pack_bf2(acc[4 * d] * inv, acc[4 * d + 1] * inv),
+                                                       pack_bf2(acc[4 * d + 2] * inv, acc[4 * d + 3] * inv));
+}
+
 }  // namespace
 
 // pair tiles of 32 (query, head) pairs per wavefront in the prefill kernel
 constexpr int kPrefillPT = 1;
 
-int prefill_queries_per_item(int group) { return 4 * 32 * kPrefillPT / group; }
+static_assert(4 * 32 * kPrefillPT == kPrefillPairs, "pairs of a prefill item");
+int prefill_queries_per_item(int group) { return kPrefillPairs / group; }
 
 // With events, they take the kernel's own start and end timestamps; without, a plain
 // launch (the form a stream capture records).
@@ -526,10 +627,20 @@ static hipError_t launch_stamped(K kernel, dim3 grid, dim3 block, hipStream_t st
 }
 
 hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
-  if (a.n_items <= 0) return hipSuccess;
-  if (a.dh == 128) return launch_stamped(decode_attn_kernel<128>, dim3(a.n_items), dim3(64), st, ev_start, ev_stop, a);
-  if (a.dh == 64) return launch_stamped(decode_attn_kernel<64>, dim3(a.n_items), dim3(64), st, ev_start, ev_stop, a);
-  return hipErrorInvalidValue;
+  if (a.dh != 128 && a.dh != 64) return hipErrorInvalidValue;
+  const bool narrow = a.n_items > 0, wide = a.n_wide > 0;
+  if (narrow) {
+    hipEvent_t e1 = wide ? nullptr : ev_stop;
+    hipError_t e = a.dh == 128 ? launch_stamped(decode_attn_kernel<128, 1>, dim3(a.n_items), dim3(64), st, ev_start, e1, a)
+                               : launch_stamped(decode_attn_kernel<64, 1>, dim3(a.n_items), dim3(64), st, ev_start, e1, a);
+    if (e != hipSuccess) return e;
+  }
+  if (wide) {
+    hipEvent_t e0 = narrow ? nullptr : ev_start;
+    return a.dh == 128 ? launch_stamped(decode_attn_kernel<128, 2>, dim3(a.n_wide), dim3(64), st, e0, ev_stop, a)
+                       : launch_stamped(decode_attn_kernel<64, 2>, dim3(a.n_wide), dim3(64), st, e0, ev_stop, a);
+  }
+  return hipSuccess;
 }
 
 hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
@@ -543,14 +654,19 @@ hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent
 
 hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st, hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (a.n_items <= 0) return hipSuccess;
-  auto go = [&](auto kernel) {
-    if (ev_start || ev_stop) hipExtLaunchKernelGGL(kernel, dim3(a.n_items), dim3(256), 0, st, ev_start, ev_stop, 0, a);
-    else hipLaunchKernelGGL(kernel, dim3(a.n_items), dim3(256), 0, st, a);
+  if (a.dh != 128 && a.dh != 64) return hipErrorInvalidValue;
+  // with merges, the start event goes on the item kernel and the end event on the merge
+  hipEvent_t e1 = a.n_merges > 0 ? nullptr : ev_stop;
+  auto go = [&](auto kernel, dim3 grid, hipEvent_t s0, hipEvent_t s1) {
+    if (s0 || s1) hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, st, s0, s1, 0, a);
+    else hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, a);
     return hipGetLastError();
   };
-  if (a.dh == 128) return go(prefill_flash_kernel<128, kPrefillPT>);
-  if (a.dh == 64) return go(prefill_flash_kernel<64, kPrefillPT>);
-  return hipErrorInvalidValue;
+  hipError_t e = a.dh == 128 ? go(prefill_flash_kernel<128, kPrefillPT>, dim3(a.n_items), ev_start, e1)
+                             : go(prefill_flash_kernel<64, kPrefillPT>, dim3(a.n_items), ev_start, e1);
+  if (e != hipSuccess || a.n_merges <= 0) return e;
+  return a.dh == 128 ? go(prefill_merge_kernel<128>, dim3(2 * a.n_merges), nullptr, ev_stop)
+                     : go(prefill_merge_kernel<64>, dim3(2 * a.n_merges), nullptr, ev_stop);
 }
 
 }  // namespace hxf

@@ -645,7 +645,6 @@ struct BigCfg {
 constexpr BigCfg kBig[] = {
     {256, 256, 4, 2, 1.02, true}, {224, 256, 1, 8, 1.10, false}, {192, 256, 2, 4, 1.0, true},
     {160, 256, 1, 8, 1.17, false}, {128, 256, 2, 4, 1.3, true},    {128, 128, 2, 2, 1.6, true},
-    {256, 256, 2, 2, 1.02, true}, {192, 256, 2, 2, 1.0, true},     {256, 128, 2, 2, 1.3, true},
 };
 constexpr int kNumBig = sizeof(kBig) / sizeof(kBig[0]);
 

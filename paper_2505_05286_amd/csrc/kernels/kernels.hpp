@@ -91,15 +91,19 @@ hipError_t kv_scatter_launch(const uint16_t* k, const uint16_t* v, const int32_t
 // One decode work item: tokens [t0, t1) of kv-head `kvh`, read through the block
 // table of entry[0], attended by the queries of entries entry[0 .. n_rows) (more
 // than one when they share those pages: forks of one parent); row r's partial
-// result goes to slot part[r].  The 16 query columns of a wavefront are (row, head)
-// pairs, so at most min(kDecodeRows, 16 / G) rows.
-constexpr int kDecodeRows = 4;
+// result goes to slot part[r].  The query columns of a wavefront are (row, head)
+// pairs: one tile of 16 (at most 16 / G rows) or, for a wide item, two tiles of 16
+// (at most min(kDecodeRows, 32 / G) rows) that share every K/V read.
+constexpr int kDecodeRows = 8;
 struct DecodeItem {
   int32_t kvh, t0, t1, n_rows;
   int32_t entry[kDecodeRows];
   int32_t part[kDecodeRows];
   int32_t pad[4];
 };
+// Rows one 16-column tile holds, and the rows a wide (two-tile) item holds, for GQA group G.
+inline int decode_rows_narrow(int G) { return std::max(1, std::min(kDecodeRows, 16 / G)); }
+inline int decode_rows_wide(int G) { return std::max(1, std::min(kDecodeRows, 32 / G)); }
 // Launch order of the decode items: longest first (equal lengths keep their
 // order), so that the wavefronts that start last, when the chip drains, are the
 // short tail partitions.  Partial slots are unchanged, so the merge is unaffected.
@@ -140,9 +144,10 @@ struct DecodeAttnArgs {
   int64_t n_blocks;
   const int32_t* bt;       // [entries][bt_stride]
   int bt_stride;
-  const DecodeItem* items;
-  int n_items;                 // items, or the launch's capacity when n_items_dev is set
-  const int32_t* n_items_dev;  // may be null: the item count in device memory (captured launches)
+  const DecodeItem* items;     // n_items one-tile items, then n_wide two-tile items
+  int n_items;                 // one-tile items, or that launch's capacity when n_items_dev is set
+  int n_wide;                  // two-tile items, or that launch's capacity when n_items_dev is set
+  const int32_t* n_items_dev;  // may be null: both counts in device memory (captured launches)
   const MergeItem* merges;
   int n_merges;
   float* part_o;           // [parts][G][dh]
@@ -159,18 +164,31 @@ hipError_t decode_attn_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_
 hipError_t decode_merge_launch(const DecodeAttnArgs& a, hipStream_t st, hipEvent_t ev_start = nullptr,
                                hipEvent_t ev_stop = nullptr);
 
-// One prefill work item: queries [q0, q0 + nq) (chunk-local) of entry `entry`, kv-head `kvh`.
+// One prefill work item: queries [q0, q0 + nq) (chunk-local) of entry `entry`, kv-head
+// `kvh`, attending keys of the 32-key tiles [t0, t1).  part < 0: the item covers every
+// key its queries see and writes the normalized output; otherwise it writes its
+// unnormalized partial (output, running max, sum) to slot `part`, and a merge job
+// combines the slots of its query block by log-sum-exp.
 struct PrefillItem {
   int32_t entry, kvh, q0, nq;
+  int32_t t0, t1, part, pad;
 };
-// Launch order of the prefill items: most visible keys first (pos0 of the item's
-// entry + q0 + nq; equal counts keep their order), so that under the causal mask
-// the short items fill the chip's tail instead of the long ones.
-inline void order_prefill_items(PrefillItem* it, size_t n, const int32_t* pos0_of_entry) {
-  std::stable_sort(it, it + n, [&](const PrefillItem& x, const PrefillItem& y) {
-    return pos0_of_entry[x.entry] + x.q0 + x.nq > pos0_of_entry[y.entry] + y.q0 + y.nq;
-  });
+// Merge job: partial slots [part0, part0 + n_part) of (entry, kvh, queries [q0, q0 + nq)).
+struct PrefillMerge {
+  int32_t entry, kvh, q0, nq;
+  int32_t part0, n_part, pad0, pad1;
+};
+// Launch order of the prefill items: most key tiles first (equal counts keep their
+// order), so that the short items fill the chip's tail instead of the long ones.
+inline void order_prefill_items(PrefillItem* it, size_t n) {
+  std::stable_sort(it, it + n, [](const PrefillItem& x, const PrefillItem& y) { return x.t1 - x.t0 > y.t1 - y.t0; });
 }
+// Workgroups of the prefill kernel resident at once (two per CU: 80 KB of LDS each),
+// and the shortest key range an item is split into.
+constexpr int kPrefillResident = 512;
+// (query, head) pairs of one prefill item (its workgroup's columns), and of a partial slot
+constexpr int kPrefillPairs = 128;
+constexpr int kPrefillMinTiles = 8;
 struct PrefillAttnArgs {
   const uint16_t* q;       // bf16 rows; entry e's query i at row row0[e] + i
   int q_stride;
@@ -183,11 +201,16 @@ struct PrefillAttnArgs {
   int bt_stride;
   const PrefillItem* items;
   int n_items;
+  const PrefillMerge* merges;   // merge jobs of the split items
+  int n_merges;
+  float* part_o;                // [slots][128 pairs][dh]: unnormalized partial outputs
+  float* part_ml;               // [slots][128 pairs][2]: (max in log2 units, sum)
   uint16_t* out;
   int out_stride;
   int Hq, Hkv, dh;
   float scale_log2;
 };
+// The items, then (when some are split) the merge of their partials.
 hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st, hipEvent_t ev_start = nullptr,
                                hipEvent_t ev_stop = nullptr);
 // Queries covered by one prefill work item for a given GQA group size.

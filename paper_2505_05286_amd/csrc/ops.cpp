@@ -191,7 +191,8 @@ int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_poo
   a.bt = bt;
   a.bt_stride = bt_stride;
   a.items = reinterpret_cast<const DecodeItem*>(ws + L.off_items);
-  a.n_items = (int)P.items.size();
+  a.n_items = (int)(P.items.size() - P.n_wide);
+  a.n_wide = (int)P.n_wide;
   a.merges = reinterpret_cast<const MergeItem*>(ws + L.off_merges);
   a.n_merges = (int)L.merges;
   a.part_o = reinterpret_cast<float*>(ws + L.off_o);
@@ -206,12 +207,42 @@ int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_poo
   return dev_rc(hipStreamSynchronize(st));
 }
 
+namespace {
+
+// Workspace of hxf_op_prefill_attention: items (whole ones plus the parts of split
+// ones), merge jobs, row0 / pos0, then the partial outputs and (max, sum) of the parts.
+struct PrefillLayout {
+  int64_t off_merges = 0, off_rp = 0, off_o = 0, off_ml = 0, total = 0;
+};
+
+PrefillLayout prefill_layout(int64_t whole_items, int S, int dh) {
+  PrefillLayout L;
+  const int64_t items = whole_items + kPrefillResident, parts = prefill_parts_bound(whole_items);
+  int64_t o = al(items * (int64_t)sizeof(PrefillItem));
+  L.off_merges = o;
+  o = al(o + whole_items * (int64_t)sizeof(PrefillMerge));
+  L.off_rp = o;
+  o = al(o + (int64_t)S * 8);
+  L.off_o = o;
+  o = al(o + parts * kPrefillPairs * dh * 4);
+  L.off_ml = o;
+  L.total = al(o + parts * kPrefillPairs * 2 * 4);
+  return L;
+}
+
+int64_t prefill_whole_items(int S, int Hkv, int qpi, const int32_t* n_host) {
+  int64_t items = 0;
+  for (int s = 0; s < S; ++s) items += (int64_t)Hkv * ((n_host[s] + qpi - 1) / qpi);
+  return items;
+}
+
+}  // namespace
+
 int64_t hxf_op_prefill_attention_workspace_bytes(int32_t S, int32_t Hq, int32_t Hkv, const int32_t* n_host) {
   if (S < 0 || !n_host || Hq <= 0 || Hkv <= 0 || Hq % Hkv) return -1;
   const int qpi = prefill_queries_per_item(Hq / Hkv);
-  int64_t items = 0;
-  for (int s = 0; s < S; ++s) items += (int64_t)Hkv * ((n_host[s] + qpi - 1) / qpi);
-  return al(items * (int64_t)sizeof(PrefillItem)) + al((int64_t)S * 8);
+  // head_dim is not an argument: size the partials for the largest (128)
+  return prefill_layout(prefill_whole_items(S, Hkv, qpi, n_host), S, 128).total;
 }
 
 int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_pool, int64_t n_blocks, const int32_t* bt,
@@ -228,31 +259,36 @@ int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_po
   const int64_t need = hxf_op_prefill_attention_workspace_bytes(S, Hq, Hkv, n_host);
   if (!workspace || ws_bytes < need) return HXF_ENOMEM;
   const int qpi = prefill_queries_per_item(Hq / Hkv);
-  std::vector<PrefillItem> items;
+  std::vector<PrefillEntry> entries;
   for (int s = 0; s < S; ++s)
-    for (int h = 0; h < Hkv; ++h)
-      for (int q0 = 0; q0 < n_host[s]; q0 += qpi) items.push_back(PrefillItem{s, h, q0, std::min(qpi, n_host[s] - q0)});
-  order_prefill_items(items.data(), items.size(), pos0);
-  const int64_t off_rp = al((int64_t)items.size() * (int64_t)sizeof(PrefillItem));
-  std::vector<uint8_t> host(off_rp + (int64_t)S * 8);
-  std::memcpy(host.data(), items.data(), items.size() * sizeof(PrefillItem));
-  std::memcpy(host.data() + off_rp, row0, (size_t)S * 4);
-  std::memcpy(host.data() + off_rp + S * 4, pos0, (size_t)S * 4);
+    if (n_host[s] > 0) entries.push_back(PrefillEntry{s, pos0[s], n_host[s]});
+  PrefillPlan P;
+  plan_prefill(entries, Hkv, qpi, P);
+  const PrefillLayout L = prefill_layout(prefill_whole_items(S, Hkv, qpi, n_host), S, 128);
+  std::vector<uint8_t> host(L.off_rp + (int64_t)S * 8);
+  std::memcpy(host.data(), P.items.data(), P.items.size() * sizeof(PrefillItem));
+  std::memcpy(host.data() + L.off_merges, P.merges.data(), P.merges.size() * sizeof(PrefillMerge));
+  std::memcpy(host.data() + L.off_rp, row0, (size_t)S * 4);
+  std::memcpy(host.data() + L.off_rp + S * 4, pos0, (size_t)S * 4);
   hipStream_t st = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
   if (hipMemcpyAsync(ws, host.data(), host.size(), hipMemcpyHostToDevice, st) != hipSuccess) return HXF_EDEVICE;
   PrefillAttnArgs a{};
   a.q = (const uint16_t*)q;
   a.q_stride = Hq * dh;
-  a.row0 = reinterpret_cast<const int32_t*>(ws + off_rp);
-  a.pos0 = reinterpret_cast<const int32_t*>(ws + off_rp + S * 4);
+  a.row0 = reinterpret_cast<const int32_t*>(ws + L.off_rp);
+  a.pos0 = reinterpret_cast<const int32_t*>(ws + L.off_rp + S * 4);
   a.k_pool = (const uint16_t*)k_pool;
   a.v_pool = (const uint16_t*)v_pool;
   a.n_blocks = n_blocks;
   a.bt = bt;
   a.bt_stride = bt_stride;
   a.items = reinterpret_cast<const PrefillItem*>(ws);
-  a.n_items = (int)items.size();
+  a.n_items = (int)P.items.size();
+  a.merges = reinterpret_cast<const PrefillMerge*>(ws + L.off_merges);
+  a.n_merges = (int)P.merges.size();
+  a.part_o = reinterpret_cast<float*>(ws + L.off_o);
+  a.part_ml = reinterpret_cast<float*>(ws + L.off_ml);
   a.out = (uint16_t*)out;
   a.out_stride = Hq * dh;
   a.Hq = Hq;

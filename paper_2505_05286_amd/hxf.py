@@ -448,15 +448,31 @@ def op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, ctx, bt_host=None, bt_st
     return lib().hxf_op_decode_attention_workspace_bytes(B, Hq, Hkv, dh, cp, bp, bt_stride)
 
 
+DECODE_ITEM_WORDS = 24
+DECODE_ROWS = 8
+
+
+def decode_rows_narrow(G):
+    """Rows of a one-tile decode item (16 query columns) for GQA group size G."""
+    return max(1, min(DECODE_ROWS, 16 // G))
+
+
+def decode_rows_wide(G):
+    """Rows of a two-tile (wide) decode item (32 query columns)."""
+    return max(1, min(DECODE_ROWS, 32 // G))
+
+
 def op_decode_plan(B, Hq, Hkv, ctx, bt_host=None, bt_stride=0):
-    """The decode-attention work list: (items int32 [n, 16], merges int32 [m, 4])."""
+    """The decode-attention work list: (items int32 [n, 24], merges int32 [m, 4]).  An item is
+    {kvh, t0, t1, n_rows, entry[8], part[8], pad[4]}; one-tile items come first, then the
+    two-tile (wide) items."""
     c, cp = _i32(ctx)
     b, bp = _i32(bt_host) if bt_host is not None else (None, None)
     ni, nm = C.c_int32(0), C.c_int32(0)
     rc = lib().hxf_op_decode_plan(B, Hq, Hkv, cp, bp, bt_stride, None, 0, C.byref(ni), None, 0, C.byref(nm))
     if rc not in (OK, ENOMEM):
         raise HxfError(rc, "hxf_op_decode_plan")
-    items = np.zeros((ni.value, 16), np.int32)
+    items = np.zeros((ni.value, DECODE_ITEM_WORDS), np.int32)
     merges = np.zeros((nm.value, 4), np.int32)
     _op(lib().hxf_op_decode_plan(B, Hq, Hkv, cp, bp, bt_stride, items.ctypes.data_as(C.POINTER(C.c_int32)),
                                  ni.value, C.byref(ni), merges.ctypes.data_as(C.POINTER(C.c_int32)), nm.value,

@@ -38,13 +38,15 @@ def _check(ctxs, hq, hkv, bt=None):
     G = hq // hkv
     items, merges = hxf.op_decode_plan(B, hq, hkv, ctxs, bt, bt.shape[1] if bt is not None else 0)
     assert merges.shape == (B * hkv, 4)
-    rows_max = min(4, 16 // G)
+    narrow, wide = hxf.decode_rows_narrow(G), hxf.decode_rows_wide(G)
+    n_wide = int(np.sum(items[:, 3] > narrow))
+    assert (items[:len(items) - n_wide, 3] <= narrow).all()      # one-tile items first, then the wide ones
     cover = {}          # (seq, kvh) -> list of (t0, t1)
     slot_owner = {}
     for it in items:
         kvh, t0, t1, n_rows = it[:4]
-        ents, parts = it[4:8], it[8:12]
-        assert 1 <= n_rows <= rows_max and 0 <= t0 < t1
+        ents, parts = it[4:12], it[12:20]
+        assert 1 <= n_rows <= wide and 0 <= t0 < t1
         assert t0 % 16 == 0
         for r in range(n_rows):
             e = int(ents[r])
@@ -63,8 +65,9 @@ def _check(ctxs, hq, hkv, bt=None):
         assert len(ranges) == n_part
         assert all(slot_owner[s] == (e, kvh) for s in range(part0, part0 + n_part))
     assert len(slot_owner) == sum(int(m[3]) for m in merges)
-    lengths = [int(t1 - t0) for t0, t1 in items[:, 1:3]]
-    assert lengths == sorted(lengths, reverse=True)       # longest first
+    for part in (items[:len(items) - n_wide], items[len(items) - n_wide:]):
+        lengths = [int(t1 - t0) for t0, t1 in part[:, 1:3]]
+        assert lengths == sorted(lengths, reverse=True)       # longest first within each kind
     return items, merges
 
 
@@ -87,26 +90,29 @@ def test_plan_fills_but_does_not_exceed_the_resident_wavefronts():
     assert len(items) == 260 * 8
 
 
-def test_plan_shares_fork_prefixes():
+@pytest.mark.parametrize("hq,hkv,per_item", [(32, 8, 8), (40, 8, 6), (64, 8, 4), (16, 8, 8)])
+def test_plan_shares_fork_prefixes(hq, hkv, per_item):
     """Two groups of 8 forks sharing 255 pages (4096-token parents), plus unrelated
-    sequences: the shared pages are read by items of min(4, 16/G) rows."""
+    sequences: the shared pages are read by items of min(8, 32/G) rows (two query tiles
+    when more than 16/G), i.e. once per group of eight forks at G <= 4."""
     rng = np.random.default_rng(4)
     ctxs = [4096 + 16 + int(k) for k in rng.integers(1, 256, 16)] + [3000, 5000]
     bt = _tables(rng, ctxs, groups=[(list(range(8)), 255), (list(range(8, 16)), 255)])
-    items, _ = _check(ctxs, 32, 8, bt)
+    items, _ = _check(ctxs, hq, hkv, bt)
     shared = items[items[:, 3] > 1]
-    assert len(shared) > 0 and (shared[:, 3] == 4).all()
+    assert len(shared) > 0 and shared[:, 3].max() == per_item
     assert (shared[:, 2] <= 255 * 16).all()
     # every fork reads the 4080 shared tokens through shared items only
     tok = {}
     for it in shared:
         for r in range(it[3]):
             tok[int(it[4 + r]), int(it[0])] = tok.get((int(it[4 + r]), int(it[0])), 0) + int(it[2] - it[1])
-    assert all(tok[(e, h)] == 255 * 16 for e in range(16) for h in range(8))
+    assert all(tok[(e, h)] == 255 * 16 for e in range(16) for h in range(hkv))
     # the (token, kv-head) pairs read drop by the sharing factor on the shared part
     read = int((items[:, 2] - items[:, 1]).sum())
-    logical = sum(ctxs) * 8
-    assert read == logical - 16 * 8 * 4080 + 4 * 8 * 4080
+    logical = sum(ctxs) * hkv
+    items_per_group = -(-8 // per_item)
+    assert read == logical - 16 * hkv * 4080 + 2 * items_per_group * hkv * 4080
 
 
 def test_plan_groups_need_a_common_full_page():
@@ -123,3 +129,20 @@ def test_plan_groups_need_a_common_full_page():
     bt = _tables(rng, ctxs, groups=[([0, 1], 1)])
     items, _ = _check(ctxs, 32, 8, bt)
     assert (items[:, 3] == 1).all()
+
+
+def test_plans_reused_across_iterations_carry_nothing_over(tmp_path):
+    """The executor plans every iteration into the same plan objects: after an
+    iteration with two-tile fork items, an iteration with no decoding sequence must
+    report no items of either kind (a stale two-tile count sent the wide kernel to
+    items before the start of an empty list).  Host code only, built with g++."""
+    import os
+    import subprocess
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    csrc = os.path.join(root, "paper_2505_05286_amd", "csrc")
+    exe = str(tmp_path / "plan_reuse")
+    subprocess.run(["g++", "-std=c++17", "-O1", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", "-I" + csrc,
+                    os.path.join(root, "tests", "plan_reuse.cpp"), os.path.join(csrc, "decode_plan.cpp"), "-o", exe],
+                   check=True, capture_output=True, timeout=300)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout + r.stderr

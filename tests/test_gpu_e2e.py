@@ -276,6 +276,37 @@ def test_graph_replays_match_eager_steps(name, layers, monkeypatch):
     log(f"{name}: {n_decode_steps} decode-only steps, graph replays bit-identical to eager launches")
 
 
+def test_prefill_only_iteration_after_two_tile_fork_decode():
+    """Regression: six forks of one parent (Hq/Hkv = 4, so their shared pages go to
+    two-tile items) decode together, then a new request's prompt runs in an iteration
+    with no decoding sequence.  The decode work list of that iteration must be empty
+    (the executor reuses one plan object across iterations), and the new request's
+    tokens are the oracle's."""
+    shape, dm, w = device_model("llama8b", 2)
+    rng = np.random.default_rng(43)
+    eng = Engine(dm, max_context=1024, n_blocks=200, max_seqs=8, chunk_tokens=256, cost_ps=COST, iter_ps=ITER)
+    prompt = rng.integers(0, shape.vocab, 100)
+    par = eng.inst.submit(0, 0, 0, 0, 10 ** 7, prompt, 1, retain=True)
+    now = 0
+    while eng.inst.step(now)[0] != hxf.IDLE:
+        now += 1000
+    kids = [eng.inst.submit(now, 0, 1, 0, 10 ** 7, np.zeros(0, np.int64), 3, parent=par) for _ in range(6)]
+    while eng.inst.step(now)[0] != hxf.IDLE:
+        now += 1000
+    fresh = rng.integers(0, shape.vocab, 40)
+    rid = eng.inst.submit(now, 1, 0, 0, 10 ** 7, fresh, 3)
+    st, _ = eng.inst.step(now)
+    assert st != hxf.IDLE and eng.inst.last_batch()[0] == [rid]     # the prompt alone: no decode rows
+    while eng.inst.step(now)[0] != hxf.IDLE:
+        now += 1000
+    ref, ref_lg = M.generate(w, [fresh.astype(np.int64)], [3])
+    compare_free_running("prefill after two-tile decode", eng.inst.tokens(rid), ref[0], ref_lg[0])
+    full = np.concatenate([prompt, eng.inst.tokens(par)]).astype(np.int64)
+    kref, kref_lg = M.generate(w, [full], [3])
+    for k in kids:
+        compare_free_running("fork", eng.inst.tokens(k), kref[0], kref_lg[0])
+
+
 def test_graph_replays_match_eager_steps_with_forks(monkeypatch):
     """The same comparison for forks of one retained parent decoding together (their
     shared full pages attended by multi-row work items)."""

@@ -345,6 +345,14 @@ def test_prefill_attention_cfg3_full_size():
     _prefill_case([(0, 2048), (6144, 2048)], 32, 8, 128, seed=3)
 
 
+@pytest.mark.parametrize("hq,hkv,dh,chunks", [(32, 8, 128, [(0, 2048)]), (40, 8, 128, [(0, 1500), (0, 300)]),
+                                               (4, 2, 64, [(0, 2048), (16, 33)]), (64, 8, 128, [(0, 1024)])])
+def test_prefill_attention_key_range_splits(hq, hkv, dh, chunks):
+    """A prompt's first chunk alone: the causal items are uneven (1 to 64 key tiles), so
+    the long ones are cut into key ranges whose partials are merged by log-sum-exp."""
+    _prefill_case(chunks, hq, hkv, dh, seed=hq + dh + len(chunks))
+
+
 @pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (40, 8, 128), (64, 8, 128), (8, 1, 128)])
 def test_prefill_attention_chunks(hq, hkv, dh):
     chunks = [(0, 1), (0, 17), (0, 64), (16, 16), (40, 9), (100, 77), (0, 300), (513, 130)]
