@@ -103,7 +103,8 @@ int hxf_op_kv_scatter(const void* k, const void* v, const int32_t* slot, void* k
  * min(8, 32 / (Hq/Hkv)) of them (a second 16-column MFMA tile reuses every K/V read when more
  * than 16 / (Hq/Hkv) rows share an item); the result is the same attention.  Each (sequence, kv-head) stream is
  * split into equal page-aligned partitions (at least 256 tokens, sized so that the work items fill
- * the wavefronts the chip holds at once), merged by log-sum-exp.
+ * the wavefronts the chip holds at once, or, with more streams than those, no longer than an even
+ * share of all the tokens over them), merged by log-sum-exp.
  * workspace: hxf_op_decode_attention_workspace_bytes(...) bytes (same ctx_host, bt_host, bt_stride). */
 int64_t hxf_op_decode_attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t head_dim,
                                                 const int32_t* ctx_host, const int32_t* bt_host, int32_t bt_stride);

@@ -183,15 +183,6 @@ __device__ __forceinline__ void load_q(bf16x8* qf, const uint16_t* qrow, bool ok
     qf[s] = ok ? as_bf16x8(*reinterpret_cast<const uint4*>(qrow + s * 32 + rq * 8)) : as_bf16x8(make_uint4(0, 0, 0, 0));
 }
 
-// Element r of a row array of a decode item, r wavefront-varying (a select chain, no
-// scratch indexing).
-__device__ __forceinline__ int32_t item_row(const int32_t (&v)[kDecodeRows], int r) {
-  int32_t x = v[0];
-#pragma unroll
-  for (int k = 1; k < kDecodeRows; ++k) x = (r == k) ? v[k] : x;
-  return x;
-}
-
 // One wavefront per work item.  NT = 1: the 16 query columns are (row, head of the
 // group) pairs of up to 16/G rows; NT = 2 (wide items of a shared prefix): 32 columns,
 // up to 32/G rows, the second tile reusing every K/V page read for the first.  The
@@ -207,7 +198,10 @@ __global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
     if (w >= (a.n_items_dev ? a.n_items_dev[1] : a.n_wide)) return;
     w += a.n_items_dev ? a.n_items_dev[0] : a.n_items;
   }
-  const DecodeItem it = a.items[w];
+  // the item's scalar fields are wavefront-uniform loads; a lane reads its own row's
+  // entry and partial slot with one vector load each (no private copy of the record)
+  const DecodeItem* it = a.items + w;
+  const int kvh = it->kvh, t0 = it->t0, t1 = it->t1, n_rows = it->n_rows, entry0 = it->entry[0];
   const int G = a.Hq / a.Hkv;
   bf16x8 qf[NT][DH / 32];
   bool ok[NT];
@@ -218,16 +212,16 @@ __global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
     const int col = t * 16 + (lane & 15);
     const int row = col / G;
     g[t] = col - row * G;
-    ok[t] = row < it.n_rows && row < kDecodeRows;
+    ok[t] = row < n_rows && row < kDecodeRows;
     const int r = ok[t] ? row : 0;
-    const int entry = item_row(it.entry, r);
-    part[t] = item_row(it.part, r);
-    const int head = it.kvh * G + (ok[t] ? g[t] : 0);
+    const int entry = it->entry[r];
+    part[t] = it->part[r];
+    const int head = kvh * G + (ok[t] ? g[t] : 0);
     load_q<DH>(qf[t], a.q + (size_t)a.q_row[entry] * a.q_stride + head * DH, ok[t], lane);
   }
   AttnState<DH> S[NT];
-  attn_range<DH, false, NT>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)it.entry[0] * a.bt_stride, a.n_blocks, it.kvh,
-                            it.t0, it.t1, 0x7FFFFFFF, a.scale_log2, lane);
+  attn_range<DH, false, NT>(S, qf, a.k_pool, a.v_pool, a.bt + (size_t)entry0 * a.bt_stride, a.n_blocks, kvh, t0, t1,
+                            0x7FFFFFFF, a.scale_log2, lane);
   const int rq = lane >> 4;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {

@@ -111,18 +111,20 @@ inline void order_decode_items(DecodeItem* it, size_t n) {
   std::stable_sort(it, it + n, [](const DecodeItem& x, const DecodeItem& y) { return x.t1 - x.t0 > y.t1 - y.t0; });
 }
 // Decode work split.  Each (sequence, kv-head) context is cut into equal, page-aligned
-// partitions no longer than a per-launch target, chosen so that the work items fill
-// (without exceeding) the wavefronts the chip holds at once: two per SIMD at the
-// kernel's register count, 2 x 4 x 256.  A partition is never shorter than
-// kDecodeMinPartition tokens unless its whole context is; with as many
-// (sequence, kv-head) pairs as resident wavefronts, each pair is one item.
+// partitions no longer than a per-launch target.  With fewer (stream, kv-head) pairs than
+// the wavefronts the chip holds at once (two per SIMD at the one-tile kernel's register
+// count, 2 x 4 x 256), the target makes the items just fill them.  With more pairs each
+// already has an item, and the target is an even share of all the tokens over the
+// resident wavefronts: a stream much longer than the others (the shared prefix of a fork
+// group next to the forks' short own tails) is cut instead of running alone after the
+// rest have drained.  A partition is never shorter than kDecodeMinPartition tokens
+// unless its whole context is.
 constexpr int kDecodeResident = 2048;
 constexpr int kDecodeMinPartition = 256;
 inline int64_t decode_target_tokens(int64_t sum_ctx, int64_t n_seqs, int64_t hkv) {
   const int64_t pairs = n_seqs * hkv;
-  if (pairs >= kDecodeResident) return int64_t(1) << 40;
-  const int64_t free_waves = kDecodeResident - pairs;
-  return std::max<int64_t>((sum_ctx * hkv + free_waves - 1) / free_waves, kDecodeMinPartition);
+  const int64_t slots = pairs < kDecodeResident ? kDecodeResident - pairs : kDecodeResident;
+  return std::max<int64_t>((sum_ctx * hkv + slots - 1) / slots, kDecodeMinPartition);
 }
 // Partition length (a whole number of pages) for a context of ctx tokens; its
 // ceil(ctx / length) parts number at most ceil(ctx / target).

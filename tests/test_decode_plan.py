@@ -84,10 +84,30 @@ def test_plan_fills_but_does_not_exceed_the_resident_wavefronts():
     ctxs = [int(c) for c in np.clip(rng.lognormal(np.log(3000), 0.5, 64), 1024, 8192)]
     items, _ = _check(ctxs, 32, 8)
     assert 0.8 * RESIDENT <= len(items) <= RESIDENT
-    # at least as many (sequence, kv-head) pairs as resident wavefronts: one item per pair
+    # at least as many (sequence, kv-head) pairs as resident wavefronts: every pair has an
+    # item, and the streams longer than an even share of all tokens are cut to that share
     ctxs = [int(c) for c in rng.integers(1, 5000, 260)]
     items, _ = _check(ctxs, 32, 8)
+    share = max(-(-sum(ctxs) * 8 // RESIDENT), 256)
+    assert 260 * 8 < len(items) <= 260 * 8 + RESIDENT
+    assert (items[:, 2] - items[:, 1]).max() <= -(-share // 16) * 16
+    # uniform lengths: the share is the length itself, one item per pair
+    items, _ = _check([3000] * 260, 32, 8)
     assert len(items) == 260 * 8
+
+
+def test_plan_cuts_a_shared_prefix_longer_than_the_even_share():
+    """32 groups of 8 forks of 4096-token parents (each fork 1-255 tokens past the
+    shared 256 pages): 288 streams x 8 kv-heads exceed the resident wavefronts, yet
+    the shared-prefix streams are cut to the even share instead of one 4096-token item
+    each."""
+    rng = np.random.default_rng(6)
+    ctxs = [4096 + int(k) for k in rng.integers(1, 256, 256)]
+    bt = _tables(rng, ctxs, groups=[(list(range(8 * g, 8 * g + 8)), 256) for g in range(32)])
+    items, _ = _check(ctxs, 32, 8, bt)
+    wide = items[items[:, 3] == 8]
+    share = -(-sum(ctxs) * 8 // RESIDENT)
+    assert len(wide) > 32 * 8 and (wide[:, 2] - wide[:, 1]).max() <= -(-share // 16) * 16
 
 
 @pytest.mark.parametrize("hq,hkv,per_item", [(32, 8, 8), (40, 8, 6), (64, 8, 4), (16, 8, 8)])
