@@ -398,8 +398,10 @@ def workload4():
         # (token, kv-head) pairs of context attended this iteration, per sequence and once per page
         kv["logical"] += info["sum_decode_ctx"]
         kv["unique"] += info["sum_decode_ctx"] - (info["n_decode"] - len(parents)) * shared
-    # the first 8 branch iterations are profiled (eager launches, kernel-stamped attention
-    # events); the rest, which replay a captured graph, are timed
+    # the forks' first iterations re-prefill the parents' partial last pages; once every
+    # fork decodes, 8 iterations are profiled (eager launches, kernel-stamped events) and
+    # the rest, which replay a captured graph, are timed
+    now, it0, _, _, _ = step_until(inst, now, lambda i: i["n_prefill_tokens"] == 0, per_step=count)
     inst.profile_enable(True)
     now, it_p, _, _, _ = step_until(inst, now, lambda i: it_p_count(), per_step=count)
     prof = inst.profile()
@@ -417,14 +419,17 @@ def workload4():
     return {"workload": "4: 8B, 32 shared 4096-token prompts x 8 branches x 256 tokens, 512-token corrections",
             "parent_prefill_tokens_per_s": round(pf1 / dt1, 1),
             "branch_decode_tokens_per_s": round(dec2 / dt2, 1), "branch_iterations_timed": it2,
-            "branch_iterations_profiled": it_p,
+            "branch_iterations_profiled": it_p, "branch_iterations_untimed_tail_prefill": it0,
             "branch_ms_per_iteration": round(dt2 / it2 * 1e3, 3),
-            "branch_kv_gb_per_iteration": {"logical": round(kv["logical"] * per_tok / (it2 + it_p) / 1e9, 2),
-                                           "unique": round(kv["unique"] * per_tok / (it2 + it_p) / 1e9, 2),
+            "branch_kv_gb_per_iteration": {"logical": round(kv["logical"] * per_tok / (it0 + it2 + it_p) / 1e9, 2),
+                                           "unique": round(kv["unique"] * per_tok / (it0 + it2 + it_p) / 1e9, 2),
                                            "read": round(prof["decode_attn_bytes"] / dec_p / 1e9, 2)},
             "branch_attention_ms_per_iteration": round(prof["decode_attn_ms"] / dec_p, 3),
             "branch_attention_read_tb_per_s": round(prof["decode_attn_bytes"] / (prof["decode_attn_ms"] * 1e-3) / 1e12,
                                                     3),
+            "branch_gemm_ms_per_iteration": {k: round(prof["gemm_ms"][k] / it_p, 3) for k in prof["gemm_ms"]},
+            "branch_gemm_tflops": {k: round(prof["gemm_flops"][k] / max(prof["gemm_ms"][k], 1e-9) / 1e9, 1)
+                                   for k in prof["gemm_ms"]},
             "correction_prefill_tokens_per_s": round(pf3 / dt3, 1)}
 
 

@@ -136,10 +136,14 @@ void plan_prefill(const std::vector<PrefillEntry>& entries, int hkv, int qpi, Pr
         whole.push_back(PrefillItem{e.entry, h, q0, nq, 0, t1, -1, 0});
         out.tiles += t1;
       }
-  // the per-slot share of one pass over the resident workgroups
+  // With fewer items than CUs some CUs would idle: items longer than the per-slot share
+  // of one pass over the resident workgroups are cut into key ranges.  With more, they
+  // are not: a CU's two resident workgroups share its matrix cores, so the one left
+  // running a long item runs it faster, and cutting only adds partial writes and a merge.
   const int64_t share = std::max<int64_t>((out.tiles + kPrefillResident - 1) / kPrefillResident, kPrefillMinTiles);
+  const bool split = (int64_t)whole.size() < kPrefillResident / 2;
   for (const PrefillItem& it : whole) {
-    if (it.t1 <= share) {
+    if (!split || it.t1 <= share) {
       out.items.push_back(it);
       continue;
     }
@@ -157,7 +161,13 @@ void plan_prefill(const std::vector<PrefillEntry>& entries, int hkv, int qpi, Pr
     out.n_parts += k;
     out.merges.push_back(PrefillMerge{it.entry, it.kvh, it.q0, it.nq, part0, k, 0, 0});
   }
+  // Most tiles first; then, among the first resident workgroups, the second half in
+  // reverse: workgroups w and w + kPrefillResident / 2 are placed on one CU, which so
+  // gets one long and one short item (the causal items of a first chunk hold 1 to 64
+  // tiles) instead of two long or two short ones.
   order_prefill_items(out.items.data(), out.items.size());
+  const size_t half = kPrefillResident / 2, window = std::min<size_t>(out.items.size(), kPrefillResident);
+  if (window > half) std::reverse(out.items.begin() + half, out.items.begin() + window);
 }
 
 }  // namespace hxf

@@ -38,10 +38,11 @@ struct DecodePlan {
 void plan_decode(const std::vector<DecodeSeq>& seqs, int hkv, int G, DecodePlan& out);
 
 // Chunked-prefill work list.  Each (prefill entry, kv-head, block of qpi queries) is
-// one item over the key tiles its queries see; when the tiles of all items exceed
-// what the resident workgroups take in one pass, an item longer than the per-slot
-// share (at least kPrefillMinTiles) is cut into equal key ranges whose partials a
-// merge job combines.  Items are launched most tiles first.
+// one item over the key tiles its queries see.  With fewer items than CUs, an item
+// longer than the per-slot share of one pass over the resident workgroups (at least
+// kPrefillMinTiles) is cut into equal key ranges whose partials a merge job combines.
+// Items are launched most tiles first, the long and short ones of the first pass
+// paired on the CUs.
 struct PrefillEntry {
   int entry, pos0, n;   // batch entry, position of its first query, queries
 };

@@ -561,45 +561,65 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   }
 }
 
-// Log-sum-exp merge of the key-range parts of split prefill items: one workgroup per
-// (merge job, 64 pairs), four lanes per pair, each lane DH/4 dims.
+// Log-sum-exp merge of the key-range parts of split prefill items: DH/8 lanes per
+// (query, head) pair, each lane 8 dims, a job's 128 pairs over DH/16 workgroups.
 template <int DH>
 __global__ __launch_bounds__(256) void prefill_merge_kernel(PrefillAttnArgs a) {
-  const int job = blockIdx.x >> 1;
+  // TPP threads per (query, head) pair, 8 output dimensions each; the pairs of one job
+  // span BPJ workgroups
+  constexpr int TPP = DH / 8, PPB = 256 / TPP, BPJ = kPrefillPairs / PPB;
+  const int job = blockIdx.x / BPJ;
   const PrefillMerge mg = a.merges[job];
   const int G = a.Hq / a.Hkv;
-  const int p = (blockIdx.x & 1) * 64 + (threadIdx.x >> 2);
+  const int p = (blockIdx.x % BPJ) * PPB + threadIdx.x / TPP;
   if (p >= mg.nq * G) return;
-  constexpr int PER = DH / 4;
-  const int d0 = (threadIdx.x & 3) * PER;
-  float M = -__builtin_huge_valf();
-  for (int j = 0; j < mg.n_part; ++j) M = fmaxf(M, a.part_ml[((size_t)(mg.part0 + j) * kPrefillPairs + p) * 2]);
-  float acc[PER];
+  const int d0 = (threadIdx.x % TPP) * 8;
+  // one pass in groups of four partials whose loads are issued together; the running
+  // maximum is finite from the first group on (partial 0 starts at key 0, which every
+  // query sees), and a partial whose keys are all masked has weight zero
+  float M = -__builtin_huge_valf(), L = 0.f;
+  float acc[8];
 #pragma unroll
-  for (int d = 0; d < PER; ++d) acc[d] = 0.f;
-  float L = 0.f;
-  for (int j = 0; j < mg.n_part; ++j) {
-    const size_t slot = (size_t)(mg.part0 + j) * kPrefillPairs + p;
-    const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + slot * 2);
-    const float wgt = __builtin_amdgcn_exp2f(ml.x - M);
-    L += wgt * ml.y;
-    const float4* po = reinterpret_cast<const float4*>(a.part_o + slot * DH + d0);
+  for (int d = 0; d < 8; ++d) acc[d] = 0.f;
+  for (int j0 = 0; j0 < mg.n_part; j0 += 4) {
+    float2 ml[4];
+    float4 v[4][2];
 #pragma unroll
-    for (int d = 0; d < PER / 4; ++d) {
-      const float4 v = po[d];
-      acc[4 * d] += wgt * v.x;
-      acc[4 * d + 1] += wgt * v.y;
-      acc[4 * d + 2] += wgt * v.z;
-      acc[4 * d + 3] += wgt * v.w;
+    for (int u = 0; u < 4; ++u) {
+      const size_t slot = (size_t)(mg.part0 + min(j0 + u, mg.n_part - 1)) * kPrefillPairs + p;
+      ml[u] = *reinterpret_cast<const float2*>(a.part_ml + slot * 2);
+      const float4* po = reinterpret_cast<const float4*>(a.part_o + slot * DH + d0);
+      v[u][0] = po[0];
+      v[u][1] = po[1];
+    }
+    float mx = M;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (j0 + u < mg.n_part) mx = fmaxf(mx, ml[u].x);
+    const float sc = __builtin_amdgcn_exp2f(M - mx);
+    M = mx;
+    L *= sc;
+#pragma unroll
+    for (int d = 0; d < 8; ++d) acc[d] *= sc;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float w = j0 + u < mg.n_part ? __builtin_amdgcn_exp2f(ml[u].x - M) : 0.f;
+      L += w * ml[u].y;
+      acc[0] += w * v[u][0].x;
+      acc[1] += w * v[u][0].y;
+      acc[2] += w * v[u][0].z;
+      acc[3] += w * v[u][0].w;
+      acc[4] += w * v[u][1].x;
+      acc[5] += w * v[u][1].y;
+      acc[6] += w * v[u][1].z;
+      acc[7] += w * v[u][1].w;
     }
   }
   const float inv = 1.f / L;
   const int qi = p / G, hj = p % G;
   uint16_t* out = a.out + (size_t)(a.row0[mg.entry] + mg.q0 + qi) * a.out_stride + (mg.kvh * G + hj) * DH + d0;
-#pragma unroll
-  for (int d = 0; d < PER / 4; ++d)
-    *reinterpret_cast<uint2*>(out + 4 * d) = make_uint2(pack_bf2(acc[4 * d] * inv, acc[4 * d + 1] * inv),
-                                                       pack_bf2(acc[4 * d + 2] * inv, acc[4 * d + 3] * inv));
+  *reinterpret_cast<uint4*>(out) = make_uint4(pack_bf2(acc[0] * inv, acc[1] * inv), pack_bf2(acc[2] * inv, acc[3] * inv),
+                                              pack_bf2(acc[4] * inv, acc[5] * inv), pack_bf2(acc[6] * inv, acc[7] * inv));
 }
 
 }  // namespace
@@ -659,8 +679,10 @@ hipError_t prefill_attn_launch(const PrefillAttnArgs& a, hipStream_t st, hipEven
   hipError_t e = a.dh == 128 ? go(prefill_flash_kernel<128, kPrefillPT>, dim3(a.n_items), ev_start, e1)
                              : go(prefill_flash_kernel<64, kPrefillPT>, dim3(a.n_items), ev_start, e1);
   if (e != hipSuccess || a.n_merges <= 0) return e;
-  return a.dh == 128 ? go(prefill_merge_kernel<128>, dim3(2 * a.n_merges), nullptr, ev_stop)
-                     : go(prefill_merge_kernel<64>, dim3(2 * a.n_merges), nullptr, ev_stop);
+  // workgroups per merge job: 128 pairs x dh / 8 threads over 256-thread workgroups
+  const unsigned grid = (unsigned)a.n_merges * (kPrefillPairs * (a.dh / 8) / 256);
+  return a.dh == 128 ? go(prefill_merge_kernel<128>, dim3(grid), nullptr, ev_stop)
+                     : go(prefill_merge_kernel<64>, dim3(grid), nullptr, ev_stop);
 }
 
 }  // namespace hxf

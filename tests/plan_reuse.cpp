@@ -1,8 +1,14 @@
-// Host-only check of the attention work lists' reuse contract: the executor plans
-// every iteration into the same DecodePlan / PrefillPlan objects, so a plan must
-// carry nothing over from the previous iteration.  Built with the host compiler
-// against decode_plan.cpp (no device code); prints "ok" or the first violation.
+// Host-only checks of the attention work lists: the executor plans every iteration
+// into the same DecodePlan / PrefillPlan objects, so a plan must carry nothing over
+// from the previous iteration; a prefill plan covers every (entry, kv-head, query
+// block) with one item over all its key tiles or with contiguous key ranges whose
+// partial slots one merge job names.  Built with the host compiler against
+// decode_plan.cpp (no device code); prints "ok" or the first violation.
+#include <algorithm>
 #include <cstdio>
+#include <map>
+#include <set>
+#include <tuple>
 #include <vector>
 
 #include "decode_plan.hpp"
@@ -26,6 +32,47 @@ static int check(const DecodePlan& P, int G, int64_t expect_rows, int it) {
       return fail("one-tile items do not precede the wide ones", it);
   for (const MergeItem& m : P.merges) rows += m.kvh == 0;
   if (rows != expect_rows) return fail("merge jobs from another iteration", it);
+  return 0;
+}
+
+// every query block's key tiles [0, ceil((pos0 + q0 + nq) / 32)) exactly once
+static int check_prefill(const std::vector<PrefillEntry>& E, int hkv, int qpi, int it) {
+  PrefillPlan P;
+  plan_prefill(E, hkv, qpi, P);
+  using Key = std::tuple<int, int, int>;
+  std::map<Key, std::vector<std::pair<int, int>>> cover;   // (entry, kvh, q0) -> key-tile ranges
+  std::map<Key, int> whole_items;
+  std::set<int> parts;
+  int64_t n_whole = 0;
+  for (const PrefillEntry& e : E) n_whole += (int64_t)hkv * ((e.n + qpi - 1) / qpi);
+  for (const PrefillItem& x : P.items) {
+    if (x.t0 < 0 || x.t1 <= x.t0 || x.nq < 1 || x.nq > qpi) return fail("bad prefill item", it);
+    cover[Key{x.entry, x.kvh, x.q0}].push_back({x.t0, x.t1});
+    if (x.part < 0) {
+      ++whole_items[Key{x.entry, x.kvh, x.q0}];
+    } else if (!parts.insert(x.part).second || x.part >= P.n_parts) {
+      return fail("a partial slot used twice or out of range", it);
+    }
+  }
+  if (!P.merges.empty() && n_whole >= kPrefillResident / 2) return fail("items split with one per CU", it);
+  for (const PrefillMerge& m : P.merges) {
+    for (int k = 0; k < m.n_part; ++k)
+      if (!parts.count(m.part0 + k)) return fail("a merge names a slot no item writes", it);
+    if (whole_items.count(Key{m.entry, m.kvh, m.q0})) return fail("a merged block also has a whole item", it);
+  }
+  for (const PrefillEntry& e : E)
+    for (int h = 0; h < hkv; ++h)
+      for (int q0 = 0; q0 < e.n; q0 += qpi) {
+        auto r = cover[Key{e.entry, h, q0}];
+        std::sort(r.begin(), r.end());
+        const int nq = std::min(qpi, e.n - q0), t1 = (e.pos0 + q0 + nq + 31) / 32;
+        int at = 0;
+        for (auto& [a, b] : r) {
+          if (a != at) return fail("key tiles missed or attended twice", it);
+          at = b;
+        }
+        if (at != t1) return fail("key tiles missed at the end", it);
+      }
   return 0;
 }
 
@@ -58,10 +105,17 @@ int main() {
   if (P.n_wide != 0) return fail("a lone sequence kept two-tile items", 3);
 
   PrefillPlan Q;
-  plan_prefill({PrefillEntry{0, 4096, 2048}}, hkv, 32, Q);
-  if (Q.merges.empty()) return fail("a 6144-token chunk was not split", 4);
+  plan_prefill({PrefillEntry{0, 4080, 16}}, hkv, 32, Q);      // 8 items of 128 key tiles
+  if (Q.merges.size() != 8) return fail("a 16-query chunk at 4080 was not split", 4);
   plan_prefill({}, hkv, 32, Q);
   if (!Q.items.empty() || !Q.merges.empty() || Q.n_parts || Q.tiles) return fail("an empty prefill plan kept work", 5);
+  const std::vector<std::vector<PrefillEntry>> cases = {
+      {{0, 0, 2048}}, {{0, 6144, 2048}}, {{0, 4352, 512}}, {{0, 4080, 16}},
+      {{0, 0, 300}, {1, 2000, 40}, {2, 17, 1}}, {{0, 0, 1}}, {{3, 100, 77}, {5, 513, 130}}};
+  int k = 6;
+  for (const auto& c : cases)
+    for (int qpi : {16, 25, 32, 64})
+      if (check_prefill(c, hkv, qpi, k++)) return 1;
   std::printf("ok\n");
   return 0;
 }

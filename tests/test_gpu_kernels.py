@@ -345,11 +345,13 @@ def test_prefill_attention_cfg3_full_size():
     _prefill_case([(0, 2048), (6144, 2048)], 32, 8, 128, seed=3)
 
 
-@pytest.mark.parametrize("hq,hkv,dh,chunks", [(32, 8, 128, [(0, 2048)]), (40, 8, 128, [(0, 1500), (0, 300)]),
-                                               (4, 2, 64, [(0, 2048), (16, 33)]), (64, 8, 128, [(0, 1024)])])
+@pytest.mark.parametrize("hq,hkv,dh,chunks", [(32, 8, 128, [(4352, 512)]), (32, 8, 128, [(4080, 16)]),
+                                               (40, 8, 128, [(0, 300), (2000, 40)]),
+                                               (4, 2, 64, [(0, 2048), (16, 33)]), (64, 8, 128, [(3000, 200)])])
 def test_prefill_attention_key_range_splits(hq, hkv, dh, chunks):
-    """A prompt's first chunk alone: the causal items are uneven (1 to 64 key tiles), so
-    the long ones are cut into key ranges whose partials are merged by log-sum-exp."""
+    """Chunks with fewer work items than CUs (a short chunk deep into a prompt, a fork's
+    re-prefilled partial page): the items are cut into key ranges whose partials are
+    merged by log-sum-exp, up to ~20 parts per item (merged four at a time)."""
     _prefill_case(chunks, hq, hkv, dh, seed=hq + dh + len(chunks))
 
 
