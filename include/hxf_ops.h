@@ -42,7 +42,7 @@ enum { HXF_EPI_BF16 = 0, HXF_EPI_RESID = 1, HXF_EPI_SWIGLU = 2, HXF_EPI_F32 = 3 
  *                   C[:, f] = bf16(silu(gate_f) * up_f), silu(z) = z / (1 + e^-z)
  *   HXF_EPI_F32:    C fp32 [M, ldc]            C = acc
  * K % 8 == 0, lda >= K.  workspace: hxf_op_gemm_workspace_bytes(M, N, K) bytes
- * (split-K partials for small M; may be 0 bytes).  */
+ * (split-K partials for M <= 512, enough for every epilogue; may be 0 bytes).  */
 int64_t hxf_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
 int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void* C, int32_t ldc, int32_t M, int32_t N,
                 int32_t K, int32_t epilogue, void* workspace, int64_t workspace_bytes, void* stream);

@@ -80,12 +80,13 @@ WsPlan plan_workspace(const hxf_model_cfg& m, const hxf_sched_cfg& s) {
                              words(p.merges_max * 4) + words(p.pf_items_max * (int64_t)(sizeof(PrefillItem) / 4)) +
                              words(p.pf_merges_max * (int64_t)(sizeof(PrefillMerge) / 4));
   p.meta_bytes = meta_words * 4;
-  // split-K partials: largest splits*M*N over the GEMM shapes at M <= 256
+  // split-K partials: largest splits*M*N over the GEMM shapes at M <= 512 (no plan
+  // splits K above 512 rows)
   int64_t part = 0;
-  const int64_t shapes[5][2] = {{qkv, d}, {d, hq * dh}, {2 * f, d}, {d, f}, {m.vocab, d}};
-  for (int64_t M = 1; M <= std::min<int64_t>(256, p.t_max); ++M)
+  const int64_t shapes[5][3] = {{qkv, d, 0}, {d, hq * dh, 0}, {2 * f, d, 1}, {d, f, 0}, {m.vocab, d, 0}};
+  for (int64_t M = 1; M <= std::min<int64_t>(512, p.t_max); ++M)
     for (auto& sh : shapes) {
-      GemmPlan g = gemm_plan((int)M, (int)sh[0], (int)sh[1], kMaxSplits);
+      GemmPlan g = gemm_plan((int)M, (int)sh[0], (int)sh[1], kMaxSplits, sh[2] != 0);
       if (g.splits > 1) part = std::max(part, (int64_t)g.splits * M * sh[0] * 4);
     }
   int64_t o = 0;

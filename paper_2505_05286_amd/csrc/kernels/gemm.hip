@@ -1,12 +1,15 @@
 // bf16 "NT" GEMMs on CDNA4 matrix cores: C[M,N] = A[M,K] * B[N,K]^T with an
 // fp32 accumulator and fused epilogues (bf16 store, fp32 residual add, SwiGLU
 // gate*up, fp32 store) or fp32 split-K partials.  A is row-major activations, B
-// the packed weights (see below).  Three kernels by M:
-//   M <= 64      gemm_stream_kernel: weight streaming through LDS DMA, split K;
-//   64 < M <= 512 gemm_nt_kernel: 64x64 / 128x128 tiles of 16x16x32 MFMAs, K
-//                staged through LDS from registers, split K for M <= 256;
-//   M > 512      gemm_big_kernel: macro tiles of up to 256 x 256 on 32x32x16 MFMAs fed
-//                by LDS DMA, four or eight wavefronts, tile shape chosen per GEMM.
+// the packed weights (see below).  Three kernels (gemm_plan picks):
+//   gemm_stream_kernel: weight streaming through LDS DMA on 16x16x32 MFMAs, split K;
+//     M <= 128;
+//   gemm_big_kernel: macro tiles of up to 256 x 256 on 32x32x16 MFMAs fed by LDS DMA,
+//     four or eight wavefronts, tile shape chosen per GEMM; M > 512, outputs of
+//     N >= 16384 above 64 rows, SwiGLU above 128 rows, and 128 < M <= 512 with split
+//     K otherwise;
+//   gemm_nt_kernel: 128x128 tiles of 16x16x32 MFMAs, K staged through LDS from
+//     registers; SwiGLU whose N is not a multiple of 64 on the big kernel's shapes.
 // Workgroups are renumbered so that consecutive output tiles (which share a
 // weight slice) land on the same XCD and its L2.
 #include <hip/hip_ext.h>
@@ -447,8 +450,10 @@ hipError_t launch_stream(const GemmArgs& a, int S, hipStream_t st, bool reduce, 
 // MFMAs while the other waits on LDS.  BM is any multiple of 32 so that the
 // row tiles can match the batch (2080 rows = 13 x 160).  SwiGLU groups logical
 // columns by 64 (32 gate rows, then the 32 matching up rows) so one lane holds
-// both; it needs BN/WN a multiple of 64.
-template <int BM, int BN, int WM, int WN, int NSTG, int EPI>
+// both; it needs BN/WN a multiple of 64.  SPLIT: grid.y splits K into chunks of
+// k_chunk (a multiple of 32) and each writes its fp32 partial [M][N] to slot
+// blockIdx.y of a.partial, summed by the consumer (not with SwiGLU).
+template <int BM, int BN, int WM, int WN, int NSTG, int EPI, bool SPLIT>
 __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
   constexpr int W = WM * WN;
   constexpr int TM = BM / WM / 32, TN = BN / WN / 32;
@@ -458,6 +463,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
   constexpr int STAGE = NBLK * 512;
   constexpr bool SW = (EPI == EPI_SWIGLU);
   static_assert(!SW || TN % 2 == 0, "SwiGLU pairs 32-column tiles");
+  static_assert(!(SW && SPLIT), "split partials hold logical columns; SwiGLU needs both halves summed first");
   static_assert(NSTG >= 3 && NSTG <= 5 && NSTG * STAGE * 2 <= 160 * 1024, "stage layout");
   __shared__ __attribute__((aligned(1024))) bf16_t L0[STAGE], L1[STAGE], L2[STAGE], L3[NSTG > 3 ? STAGE : 8],
       L4[NSTG > 4 ? STAGE : 8];
@@ -473,7 +479,9 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
   const int m0 = tm * BM, n0 = tn * BN;
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w / WN, wn = w % WN;
-  const int nst = (a.K + 31) / 32;
+  const int kb = SPLIT ? blockIdx.y * a.k_chunk : 0;
+  const int ke = SPLIT ? min(a.K, kb + a.k_chunk) : a.K;
+  const int nst = (ke - kb + 31) / 32;
 
   // This wavefront's DMA blocks w*PER_W + u: an A block (16 activation rows, the
   // lane's row and 8-column chunk) or a packed weight tile (1 KB contiguous).  No
@@ -505,10 +513,10 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
   // A past K: the last 16-byte chunk of the row is read again (its weights are zero)
   const int a_last = a.K - 8 - (lane >> 4) * 8;
   auto issue = [&](int s, bf16_t* base) {
-    const int st = min(s, nst - 1);   // past the end: reload the last stage (unused)
+    const int k0 = kb + min(s, nst - 1) * 32;   // past the end: reload the last stage (unused)
 #pragma unroll
     for (int u = 0; u < PER_W; ++u) {
-      const int off = step[u] == 32 ? min(st * 32, a_last) : st * 512;
+      const int off = step[u] == 32 ? min(k0, a_last) : (k0 >> 5) * 512;
       dma16(src[u] + off, base + dst[u]);
     }
   };
@@ -576,6 +584,22 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
   // lane holds column l % 32 and rows 8*(r/4) + 4*(lane/32) + r%4 of each 32x32 tile
   const int l32 = lane & 31, rq = (lane >> 5) * 4;
   const int wr0 = m0 + wm * (BM / WM), wc0 = n0 + wn * (BN / WN);
+  if (SPLIT) {
+    float* P = a.partial + (size_t)blockIdx.y * a.M * a.N;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = wr0 + i * 32 + (r >> 2) * 8 + rq + (r & 3);
+        if (row >= a.M) continue;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int col = wc0 + j * 32 + l32;
+          if (col < a.N) P[(size_t)row * a.N + col] = acc[i][j][r];
+        }
+      }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     if (EPI == EPI_RESID) {
@@ -645,29 +669,45 @@ struct BigCfg {
 constexpr BigCfg kBig[] = {
     {256, 256, 4, 2, 1.02, true}, {224, 256, 1, 8, 1.10, false}, {192, 256, 2, 4, 1.0, true},
     {160, 256, 1, 8, 1.17, false}, {128, 256, 2, 4, 1.3, true},    {128, 128, 2, 2, 1.6, true},
+    {256, 128, 2, 2, 1.3, true},
 };
 constexpr int kNumBig = sizeof(kBig) / sizeof(kBig[0]);
+constexpr int kNumPrefillBig = 6;   // the shapes chosen among for M > 512
 
 template <int BM, int BN, int WM, int WN, int EPI>
-hipError_t launch_big(const GemmArgs& a, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+hipError_t launch_big(const GemmArgs& a, int S, hipStream_t st, bool reduce, hipEvent_t e0, hipEvent_t e1) {
   constexpr int STAGE_BYTES = (BM + BN) * 64;
   constexpr int NSTG = std::min(5, 160 * 1024 / STAGE_BYTES);
   const int nb = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  return launch_ev(gemm_big_kernel<BM, BN, WM, WN, NSTG, EPI>, dim3(nb), dim3(64 * WM * WN), st, e0, e1, a);
+  if constexpr (EPI != EPI_SWIGLU) {
+    if (S > 1) {
+      if (hipError_t e = launch_ev(gemm_big_kernel<BM, BN, WM, WN, NSTG, EPI, true>, dim3(nb, S), dim3(64 * WM * WN),
+                                   st, e0, reduce ? nullptr : e1, a))
+        return e;
+      if (!reduce) return hipSuccess;
+      const size_t tot = (size_t)a.M * a.N;
+      return launch_ev(splitk_reduce_kernel<EPI>, dim3((tot + 255) / 256), dim3(256), st, nullptr, e1, a, S);
+    }
+  } else {
+    if (S > 1) return hipErrorInvalidValue;
+  }
+  return launch_ev(gemm_big_kernel<BM, BN, WM, WN, NSTG, EPI, false>, dim3(nb), dim3(64 * WM * WN), st, e0, e1, a);
 }
 
 template <int EPI>
-hipError_t launch_big_cfg(const GemmArgs& a, int cfg, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+hipError_t launch_big_cfg(const GemmArgs& a, int cfg, int S, hipStream_t st, bool reduce, hipEvent_t e0,
+                          hipEvent_t e1) {
   switch (cfg) {
-    case 0: return launch_big<256, 256, 4, 2, EPI>(a, st, e0, e1);
-    case 2: return launch_big<192, 256, 2, 4, EPI>(a, st, e0, e1);
-    case 4: return launch_big<128, 256, 2, 4, EPI>(a, st, e0, e1);
-    case 5: return launch_big<128, 128, 2, 2, EPI>(a, st, e0, e1);
+    case 0: return launch_big<256, 256, 4, 2, EPI>(a, S, st, reduce, e0, e1);
+    case 2: return launch_big<192, 256, 2, 4, EPI>(a, S, st, reduce, e0, e1);
+    case 4: return launch_big<128, 256, 2, 4, EPI>(a, S, st, reduce, e0, e1);
+    case 5: return launch_big<128, 128, 2, 2, EPI>(a, S, st, reduce, e0, e1);
+    case 6: return launch_big<256, 128, 2, 2, EPI>(a, S, st, reduce, e0, e1);
     default: break;
   }
   if constexpr (EPI != EPI_SWIGLU) {
-    if (cfg == 1) return launch_big<224, 256, 1, 8, EPI>(a, st, e0, e1);
-    if (cfg == 3) return launch_big<160, 256, 1, 8, EPI>(a, st, e0, e1);
+    if (cfg == 1) return launch_big<224, 256, 1, 8, EPI>(a, S, st, reduce, e0, e1);
+    if (cfg == 3) return launch_big<160, 256, 1, 8, EPI>(a, S, st, reduce, e0, e1);
   }
   return hipErrorInvalidValue;
 }
@@ -691,14 +731,12 @@ hipError_t launch_epi(GemmArgs a, const GemmPlan& p, hipStream_t st, bool reduce
   if (p.stream) {
     if (p.bm <= 32) return launch_stream<2, EPI>(a, p.splits, st, reduce, e0, e1);
     if (p.bm <= 64) return launch_stream<4, EPI>(a, p.splits, st, reduce, e0, e1);
-    if (p.bm <= 128) return launch_stream<8, EPI>(a, p.splits, st, reduce, e0, e1);
-    if constexpr (stream_stages<16>() >= 2) return launch_stream<16, EPI>(a, p.splits, st, reduce, e0, e1);
-    else return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce, e0, e1);
+    return launch_stream<8, EPI>(a, p.splits, st, reduce, e0, e1);
   }
   if (p.big) {
     // SwiGLU on the big kernel pairs 32 gate with 32 up columns: needs F % 32 == 0
     if (EPI == EPI_SWIGLU && a.N % 64 != 0) return launch_tile<128, 128, 64, 2, EPI>(a, 1, st, true, e0, e1);
-    return launch_big_cfg<EPI>(a, p.cfg, st, e0, e1);
+    return launch_big_cfg<EPI>(a, p.cfg, p.splits, st, reduce, e0, e1);
   }
   return launch_tile<128, 128, 64, 2, EPI>(a, p.splits, st, reduce, e0, e1);
 }
@@ -729,16 +767,17 @@ hipError_t pack_weight_launch(const uint16_t* W, int N, int K, uint16_t* out, hi
   return hipGetLastError();
 }
 
-// Kernel, tile and split-K choice.  M <= 256: the weight-streaming kernel, except
+// Kernel, tile and split-K choice.  M <= 128: the weight-streaming kernel, except
 // for wide outputs (N >= 16384) above 64 rows, which take the big-tile kernel as
-// every M > 512 does.  256 < M <= 512: 128x128 tiles of the LDS-staged kernel.
+// every M > 512 and every SwiGLU above 128 rows do.  The other 128 < M <= 512
+// shapes: the big-tile kernel with split K.
 GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu) {
   GemmPlan p;
   // big tiles: the shape minimising whole rounds of one workgroup per CU times tile area
   // times its cost factor (the last round costs as much as a full one)
   auto big = [&]() {
     double best = 0;
-    for (int c = 0; c < kNumBig; ++c) {
+    for (int c = 0; c < kNumPrefillBig; ++c) {
       const BigCfg& g = kBig[c];
       if (swiglu && !g.swiglu) continue;
       const int tiles = ((M + g.bm - 1) / g.bm) * ((N + g.bn - 1) / g.bn);
@@ -755,12 +794,43 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu) {
     p.k_chunk = K;
     return p;
   };
-  if (M > 512 || (M > 64 && M <= 256 && N >= 16384)) return big();
-  if (M <= 256) {
+  // 128 < M <= 512, N < 16384, not SwiGLU: big tiles with K split (fp32 partials the
+  // consumer sums).  Shape and split minimise a per-launch estimate fitted to measured
+  // times on the 8B projections at 128-512 rows: 0.366 us per million tile-area x
+  // K-chunk x cost-factor units (every workgroup of a round runs at once), plus 0.24 us
+  // per MB of partials written and read back.
+  auto mid = [&]() {
+    double best = 0;
+    for (int c : {4, 5, 0, 6}) {
+      const BigCfg& g = kBig[c];
+      const int tiles = ((M + g.bm - 1) / g.bm) * ((N + g.bn - 1) / g.bn);
+      for (int s = 1; s <= max_splits; ++s) {
+        if (s > 1 && (tiles * s > 256 || K / s < 512)) break;
+        const int kc = ((K + s - 1) / s + 31) / 32 * 32;
+        const int splits = (K + kc - 1) / kc;
+        const double rounds = (tiles * splits + 255) / 256;
+        const double t = 0.366e-6 * rounds * g.bm * g.bn * (double)kc * g.f +
+                         (splits > 1 ? 0.24e-6 * splits * (double)M * N * 4 : 0.0);
+        if (best == 0 || t < best - 1e-9) {
+          best = t;
+          p.cfg = c;
+          p.bm = g.bm;
+          p.bn = g.bn;
+          p.k_chunk = kc;
+          p.splits = splits;
+        }
+      }
+    }
+    p.big = true;
+    return p;
+  };
+  if (M > 128 && M <= 512 && N < 16384 && !swiglu) return mid();
+  if (M > 512 || (M > 64 && N >= 16384) || (M > 128 && swiglu)) return big();
+  if (M <= 128) {
     // weight streaming (16 * MT rows): 128 columns per workgroup; K split into the most
     // pieces that keep the grid within one workgroup per CU and >= 512 of K per piece
     p.stream = true;
-    p.bm = M <= 32 ? 32 : M <= 64 ? 64 : M <= 128 ? 128 : 256;
+    p.bm = M <= 32 ? 32 : M <= 64 ? 64 : 128;
     const int tiles = (N + ST_COLS - 1) / ST_COLS;
     int s = 1;
     while (s + 1 <= max_splits && tiles * (s + 1) <= 256 && K / (s + 1) >= 512) ++s;

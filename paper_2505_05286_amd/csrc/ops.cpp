@@ -56,8 +56,13 @@ extern "C" {
 
 int64_t hxf_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
   if (M <= 0 || N <= 0 || K <= 0) return 0;
-  GemmPlan p = gemm_plan(M, N, K, 8);
-  return p.splits > 1 ? (int64_t)p.splits * M * N * 4 : 0;
+  // enough for every epilogue (the SwiGLU plan may differ)
+  int64_t need = 0;
+  for (bool sw : {false, true}) {
+    const GemmPlan p = gemm_plan(M, N, K, 8, sw);
+    if (p.splits > 1) need = std::max(need, (int64_t)p.splits * M * N * 4);
+  }
+  return need;
 }
 
 int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void* C, int32_t ldc, int32_t M, int32_t N,

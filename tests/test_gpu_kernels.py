@@ -65,7 +65,9 @@ def _gemm_case(M_, N, K, epi, seed, rows=None):
                                     (2080, 384, 512), (600, 1000, 688), (2080, 6144, 1024), (1031, 4096, 1384),
                                     (2048, 4096, 256), (2080, 4096, 264), (2048, 6144, 96), (200, 32768, 512),
                                     (96, 20000, 256), (250, 6144, 1024), (2300, 6144, 72), (960, 11008, 72),
-                                    (64, 10240, 8192), (64, 8192, 28672), (2080, 10240, 1024)])
+                                    (64, 10240, 8192), (64, 8192, 28672), (2080, 10240, 1024),
+                                    (256, 6144, 4096), (256, 4096, 14336), (512, 4096, 4096), (129, 4096, 4096),
+                                    (500, 1000, 4096), (384, 6144, 1000), (200, 8192, 2056)])
 @pytest.mark.parametrize("epi", [hxf.EPI_BF16, hxf.EPI_RESID, hxf.EPI_F32])
 def test_gemm(M_, N, K, epi):
     _gemm_case(M_, N, K, epi, seed=M_ * 7 + N + K + epi)
@@ -75,7 +77,8 @@ def test_gemm(M_, N, K, epi):
                                     (20, 2 * 4096, 4096), (64, 2 * 96, 8192), (2080, 2 * 4096, 200),
                                     (300, 2 * 1376, 512), (128, 2 * 14336, 4096), (700, 2 * 688, 256),
                                     (2080, 2 * 2080, 512), (1040, 2 * 5504, 72), (520, 2 * 3584, 72),
-                                    (64, 2 * 28672, 8192), (1024, 2 * 5632, 1000), (2080, 2 * 7168, 1000)])
+                                    (64, 2 * 28672, 8192), (1024, 2 * 5632, 1000), (2080, 2 * 7168, 1000),
+                                    (256, 2 * 14336, 4096), (512, 2 * 14336, 4096), (200, 2 * 1376, 1000)])
 def test_gemm_swiglu(M_, N, K):
     _gemm_case(M_, N, K, hxf.EPI_SWIGLU, seed=M_ + N + K)
 
@@ -94,11 +97,13 @@ def test_gemm_full_size_sampled(name, M_, N, K, epi):
     _gemm_case(M_, N, K, epi, seed=M_ + N + K, rows=rows)
 
 
-def test_gemm_split_repeatable():
-    """Repeated split-K calls on one workspace give bit-identical results."""
+@pytest.mark.parametrize("M_", [64, 256])
+def test_gemm_split_repeatable(M_):
+    """Repeated split-K calls on one workspace give bit-identical results (the weight-
+    streaming kernel at 64 rows, the big-tile kernel at 256)."""
     t = torch()
     rng = np.random.default_rng(77)
-    M_, N, K = 64, 6144, 4096
+    N, K = 6144, 4096
     ab, _ = rand_bf16(rng, (M_, K))
     bb, _ = rand_bf16(rng, (N, K), 0.05)
     A, B = dev_bits(ab), dev_packed(bb)
