@@ -33,11 +33,13 @@ sys.path.insert(0, ROOT)
 
 METRIC = "prefill+decode tokens/s per MI355X at 8B shape; decode-attn HBM % of peak"
 HBM_PEAK_GBS = 8000.0
-# HBM bytes per launch of decode_attn_kernel<128> from hardware counters
-# (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, over `bench.py --attn-kernel-probe`,
-# each scaled by what the counter reads for a 1 GiB copy: 2.000 and 1.000); valid
-# for the kernel as it stands, to be re-measured whenever it changes.
-DECODE_ATTN_TRAFFIC = {"bytes_per_launch": 838_258_660, "algorithmic_bytes_per_launch": 829_956_096,
+# HBM bytes per launch pair of decode_attn_kernel<128> + decode_merge_kernel<128> from
+# hardware counters (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, over
+# `bench.py --attn-kernel-probe`, each scaled by what the counter reads for a 1 GiB
+# copy: 2.000 and 1.000); valid for the kernels as they stand, to be re-measured
+# whenever they change.
+DECODE_ATTN_TRAFFIC = {"bytes_per_launch": 842_801_290, "algorithmic_bytes_per_launch": 829_956_096,
+                       "attention_bytes": 838_459_399, "merge_bytes": 4_341_892,
                        "sample": "attention probe, 64 contexts of the benchmark, 202626 tokens"}
 BATCH = 64
 MAX_NEW = 1000
@@ -773,6 +775,31 @@ def hbm_copy_probe(nbytes=4 << 30, reps=5):
             "note": "a copy reads and writes HBM at once; a read-only stream, like the decode attention's, runs faster"}
 
 
+def hbm_read_probe(nbytes=8 << 30, reps=5):
+    """Achievable HBM read bandwidth for context: the library's streaming-read kernel
+    (16-byte loads, four in flight per thread, 4096 workgroups) over an 8 GiB buffer,
+    bytes read per second (best of `reps`)."""
+    import torch
+    from paper_2505_05286_amd import hxf
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda:0")
+    sink = torch.empty(hxf.READ_SINK_WORDS, dtype=torch.int32, device="cuda:0")
+    st = torch.cuda.current_stream().cuda_stream
+    hxf.op_read(src.data_ptr(), nbytes, sink.data_ptr(), st)
+    best = None
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        hxf.op_read(src.data_ptr(), nbytes, sink.data_ptr(), st)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    del src, sink
+    gbs = nbytes / (best * 1e-3) / 1e9
+    return {"kernel": "read_kernel (hxf_op_read)", "bytes_read": nbytes, "ms": round(best, 3),
+            "gb_per_s": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
+
+
 def gemm_probe(reps=3, M=2080):
     """Only the four prefill projections of the 8B shape at 2080 rows (a 2048-token chunk
     plus 32 decodes), `reps` times each, through the library's GEMM entry point with
@@ -1050,6 +1077,7 @@ def main():
         us = prof["gemm_ms"][k] / n * 1e3
         out["decode_gemms"][k] = {"avg_us": round(us, 2), "weight_tb_s": round(2 * nbytes / (us * 1e-6) / 1e12, 3)}
     out["hbm_copy_probe"] = hbm_copy_probe()
+    out["hbm_read_probe"] = hbm_read_probe()
     del eng, inst
     if not args.no_gemm_roofline:
         progress("workload-3 mixed iterations, profiled: MFMA roofline of the 2080-row projections")

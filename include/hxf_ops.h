@@ -137,6 +137,14 @@ int hxf_op_argmax(const float* logits, int32_t* out, int32_t R, int32_t V, void*
 /* dst = src, bytes % 16 == 0 (HBM bandwidth probe). */
 int hxf_op_copy(const void* src, void* dst, int64_t bytes, void* stream);
 
+/* HBM read-bandwidth probe: reads src (bytes % 16 == 0) once with 16-byte loads and
+ * writes to sink (device, HXF_READ_SINK_WORDS uint32 words, caller-owned) one word per
+ * thread of the launch, the XOR of the 32-bit words that thread read; words of sink
+ * past the launch's threads are left as they are, so the XOR of the whole sink, zeroed
+ * first, is the XOR of every 32-bit word of src. */
+#define HXF_READ_SINK_WORDS (4096 * 256)
+int hxf_op_read(const void* src, int64_t bytes, uint32_t* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

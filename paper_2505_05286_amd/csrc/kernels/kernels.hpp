@@ -223,5 +223,9 @@ int prefill_queries_per_item(int group);
 hipError_t argmax_launch(const float* logits, int32_t* out, int R, int V, hipStream_t st);
 // dst = src (bytes % 16 == 0); HBM bandwidth probe.
 hipError_t copy_launch(const void* src, void* dst, size_t bytes, hipStream_t st);
+// Read-bandwidth probe: at most kReadProbeBlocks workgroups of 256 threads; thread t of
+// the launch writes sink[t] (the XOR of the words it read), the rest of sink is untouched.
+constexpr int kReadProbeBlocks = 4096;
+hipError_t read_launch(const void* src, size_t bytes, uint32_t* sink, hipStream_t st);
 
 }  // namespace hxf

@@ -55,6 +55,21 @@ __global__ __launch_bounds__(256) void copy_kernel(const uint4* src, uint4* dst,
   for (; i < n; i += stride) dst[i] = src[i];
 }
 
+// Streaming read: thread t XORs the 16-byte words it reads (grid-stride, four loads in
+// flight per step) into sink[t], so that no load is dead.
+__global__ __launch_bounds__(256) void read_kernel(const uint4* src, size_t n, uint32_t* sink) {
+  uint32_t acc = 0;
+  const size_t stride = (size_t)gridDim.x * 1024;
+  for (size_t i = (size_t)blockIdx.x * 1024 + threadIdx.x; i < n; i += stride) {
+    uint4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = i + u * 256 < n ? src[i + u * 256] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  sink[(size_t)blockIdx.x * 256 + threadIdx.x] = acc;
+}
+
 }  // namespace
 
 hipError_t argmax_launch(const float* logits, int32_t* out, int R, int V, hipStream_t st) {
@@ -70,6 +85,16 @@ hipError_t copy_launch(const void* src, void* dst, size_t bytes, hipStream_t st)
   if (blocks > 256 * 64) blocks = 256 * 64;
   hipLaunchKernelGGL(copy_kernel, dim3((unsigned)blocks), dim3(256), 0, st, reinterpret_cast<const uint4*>(src),
                      reinterpret_cast<uint4*>(dst), n);
+  return hipGetLastError();
+}
+
+hipError_t read_launch(const void* src, size_t bytes, uint32_t* sink, hipStream_t st) {
+  const size_t n = bytes / 16;
+  size_t blocks = (n + 1023) / 1024;
+  if (blocks > kReadProbeBlocks) blocks = kReadProbeBlocks;
+  if (blocks == 0) blocks = 1;   // no words: every sink word is written as 0
+  hipLaunchKernelGGL(read_kernel, dim3((unsigned)blocks), dim3(256), 0, st, reinterpret_cast<const uint4*>(src), n,
+                     sink);
   return hipGetLastError();
 }
 

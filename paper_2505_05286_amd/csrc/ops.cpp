@@ -314,4 +314,10 @@ int hxf_op_copy(const void* src, void* dst, int64_t bytes, void* stream) {
   return dev_rc(copy_launch(src, dst, (size_t)bytes, (hipStream_t)stream));
 }
 
+int hxf_op_read(const void* src, int64_t bytes, uint32_t* sink, void* stream) {
+  static_assert(HXF_READ_SINK_WORDS == kReadProbeBlocks * 256, "sink size");
+  if (!src || !sink || bytes < 0 || bytes % 16) return HXF_EINVAL;
+  return dev_rc(read_launch(src, (size_t)bytes, sink, (hipStream_t)stream));
+}
+
 }  // extern "C"

@@ -166,6 +166,7 @@ _SIGS = {
                                            C.c_int64, C.c_void_p]),
     "hxf_op_argmax": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p]),
     "hxf_op_copy": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p]),
+    "hxf_op_read": (C.c_int, [C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p]),
 }
 
 EXPORTED = tuple(_SIGS)
@@ -508,3 +509,11 @@ def op_argmax(logits, out, R, V, stream=0):
 
 def op_copy(src, dst, nbytes, stream=0):
     _op(lib().hxf_op_copy(src, dst, nbytes, stream or None), "hxf_op_copy")
+
+
+READ_SINK_WORDS = 4096 * 256
+
+
+def op_read(src, nbytes, sink, stream=0):
+    """HBM read probe: sink (READ_SINK_WORDS uint32) gets one XOR word per thread."""
+    _op(lib().hxf_op_read(src, nbytes, sink, stream or None), "hxf_op_read")

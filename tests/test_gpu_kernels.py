@@ -391,6 +391,23 @@ def test_copy_probe():
     assert t.equal(a, b)
 
 
+@pytest.mark.parametrize("nbytes", [0, 16, 4096 + 48, 64 << 20])
+def test_read_probe(nbytes):
+    """Every 32-bit word of src is read exactly once: the XOR over the (zeroed) sink is
+    the XOR of all words, which a dropped or repeated load would change."""
+    t = torch()
+    rng = np.random.default_rng(nbytes % 1000)
+    words = rng.integers(0, 2 ** 32, nbytes // 4, dtype=np.uint64).astype(np.uint32)
+    src = t.from_numpy(words.view(np.int32).copy()).to("cuda:0") if nbytes else t.zeros(4, dtype=t.int32,
+                                                                                         device="cuda:0")
+    sink = t.zeros(hxf.READ_SINK_WORDS, dtype=t.int32, device="cuda:0")
+    hxf.op_read(src.data_ptr(), nbytes, sink.data_ptr())
+    t.cuda.synchronize()
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    want = np.bitwise_xor.reduce(words) if nbytes else np.uint32(0)
+    assert got == want
+
+
 @pytest.mark.parametrize("N,K", [(37, 72), (64, 4096), (1, 8), (200, 136)])
 def test_pack_weight_layout(N, K):
     """The packed weight layout is the row-major matrix, zero padded to 16 x 32
