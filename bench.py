@@ -618,7 +618,9 @@ def policy_ablation(n_wf=300):
             st = d.stats()
             rnd = lambda v: None if v is None else round(v, 2)
             res = {"slo_attainment": round(st["slo_attainment"], 4), "p95_latency_s": rnd(st["p95_latency_s"]),
-                   "mean_latency_s": rnd(st["mean_latency_s"]), "finished": st["finished"]}
+                   "mean_latency_s": rnd(st["mean_latency_s"]), "finished": st["finished"],
+                   "mean_in_flight": rnd(st["mean_in_flight"]), "stage_wait_mean_s": st["stage_wait_mean_s"],
+                   "stage_wait_p95_s": st["stage_wait_p95_s"]}
             if mix is not None:
                 for t, sc in enumerate(mix):
                     sel = [w for w in d.wf if w.wid % 2 == t]
@@ -669,7 +671,8 @@ def measured_ablation(n_wf, rate, policies=("pq", "fcfs", "llf"), slo_scale=10, 
         res = {"policy": name, "slo_attainment": round(st["slo_attainment"], 4),
                "p95_latency_s": rnd(st["p95_latency_s"]), "mean_latency_s": rnd(st["mean_latency_s"]),
                "finished": st["finished"], "iterations": st["iterations"],
-               "gpu_seconds": round(time.perf_counter() - t0, 1)}
+               "gpu_seconds": round(time.perf_counter() - t0, 1), "mean_in_flight": rnd(st["mean_in_flight"]),
+               "stage_wait_mean_s": st["stage_wait_mean_s"], "stage_wait_p95_s": st["stage_wait_p95_s"]}
         if tenants is not None:
             for t, sc in enumerate(tenants):
                 sel = [w for w in d.wf if w.wid % 2 == t]
@@ -837,6 +840,46 @@ def gemm_probe(reps=3, M=2080):
     return {"probe": "prefill GEMMs at 2080 rows", "gemms": out}
 
 
+PREFILL_PROBE_CHUNKS = ((0, 2048), (2048, 2048), (6144, 2048), (0, 1024), (4352, 512), (4080, 16))
+
+
+def prefill_attn_probe(reps=11):
+    """Only the chunked-prefill attention (plus its merge when items are cut), one chunk
+    of one sequence at a time at the 8B head shape, `reps` times per chunk (first position,
+    queries) of PREFILL_PROBE_CHUNKS: the short program the kernel-trace run profiles (each
+    call uploads its work list and synchronises, so per-kernel times come from the trace)."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2505_05286_amd import hxf
+
+    hxf.lib()
+    shape = synth.model_shape("llama8b")
+    hq, hkv, dh = shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+    dev = "cuda:0"
+    g = torch.Generator(device=dev).manual_seed(0)
+    out = []
+    for p0, n in PREFILL_PROBE_CHUNKS:
+        pages = -(-(p0 + n) // 16)
+        bt = np.arange(pages, dtype=np.int32)[None, :]
+        per = hkv * pages * 16 * dh
+        kp = (torch.randn(per, device=dev, generator=g) * 0.5).to(torch.bfloat16)
+        vp = (torch.randn(per, device=dev, generator=g) * 0.5).to(torch.bfloat16)
+        q = (torch.randn(n * hq * dh, device=dev, generator=g) * 0.5).to(torch.bfloat16)
+        o = torch.empty_like(q)
+        btd = torch.from_numpy(bt).to(dev)
+        wsn = hxf.op_prefill_attention_workspace_bytes(1, hq, hkv, [n])
+        ws = torch.empty(max(wsn, 256), dtype=torch.uint8, device=dev)
+        for _ in range(reps):
+            hxf.op_prefill_attention(q.data_ptr(), kp.data_ptr(), vp.data_ptr(), pages, btd.data_ptr(), pages, [0],
+                                     [p0], [n], o.data_ptr(), 1, hq, hkv, dh, ws.data_ptr(), ws.numel())
+        torch.cuda.synchronize()
+        flops = (p0 * n + n * (n + 1) // 2) * 4 * dh * hq
+        out.append({"first_position": p0, "queries": n, "launches": reps, "flops": flops})
+    return {"probe": "prefill attention, one 8B-shaped chunk per call", "chunks": out}
+
+
 def attn_kernel_probe(reps=8):
     """Only the paged decode-attention kernel (plus its merge) on the benchmark's
     64 contexts, `reps` times, then one 1 GiB device copy of known size: the short
@@ -902,6 +945,8 @@ def main():
                     help="CPU baseline leg for workloads 1, 3, 4 and 5: the oracle timed on the host cores")
     ap.add_argument("--gemm-probe", action="store_true",
                     help="run only the four 2080-row prefill GEMMs (for MFMA counter runs)")
+    ap.add_argument("--prefill-attn-probe", action="store_true",
+                    help="run only the prefill attention on six chunk shapes (for kernel-trace runs)")
     ap.add_argument("--policy-ablation", action="store_true",
                     help="PQ / FCFS / LLF on config-5 workflows, virtual clock, scheduler only (CPU)")
     ap.add_argument("--measured-ablation", action="store_true",
@@ -935,6 +980,10 @@ def main():
 
     if args.gemm_probe:
         print(json.dumps(gemm_probe()), flush=True)
+        return
+
+    if args.prefill_attn_probe:
+        print(json.dumps(prefill_attn_probe()), flush=True)
         return
 
     if args.calibrate:

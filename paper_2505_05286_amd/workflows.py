@@ -49,6 +49,7 @@ class Driver:
         self.tokens = 0
         self.prefill_tokens = 0
         self.decode_tokens = 0
+        self.stage_waits = {}        # stage index -> queueing delays (first scheduled - submitted), us
 
     def _submit_stage(self, w, now):
         w.stage += 1
@@ -103,6 +104,8 @@ class Driver:
             for c in self.inst.drain():
                 w = self.by_id[c["id"]]
                 j = c["stage_index"]
+                if "t_first_sched_us" in c:
+                    self.stage_waits.setdefault(j, []).append(c["t_first_sched_us"] - c["t_submit_us"])
                 w.done[j] += 1
                 if w.done[j] == len(w.stages[j]):
                     if j + 1 < len(w.stages):
@@ -124,6 +127,8 @@ class Driver:
         slo = np.array([w.slo_us for w in self.wf], dtype=np.float64)
         makespan = max(w.finish_us for w in done) - min(w.arrival_us for w in self.wf) if done else 0
         p95 = float(np.percentile(lat, 95))
+        waits = [np.asarray(self.stage_waits.get(j, [0]), dtype=np.float64) / 1e6
+                 for j in range(max(self.stage_waits, default=-1) + 1)]
         return {
             "workflows": len(self.wf),
             "finished": len(done),
@@ -133,6 +138,11 @@ class Driver:
             "mean_latency_s": float(np.mean([w.finish_us - w.arrival_us for w in done]) / 1e6) if done else None,
             "p95_slo_scale": float(np.percentile(lat / (slo / 10.0), 95)) if np.isfinite(p95) else None,
             "throughput_wf_per_s": len(done) / (makespan / 1e6) if makespan > 0 else 0.0,
+            # workflows in flight, averaged over the run (Little's law: total latency / makespan)
+            "mean_in_flight": float(sum(w.finish_us - w.arrival_us for w in done) / makespan) if makespan > 0 else 0.0,
+            # per stage index: mean and P95 of the requests' queueing delay (submission to first batch)
+            "stage_wait_mean_s": [round(float(np.mean(x)), 3) for x in waits],
+            "stage_wait_p95_s": [round(float(np.percentile(x, 95)), 3) for x in waits],
             "iterations": self.iterations,
             "prefill_tokens": self.prefill_tokens,
             "decode_tokens": self.decode_tokens,

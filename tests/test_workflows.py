@@ -51,7 +51,8 @@ class OracleInstance:
         return (hxf.IDLE if st == S.IDLE else hxf.OK), info
 
     def drain(self):
-        return [dict(id=d["id"], stage_index=d["stage"], t_finish_us=d["t_finish"]) for d in self.s.drain()]
+        return [dict(id=d["id"], stage_index=d["stage"], t_finish_us=d["t_finish"], t_submit_us=d["t_submit"],
+                     t_first_sched_us=d["t_first_sched"]) for d in self.s.drain()]
 
     def release(self, rid):
         self.s.release(rid)
