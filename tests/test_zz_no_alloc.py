@@ -57,7 +57,7 @@ def test_noalloc_matches_the_workspace_entry_point_twice(first, second):
 
 def test_noalloc_refuses_partials_beyond_its_array():
     t = torch()
-    M, N, K = 256, 4096, 4096                       # 8 splits x 256 x 4096 x 4 B = 32 MiB
+    M, N, K = 256, 4096, 14336                      # a down projection at 256 rows: split-K partials of 32 MiB
     assert hxf.op_gemm_workspace_bytes(M, N, K) > hxf.GEMM_NOALLOC_MAX_BYTES
     rng = np.random.default_rng(3)
     A, Bs, C0, rows = _operands(rng, M, N, K, hxf.EPI_RESID)
