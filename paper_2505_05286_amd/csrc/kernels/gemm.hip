@@ -510,8 +510,9 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
       step[u] = 512;
     }
   }
-  // A past K: the last 16-byte chunk of the row is read again (its weights are zero)
-  const int a_last = a.K - 8 - (lane >> 4) * 8;
+  // A past K: a chunk of the row is read again (its weights are zero): the lane's last
+  // in-row chunk, or the row's first when K < 32 (never an address before the row)
+  const int a_last = max(a.K - 8 - (lane >> 4) * 8, 0);
   auto issue = [&](int s, bf16_t* base) {
     const int k0 = kb + min(s, nst - 1) * 32;   // past the end: reload the last stage (unused)
 #pragma unroll

@@ -67,7 +67,8 @@ def _gemm_case(M_, N, K, epi, seed, rows=None):
                                     (96, 20000, 256), (250, 6144, 1024), (2300, 6144, 72), (960, 11008, 72),
                                     (64, 10240, 8192), (64, 8192, 28672), (2080, 10240, 1024),
                                     (256, 6144, 4096), (256, 4096, 14336), (512, 4096, 4096), (129, 4096, 4096),
-                                    (500, 1000, 4096), (384, 6144, 1000), (200, 8192, 2056)])
+                                    (500, 1000, 4096), (384, 6144, 1000), (200, 8192, 2056),
+                                    (600, 256, 8), (1030, 320, 24)])
 @pytest.mark.parametrize("epi", [hxf.EPI_BF16, hxf.EPI_RESID, hxf.EPI_F32])
 def test_gemm(M_, N, K, epi):
     _gemm_case(M_, N, K, epi, seed=M_ * 7 + N + K + epi)
