@@ -126,6 +126,18 @@ int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_poo
  * pos0_host[s] .. pos0_host[s]+n-1, stored at rows row0_host[s].. of q bf16 [*, Hq, dh];
  * it attends to positions [0, pos0+i] of its block table row bt[s] (device).  out rows as q. */
 int64_t hxf_op_prefill_attention_workspace_bytes(int32_t S, int32_t Hq, int32_t Hkv, const int32_t* n_host);
+/* Introspection (host only, no device work): the prefill-attention work list the call below
+ * builds for the same chunks.  items: n_items records of 8 int32 {entry, kvh, q0, nq, t0, t1, part,
+ * pad} (queries [q0, q0 + nq) of chunk `entry` on kv-head kvh over key tiles [t0, t1) of 32
+ * positions; part = -1 for an item that writes its output, else the partial slot of a cut item),
+ * in launch order; merges: n_merges records of 8 int32 {entry, kvh, q0, nq, part0, n_part, pad,
+ * pad} (the partial slots [part0, part0 + n_part) of one cut item, combined by log-sum-exp).
+ * Items are cut into key ranges only when there are fewer of them than CUs: those longer than an
+ * even share of all key tiles over the resident workgroups (two per CU), at least 8 tiles.
+ * HXF_ENOMEM (with the counts set) when a capacity is short. */
+int hxf_op_prefill_plan(int32_t S, int32_t Hq, int32_t Hkv, const int32_t* pos0_host, const int32_t* n_host,
+                        int32_t* items, int32_t items_cap, int32_t* n_items, int32_t* merges, int32_t merges_cap,
+                        int32_t* n_merges);
 int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_pool, int64_t n_blocks, const int32_t* bt,
                              int32_t bt_stride, const int32_t* row0_host, const int32_t* pos0_host,
                              const int32_t* n_host, void* out, int32_t S, int32_t Hq, int32_t Hkv, int32_t head_dim,

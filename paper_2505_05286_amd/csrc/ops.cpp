@@ -250,6 +250,28 @@ int64_t hxf_op_prefill_attention_workspace_bytes(int32_t S, int32_t Hq, int32_t 
   return prefill_layout(prefill_whole_items(S, Hkv, qpi, n_host), S, 128).total;
 }
 
+int hxf_op_prefill_plan(int32_t S, int32_t Hq, int32_t Hkv, const int32_t* pos0, const int32_t* n_host,
+                        int32_t* items, int32_t items_cap, int32_t* n_items, int32_t* merges, int32_t merges_cap,
+                        int32_t* n_merges) {
+  if (S < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv || Hq / Hkv > 16 || (S > 0 && (!pos0 || !n_host)) || !n_items ||
+      !n_merges || (items_cap > 0 && !items) || (merges_cap > 0 && !merges))
+    return HXF_EINVAL;
+  std::vector<PrefillEntry> entries;
+  for (int s = 0; s < S; ++s) {
+    if (n_host[s] < 0 || pos0[s] < 0) return HXF_EINVAL;
+    if (n_host[s] > 0) entries.push_back(PrefillEntry{s, pos0[s], n_host[s]});
+  }
+  PrefillPlan P;
+  plan_prefill(entries, Hkv, prefill_queries_per_item(Hq / Hkv), P);
+  *n_items = (int32_t)P.items.size();
+  *n_merges = (int32_t)P.merges.size();
+  if ((int64_t)items_cap < (int64_t)P.items.size() || (int64_t)merges_cap < (int64_t)P.merges.size())
+    return HXF_ENOMEM;
+  std::memcpy(items, P.items.data(), P.items.size() * sizeof(PrefillItem));
+  std::memcpy(merges, P.merges.data(), P.merges.size() * sizeof(PrefillMerge));
+  return HXF_OK;
+}
+
 int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_pool, int64_t n_blocks, const int32_t* bt,
                              int32_t bt_stride, const int32_t* row0, const int32_t* pos0, const int32_t* n_host,
                              void* out, int32_t S, int32_t Hq, int32_t Hkv, int32_t dh, void* workspace,

@@ -155,6 +155,9 @@ _SIGS = {
     "hxf_op_decode_plan": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
                                      C.c_int32, C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32),
                                      C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32)]),
+    "hxf_op_prefill_plan": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
+                                      C.POINTER(C.c_int32), C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_int32),
+                                      C.c_int32, C.POINTER(C.c_int32)]),
     "hxf_op_decode_attention": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p, C.c_int32,
                                           C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.c_void_p, C.c_int32,
                                           C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int64, C.c_void_p]),
@@ -478,6 +481,25 @@ def op_decode_plan(B, Hq, Hkv, ctx, bt_host=None, bt_stride=0):
     _op(lib().hxf_op_decode_plan(B, Hq, Hkv, cp, bp, bt_stride, items.ctypes.data_as(C.POINTER(C.c_int32)),
                                  ni.value, C.byref(ni), merges.ctypes.data_as(C.POINTER(C.c_int32)), nm.value,
                                  C.byref(nm)), "hxf_op_decode_plan")
+    return items, merges
+
+
+def op_prefill_plan(Hq, Hkv, pos0, n):
+    """The prefill-attention work list for chunks of n[s] queries from position pos0[s]:
+    (items int32 [k, 8] {entry, kvh, q0, nq, t0, t1, part, pad} in launch order, merges int32
+    [m, 8] {entry, kvh, q0, nq, part0, n_part, pad, pad})."""
+    S = len(n)
+    p, pp = _i32(pos0)
+    c, cp = _i32(n)
+    ni, nm = C.c_int32(0), C.c_int32(0)
+    rc = lib().hxf_op_prefill_plan(S, Hq, Hkv, pp, cp, None, 0, C.byref(ni), None, 0, C.byref(nm))
+    if rc not in (OK, ENOMEM):
+        raise HxfError(rc, "hxf_op_prefill_plan")
+    items = np.zeros((ni.value, 8), np.int32)
+    merges = np.zeros((nm.value, 8), np.int32)
+    _op(lib().hxf_op_prefill_plan(S, Hq, Hkv, pp, cp, items.ctypes.data_as(C.POINTER(C.c_int32)), ni.value,
+                                  C.byref(ni), merges.ctypes.data_as(C.POINTER(C.c_int32)), nm.value, C.byref(nm)),
+        "hxf_op_prefill_plan")
     return items, merges
 
 

@@ -166,3 +166,73 @@ def test_plans_reused_across_iterations_carry_nothing_over(tmp_path):
                    check=True, capture_output=True, timeout=300)
     r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
     assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout + r.stderr
+
+
+# ------------------------------------------------------------------ prefill work list
+
+PF_PAIRS, PF_RESIDENT = 128, 512
+
+
+def _check_prefill(pos0, n, hq, hkv):
+    """Every (chunk, kv-head, query block) attends to its key tiles exactly once, either as
+    one whole item or as the consecutive parts of one merge; returns (items, merges, share)."""
+    items, merges = hxf.op_prefill_plan(hq, hkv, pos0, n)
+    G = hq // hkv
+    qpi = PF_PAIRS // G
+    whole = {}
+    for s, (p0, ns) in enumerate(zip(pos0, n)):
+        for h in range(hkv):
+            for q0 in range(0, ns, qpi):
+                nq = min(qpi, ns - q0)
+                whole[(s, h, q0)] = (nq, -(-(p0 + q0 + nq) // 32))
+    tiles = sum(t for _, t in whole.values())
+    share = max(-(-tiles // PF_RESIDENT), 8)
+    assert len(items) <= len(whole) + PF_RESIDENT
+    got = {}
+    for e, h, q0, nq, t0, t1, part, _ in items:
+        assert (e, h, q0) in whole and whole[(e, h, q0)][0] == nq
+        assert 0 <= t0 < t1 <= whole[(e, h, q0)][1]
+        got.setdefault((e, h, q0), []).append((t0, t1, part))
+    assert set(got) == set(whole)
+    parts_seen = set()
+    merged = {(m[0], m[1], m[2]): m for m in merges}
+    for key, ranges in got.items():
+        ranges.sort()
+        assert ranges[0][0] == 0 and ranges[-1][1] == whole[key][1]
+        for (a0, a1, _), (b0, b1, _) in zip(ranges, ranges[1:]):
+            assert a1 == b0                                  # no gap, no overlap
+        if len(ranges) == 1:
+            assert ranges[0][2] == -1 and key not in merged
+        else:
+            m = merged[key]
+            assert m[3] == whole[key][0] and m[5] == len(ranges)
+            assert [r[2] for r in ranges] == list(range(m[4], m[4] + m[5]))
+            parts_seen.update(r[2] for r in ranges)
+    assert len(parts_seen) == sum(m[5] for m in merges) <= len(whole) + PF_RESIDENT
+    return items, merges, share, whole
+
+
+def test_prefill_plan_full_chunks_are_not_cut():
+    """With at least one item per CU nothing is cut: a prompt's first 2048-token chunk at the
+    8B heads (512 causal items of 1 to 64 key tiles), its second, one deep into the prompt, and
+    a 1024-token first chunk (256 items)."""
+    for p0, n in ((0, 2048), (2048, 2048), (6144, 2048), (0, 1024)):
+        items, merges, share, whole = _check_prefill([p0], [n], 32, 8)
+        assert len(merges) == 0 and len(items) == len(whole) == n // 4
+        assert (items[:, 6] == -1).all()
+
+
+@pytest.mark.parametrize("p0,n", [(4352, 512), (4080, 16), (0, 960)])
+def test_prefill_plan_few_items_cut_to_the_share(p0, n):
+    """Fewer items than CUs: every item longer than the share is cut."""
+    items, merges, share, whole = _check_prefill([p0], [n], 32, 8)
+    assert len(whole) < PF_RESIDENT // 2
+    assert max(t1 - t0 for *_, t0, t1, _p, _pad in items) <= share
+    assert len(merges) == sum(1 for nq, t in whole.values() if t > share)
+
+
+@pytest.mark.parametrize("pos0,n,hq,hkv", [
+    ([0, 100, 5000], [700, 33, 2048], 32, 8), ([0], [1], 4, 2), ([4080], [16], 40, 8), ([0, 0], [2048, 2048], 64, 8),
+    ([17, 0, 3000], [2300, 5, 640], 4, 2)])
+def test_prefill_plan_covers_every_key_tile_once(pos0, n, hq, hkv):
+    _check_prefill(pos0, n, hq, hkv)
