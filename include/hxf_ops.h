@@ -30,8 +30,9 @@
 extern "C" {
 #endif
 
-/* GEMM epilogues */
+/* GEMM epilogues, and layout flags that may be or-ed into the epilogue argument */
 enum { HXF_EPI_BF16 = 0, HXF_EPI_RESID = 1, HXF_EPI_SWIGLU = 2, HXF_EPI_F32 = 3 };
+enum { HXF_GEMM_A_PACKED = 0x100, HXF_GEMM_C_PACKED = 0x200 };
 
 /* C = A[M,K] . B[N,K]^T, bf16 inputs, fp32 accumulation.  A is row-major with row
  * stride lda; B (and B2) are PACKED weights (hxf_op_pack_weight of the row-major
@@ -42,14 +43,21 @@ enum { HXF_EPI_BF16 = 0, HXF_EPI_RESID = 1, HXF_EPI_SWIGLU = 2, HXF_EPI_F32 = 3 
  *                   C[:, f] = bf16(silu(gate_f) * up_f), silu(z) = z / (1 + e^-z)
  *   HXF_EPI_F32:    C fp32 [M, ldc]            C = acc
  * K % 8 == 0, lda >= K.  workspace: hxf_op_gemm_workspace_bytes(M, N, K) bytes
- * (split-K partials for M <= 512, enough for every epilogue; may be 0 bytes).  */
+ * (split-K partials for M <= 512, enough for every epilogue; may be 0 bytes).
+ * HXF_GEMM_A_PACKED: A is in the packed layout of the weights (hxf_op_pack_weight of the
+ * row-major [M,K] activations, ceil(M/16)*16 rows; lda unused), so that a 16 x 32 block of
+ * it is one contiguous kilobyte; M > 512 and K % 32 == 0 only.  HXF_GEMM_C_PACKED (SwiGLU,
+ * M > 512, F % 32 == 0): C is written in that packed layout ([M,F] with ceil(F/32) tiles per
+ * row tile; ldc unused), the form in which the down projection reads it.  Either flag on
+ * another shape: HXF_EINVAL. */
 int64_t hxf_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
 int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void* C, int32_t ldc, int32_t M, int32_t N,
                 int32_t K, int32_t epilogue, void* workspace, int64_t workspace_bytes, void* stream);
 
 /* hxf_op_gemm without a workspace, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid it).
- * Same arguments and result as hxf_op_gemm; the split-K partials go to a device
+ * Same arguments and result as hxf_op_gemm (the layout flags are refused: HXF_EINVAL);
+ * the split-K partials go to a device
  * array of HXF_GEMM_NOALLOC_MAX_BYTES that the library holds on each GPU it runs on
  * until the process ends (its address is looked up on the first call on a device,
  * which must be the current device).  Nothing is allocated.  HXF_ENOMEM (nothing

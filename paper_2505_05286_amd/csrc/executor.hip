@@ -18,6 +18,17 @@ namespace hxf {
 namespace {
 
 constexpr int kMaxSplits = 8;
+// Iterations of more rows than this keep the GEMM activations (the normed hidden state,
+// the attention output, the SwiGLU output) in the packed tile layout of the weights, in
+// which a 16 x 32 block the prefill GEMMs stage is one contiguous kilobyte rather than 16
+// row pieces (the GEMMs of these sizes run on the big-tile kernel, which reads it).
+constexpr int kPackRows = 512;
+
+// memcpy of a vector's elements; nothing for an empty one (whose data() may be null)
+template <typename T>
+void copy_vec(void* dst, const std::vector<T>& v) {
+  if (!v.empty()) std::memcpy(dst, v.data(), v.size() * sizeof(T));
+}
 
 int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 
@@ -94,10 +105,13 @@ WsPlan plan_workspace(const hxf_model_cfg& m, const hxf_sched_cfg& s) {
   p.off_meta = take(p.meta_bytes);
   p.off_rope = take((int64_t)m.max_context * (dh / 2) * 8);
   p.off_resid = take(p.t_max * d * 4);
-  p.off_h = take(p.t_max * d * 2);
+  // the GEMM activations of prefill-sized iterations are stored in the packed tile layout,
+  // whole 16-row tiles
+  const int64_t t16 = (p.t_max + 15) / 16 * 16;
+  p.off_h = take(t16 * d * 2);
   p.off_qkv = take(p.t_max * qkv * 2);
-  p.off_attn = take(p.t_max * hq * dh * 2);
-  p.off_act = take(p.t_max * f * 2);
+  p.off_attn = take(t16 * hq * dh * 2);
+  p.off_act = take(t16 * f * 2);
   p.part_bytes = part;
   p.off_part = take(std::max<int64_t>(part, 256));
   p.off_attn_o = take(p.dec_items_max * G * dh * 4);
@@ -171,8 +185,10 @@ class HipExecutor : public Executor {
   // With `pending` set, a split-K plan leaves its partials in the workspace and
   // *pending = its split count (0 when the GEMM finished its own epilogue).
   // `kind` (HXF_PROF_*) names the projection for profiling.
+  // a_packed: A in the packed tile layout; c_kt > 0: the SwiGLU output packed (both only
+  // for prefill-sized M, see kPackRows).
   int gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M, int N, int K,
-           int epi, int kind, std::string& err, int* pending = nullptr);
+           int epi, int kind, std::string& err, int* pending = nullptr, bool a_packed = false, int c_kt = 0);
   // A pair of events for a profiled launch of `kind` (0-4 GEMMs, 5 prefill attention)
   // doing `flops`; null events when profiling is off.
   int prof_events(int kind, double flops, hipEvent_t* e0, hipEvent_t* e1, std::string& err);
@@ -235,8 +251,10 @@ int HipExecutor::prof_events(int kind, double flops, hipEvent_t* e0, hipEvent_t*
 }
 
 int HipExecutor::gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M,
-                      int N, int K, int epi, int kind, std::string& err, int* pending) {
+                      int N, int K, int epi, int kind, std::string& err, int* pending, bool a_packed, int c_kt) {
   GemmArgs a{};
+  a.a_packed = a_packed ? 1 : 0;
+  a.c_kt = c_kt;
   a.A = A;
   a.B = B;
   a.B2 = B2;
@@ -353,10 +371,10 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   const int64_t n_wide = dplan_.n_wide, n_narrow = (int64_t)ditems.size() - n_wide;
   hm[o_nitems] = (int32_t)n_narrow;
   hm[o_nitems + 1] = (int32_t)n_wide;
-  std::memcpy(hm + o_ditems, ditems.data(), ditems.size() * sizeof(DecodeItem));
-  std::memcpy(hm + o_merges, merges.data(), merges.size() * sizeof(MergeItem));
-  std::memcpy(hm + o_pitems, pitems.data(), pitems.size() * sizeof(PrefillItem));
-  std::memcpy(hm + o_pmerges, pmerges.data(), pmerges.size() * sizeof(PrefillMerge));
+  copy_vec(hm + o_ditems, ditems);
+  copy_vec(hm + o_merges, merges);
+  copy_vec(hm + o_pitems, pitems);
+  copy_vec(hm + o_pmerges, pmerges);
   if (check_) {
     // every index a kernel follows, checked on the host against the buffers it addresses
     auto fail = [&](const char* what, int64_t i) {
@@ -423,6 +441,8 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   uint16_t* act = dev<uint16_t>(plan_.off_act);
   const float2* rope = dev<float2>(plan_.off_rope);
   const float scale_log2 = 1.4426950408889634f / std::sqrt((float)dh);
+  const bool pack = T > kPackRows && d % 32 == 0 && f % 32 == 0 && (hq * dh) % 32 == 0;
+  const int kt_h = pack ? d / 32 : 0, kt_attn = pack ? hq * dh / 32 : 0, kt_act = pack ? f / 32 : 0;
   const int64_t layer_pool = (int64_t)s_.n_blocks * hkv * kPage * dh;   // bf16 elements per K (or V) pool
   uint16_t* pool = reinterpret_cast<uint16_t*>(b_.kv_pool);
 
@@ -443,6 +463,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   da.part_ml = dev<float>(plan_.off_attn_ml);
   da.out = attn;
   da.out_stride = hq * dh;
+  da.out_kt = kt_attn;
   da.Hq = hq;
   da.Hkv = hkv;
   da.dh = dh;
@@ -463,6 +484,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   pa.part_ml = dev<float>(plan_.off_pf_ml);
   pa.out = attn;
   pa.out_stride = hq * dh;
+  pa.out_kt = kt_attn;
   pa.Hq = hq;
   pa.Hkv = hkv;
   pa.dh = dh;
@@ -481,7 +503,7 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   auto forward = [&]() -> int {
     HXF_HIP(hipMemcpyAsync(dm, hm, w * 4, hipMemcpyHostToDevice, st_));
     HXF_HIP(embed_rmsnorm_launch(dm + o_ids, (const uint16_t*)b_.embed, (const uint16_t*)layers_[0].attn_norm,
-                                 resid, h, T, d, m_.rms_eps, st_));
+                                 resid, h, T, d, m_.rms_eps, st_, kt_h));
     // Split-K GEMMs of decode-sized batches hand their partials to the next kernel
     // (RoPE/KV write, residual add + RMSNorm), which sums them in split order.
     float* part = dev<float>(plan_.off_part);
@@ -492,10 +514,10 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
       uint16_t* vp = kp + layer_pool;
       if (l > 0)
         HXF_HIP(resid_rmsnorm_launch(resid, part, pend_down, T, nullptr, (const uint16_t*)L.attn_norm, h, T, d,
-                                     m_.rms_eps, st_));
+                                     m_.rms_eps, st_, kt_h));
       int pend_qkv = 0;
       if (int rc = gemm(h, d, (const uint16_t*)L.wqkv, nullptr, qkv, qkv_w, T, qkv_w, d, EPI_BF16, HXF_PROF_QKV, err,
-                        &pend_qkv))
+                        &pend_qkv, pack))
         return rc;
       if (pend_qkv)
         HXF_HIP(rope_kv_partials_launch(qkv, part, pend_qkv, dm + o_pos, dm + o_slot, rope, kp, vp, s_.n_blocks, T, hq,
@@ -529,16 +551,16 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
       int pend_o = 0;
       if (int rc =
               gemm(attn, hq * dh, (const uint16_t*)L.wo, nullptr, resid, d, T, d, hq * dh, EPI_RESID, HXF_PROF_O, err,
-                   &pend_o))
+                   &pend_o, pack))
         return rc;
       HXF_HIP(resid_rmsnorm_launch(resid, part, pend_o, T, nullptr, (const uint16_t*)L.ffn_norm, h, T, d, m_.rms_eps,
-                                   st_));
+                                   st_, kt_h));
       if (int rc =
               gemm(h, d, (const uint16_t*)L.w_gate, (const uint16_t*)L.w_up, act, f, T, 2 * f, d, EPI_SWIGLU,
-                   HXF_PROF_GATE_UP, err))
+                   HXF_PROF_GATE_UP, err, nullptr, pack, kt_act))
         return rc;
       if (int rc = gemm(act, f, (const uint16_t*)L.w_down, nullptr, resid, d, T, d, f, EPI_RESID, HXF_PROF_DOWN, err,
-                        &pend_down))
+                        &pend_down, pack))
         return rc;
     }
     if (R > 0) {

@@ -307,7 +307,8 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeAttnArgs a) {
     }
   }
   const float inv = 1.f / L;
-  uint16_t* out = a.out + (size_t)orow * a.out_stride + (mi.kvh * G + g) * DH + lane * PER;
+  const int col = (mi.kvh * G + g) * DH + lane * PER;   // (PER columns in one 8-column group)
+  uint16_t* out = a.out + (a.out_kt ? packed_elem(orow, col, a.out_kt) : (size_t)orow * a.out_stride + col);
   if constexpr (PER == 2) *reinterpret_cast<uint32_t*>(out) = pack_bf2(acc[0] * inv, acc[PER - 1] * inv);
   else out[0] = f2bf(acc[0] * inv);
 }
@@ -548,13 +549,14 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
     if (p >= npairs) continue;
     const float inv = 1.f / lt[pt];
     const int qi = p / G, hj = p % G;
-    uint16_t* out = a.out + (size_t)(a.row0[it.entry] + it.q0 + qi) * a.out_stride + (it.kvh * G + hj) * DH;
+    const int orow = a.row0[it.entry] + it.q0 + qi, col0 = (it.kvh * G + hj) * DH;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        const int d = dt * 32 + g4 * 8 + h * 4;
-        *reinterpret_cast<uint2*>(out + d) =
+        const int d = dt * 32 + g4 * 8 + h * 4;   // 4 columns inside one 8-column group
+        const size_t at = a.out_kt ? packed_elem(orow, col0 + d, a.out_kt) : (size_t)orow * a.out_stride + col0 + d;
+        *reinterpret_cast<uint2*>(a.out + at) =
             make_uint2(pack_bf2(o[pt][dt][g4 * 4] * inv, o[pt][dt][g4 * 4 + 1] * inv),
                        pack_bf2(o[pt][dt][g4 * 4 + 2] * inv, o[pt][dt][g4 * 4 + 3] * inv));
       }
@@ -617,7 +619,8 @@ __global__ __launch_bounds__(256) void prefill_merge_kernel(PrefillAttnArgs a) {
   }
   const float inv = 1.f / L;
   const int qi = p / G, hj = p % G;
-  uint16_t* out = a.out + (size_t)(a.row0[mg.entry] + mg.q0 + qi) * a.out_stride + (mg.kvh * G + hj) * DH + d0;
+  const int orow = a.row0[mg.entry] + mg.q0 + qi, col = (mg.kvh * G + hj) * DH + d0;   // one 8-column group
+  uint16_t* out = a.out + (a.out_kt ? packed_elem(orow, col, a.out_kt) : (size_t)orow * a.out_stride + col);
   *reinterpret_cast<uint4*>(out) = make_uint4(pack_bf2(acc[0] * inv, acc[1] * inv), pack_bf2(acc[2] * inv, acc[3] * inv),
                                               pack_bf2(acc[4] * inv, acc[5] * inv), pack_bf2(acc[6] * inv, acc[7] * inv));
 }

@@ -484,9 +484,9 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
   const int nst = (ke - kb + 31) / 32;
 
   // This wavefront's DMA blocks w*PER_W + u: an A block (16 activation rows, the
-  // lane's row and 8-column chunk) or a packed weight tile (1 KB contiguous).  No
-  // per-block branches at issue time, so the compiler keeps track of which LDS
-  // array each DMA writes.
+  // lane's row and 8-column chunk; with packed activations a 1 KB tile like the
+  // weights') or a packed weight tile (1 KB contiguous).  No per-block branches at
+  // issue time, so the compiler keeps track of which LDS array each DMA writes.
   const bf16_t* src[PER_W];
   int step[PER_W];   // elements per stage: 32 along an activation row, 512 for a weight tile
   int dst[PER_W];
@@ -494,7 +494,11 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
   for (int u = 0; u < PER_W; ++u) {
     const int gb = min(w * PER_W + u, NBLK - 1);
     dst[u] = gb * 512;
-    if (gb < AB) {
+    if (gb < AB && a.a_packed) {
+      // row tiles past M repeat the last one (its rows past M are never stored)
+      src[u] = a.A + (size_t)min(m0 / 16 + gb, (a.M - 1) / 16) * a.kt * 512 + lane * 8;
+      step[u] = 512;
+    } else if (gb < AB) {
       src[u] = a.A + (size_t)min(m0 + gb * 16 + (lane & 15), a.M - 1) * a.lda + (lane >> 4) * 8;
       step[u] = 32;
     } else {
@@ -641,7 +645,8 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_big_kernel(GemmArgs a) {
           const int lc = wc0 + j * 32;   // first (gate) logical column of the 64-group
           if (lc >= a.N) continue;
           const float g = acc[i][j][r], u = acc[i][j + 1][r];
-          reinterpret_cast<bf16_t*>(a.C)[(size_t)row * a.ldc + (lc >> 6) * 32 + l32] =
+          const int oc = (lc >> 6) * 32 + l32;
+          reinterpret_cast<bf16_t*>(a.C)[a.c_kt ? packed_elem(row, oc, a.c_kt) : (size_t)row * a.ldc + oc] =
               f2bf(g / (1.f + __expf(-g)) * u);
         }
       } else {
@@ -847,6 +852,10 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu) {
 
 hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st, bool reduce, hipEvent_t e0,
                        hipEvent_t e1) {
+  // packed activations in or SwiGLU output packed: the big-tile kernel without split K only
+  if ((a.a_packed || a.c_kt) && (!p.big || p.splits > 1 || (epi == EPI_SWIGLU && a.N % 64 != 0) ||
+                                 (a.c_kt && (epi != EPI_SWIGLU || a.c_kt * 64 != a.N)) || (a.a_packed && a.K % 32)))
+    return hipErrorInvalidValue;
   switch (epi) {
     case EPI_BF16: return launch_epi<EPI_BF16>(a, p, st, reduce, e0, e1);
     case EPI_RESID: return launch_epi<EPI_RESID>(a, p, st, reduce, e0, e1);

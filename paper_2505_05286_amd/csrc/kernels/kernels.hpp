@@ -26,6 +26,14 @@ __host__ __device__ inline int v_pos(int t) { return (t & 3) | ((t >> 1) & 4) | 
 // ------------------------------------------------------------------ GEMM
 enum { EPI_BF16 = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3 };
 
+// Packed tile layout of a bf16 [rows, K] matrix (the weights', also used for the
+// activations the prefill GEMMs read): 16-row x 32-column tiles of 1 KB, row tiles
+// outermost, kt = ceil(K / 32) tiles per row tile, inside a tile [k%32 / 8][r%16][k%8].
+// A DMA of one 16 x 32 block is then one contiguous kilobyte instead of 16 row pieces.
+__host__ __device__ inline size_t packed_elem(int r, int k, int kt) {
+  return ((size_t)(r >> 4) * kt + (k >> 5)) * 512 + ((k >> 3) & 3) * 128 + (r & 15) * 8 + (k & 7);
+}
+
 struct GemmArgs {
   const uint16_t* A;   // bf16 [M, lda]
   const uint16_t* B;   // bf16 [N, K] (SwiGLU: gate rows [F, K])
@@ -36,6 +44,8 @@ struct GemmArgs {
   int lda, ldc;
   int k_chunk;
   int kt;              // K tiles of the packed weights, ceil(K / 32)
+  int a_packed;        // A is in the packed tile layout (lda unused); the big-tile kernel only
+  int c_kt;            // SwiGLU: > 0 writes C in the packed tile layout with c_kt tiles per row tile
 };
 
 struct GemmPlan {
@@ -65,12 +75,14 @@ hipError_t pack_weight_launch(const uint16_t* W, int N, int K, uint16_t* out, hi
 hipError_t rmsnorm_launch(const float* x, const int32_t* rows, const uint16_t* g, uint16_t* out,
                           int n_rows, int d, float eps, hipStream_t st);
 // x[rows[r]] += sum over z < S of part[z][rows[r]] (split-K partials [S][part_rows][d] of a
-// residual GEMM, in split order), then out[r] = bf16(rmsnorm(x[rows[r]]) * g)
+// residual GEMM, in split order), then out[r] = bf16(rmsnorm(x[rows[r]]) * g); out_kt > 0
+// writes out in the packed tile layout (d / 32 tiles per row tile, d % 32 == 0)
 hipError_t resid_rmsnorm_launch(float* x, const float* part, int S, int part_rows, const int32_t* rows,
-                                const uint16_t* g, uint16_t* out, int n_rows, int d, float eps, hipStream_t st);
-// resid[t] = E[ids[t]] (fp32); out[t] = bf16(rmsnorm(resid[t]) * g)
+                                const uint16_t* g, uint16_t* out, int n_rows, int d, float eps, hipStream_t st,
+                                int out_kt = 0);
+// resid[t] = E[ids[t]] (fp32); out[t] = bf16(rmsnorm(resid[t]) * g) (packed as above with out_kt)
 hipError_t embed_rmsnorm_launch(const int32_t* ids, const uint16_t* E, const uint16_t* g, float* resid,
-                                uint16_t* out, int T, int d, float eps, hipStream_t st);
+                                uint16_t* out, int T, int d, float eps, hipStream_t st, int out_kt = 0);
 
 // ------------------------------------------------------------------ RoPE + KV write
 // qkv bf16 [T, (Hq+2Hkv)*dh]: rotates q (in place) and k at pos[t] with the
@@ -156,6 +168,7 @@ struct DecodeAttnArgs {
   float* part_ml;          // [parts][G][2]  (max in log2 units, sum)
   uint16_t* out;           // bf16, row q_row[e]*out_stride + head*dh
   int out_stride;
+  int out_kt;              // > 0: out in the packed tile layout with out_kt tiles per row tile
   int Hq, Hkv, dh;
   float scale_log2;        // log2(e) / sqrt(dh)
 };
@@ -209,6 +222,7 @@ struct PrefillAttnArgs {
   float* part_ml;               // [slots][128 pairs][2]: (max in log2 units, sum)
   uint16_t* out;
   int out_stride;
+  int out_kt;                   // > 0: out in the packed tile layout with out_kt tiles per row tile
   int Hq, Hkv, dh;
   float scale_log2;
 };

@@ -21,9 +21,12 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return s;
 }
 
+// out: the output matrix; row `row` of it is written, row-major with stride d, or in the
+// packed tile layout with out_kt tiles per row tile (each thread's 4 columns stay
+// contiguous there: they lie in one 8-column group)
 template <int NT = 256>
-__device__ __forceinline__ void norm_store(const float4* x4, const uint16_t* g, uint16_t* out, int d, float eps,
-                                           float* red) {
+__device__ __forceinline__ void norm_store(const float4* x4, const uint16_t* g, uint16_t* out, int row, int out_kt,
+                                           int d, float eps, float* red) {
   const int n4 = d >> 2;
   float ss = 0.f;
   for (int i = threadIdx.x; i < n4; i += NT) {
@@ -32,12 +35,13 @@ __device__ __forceinline__ void norm_store(const float4* x4, const uint16_t* g, 
   }
   const float r = rsqrtf(block_sum<NT>(ss, red) / (float)d + eps);
   const uint2* g2 = reinterpret_cast<const uint2*>(g);
-  uint2* o2 = reinterpret_cast<uint2*>(out);
   for (int i = threadIdx.x; i < n4; i += NT) {
     const float4 v = x4[i];
     const uint2 gg = g2[i];
     const float g0 = bf2f(gg.x & 0xFFFF), g1 = bf2f(gg.x >> 16), g2v = bf2f(gg.y & 0xFFFF), g3 = bf2f(gg.y >> 16);
-    o2[i] = make_uint2(pack_bf2(v.x * r * g0, v.y * r * g1), pack_bf2(v.z * r * g2v, v.w * r * g3));
+    const size_t o = out_kt ? packed_elem(row, 4 * i, out_kt) : (size_t)row * d + 4 * i;
+    *reinterpret_cast<uint2*>(out + o) =
+        make_uint2(pack_bf2(v.x * r * g0, v.y * r * g1), pack_bf2(v.z * r * g2v, v.w * r * g3));
   }
 }
 
@@ -49,7 +53,7 @@ __device__ __forceinline__ void norm_store(const float4* x4, const uint16_t* g, 
 // four), 256 otherwise.
 template <int S, int NT>
 __global__ __launch_bounds__(NT) void rmsnorm_kernel(float* x, const int32_t* rows, const float* part, int part_rows,
-                                                     const uint16_t* g, uint16_t* out, int d, float eps) {
+                                                     const uint16_t* g, uint16_t* out, int d, float eps, int out_kt) {
   __shared__ float red[NT / 64];
   const int r = blockIdx.x;
   const int src = rows ? rows[r] : r;
@@ -71,11 +75,11 @@ __global__ __launch_bounds__(NT) void rmsnorm_kernel(float* x, const int32_t* ro
       x4[i] = v;
     }
   }
-  norm_store<NT>(x4, g, out + (size_t)r * d, d, eps, red);
+  norm_store<NT>(x4, g, out, r, out_kt, d, eps, red);
 }
 
 __global__ __launch_bounds__(256) void embed_rmsnorm_kernel(const int32_t* ids, const uint16_t* E, const uint16_t* g,
-                                                            float* resid, uint16_t* out, int d, float eps) {
+                                                            float* resid, uint16_t* out, int d, float eps, int out_kt) {
   __shared__ float red[4];
   const int t = blockIdx.x;
   const uint2* e2 = reinterpret_cast<const uint2*>(E + (size_t)ids[t] * d);
@@ -85,7 +89,7 @@ __global__ __launch_bounds__(256) void embed_rmsnorm_kernel(const int32_t* ids, 
     r4[i] = make_float4(bf2f(e.x & 0xFFFF), bf2f(e.x >> 16), bf2f(e.y & 0xFFFF), bf2f(e.y >> 16));
   }
   __syncthreads();
-  norm_store<256>(r4, g, out + (size_t)t * d, d, eps, red);
+  norm_store<256>(r4, g, out, t, out_kt, d, eps, red);
 }
 
 }  // namespace
@@ -96,16 +100,18 @@ hipError_t rmsnorm_launch(const float* x, const int32_t* rows, const uint16_t* g
 }
 
 hipError_t resid_rmsnorm_launch(float* x, const float* part, int S, int part_rows, const int32_t* rows,
-                                const uint16_t* g, uint16_t* out, int n_rows, int d, float eps, hipStream_t st) {
+                                const uint16_t* g, uint16_t* out, int n_rows, int d, float eps, hipStream_t st,
+                                int out_kt) {
   if (n_rows <= 0) return hipSuccess;
+  if (out_kt && (d % 32 || out_kt != d / 32)) return hipErrorInvalidValue;
 #define HXF_NORM(SS)                                                                                        \
   case SS:                                                                                                  \
     if (n_rows <= 256)                                                                                      \
       hipLaunchKernelGGL((rmsnorm_kernel<SS, 1024>), dim3(n_rows), dim3(1024), 0, st, x, rows, part, part_rows, g, \
-                         out, d, eps);                                                                      \
+                         out, d, eps, out_kt);                                                              \
     else                                                                                                    \
       hipLaunchKernelGGL((rmsnorm_kernel<SS, 256>), dim3(n_rows), dim3(256), 0, st, x, rows, part, part_rows, g, \
-                         out, d, eps);                                                                      \
+                         out, d, eps, out_kt);                                                              \
     break;
   switch (S) {
     HXF_NORM(0) HXF_NORM(1) HXF_NORM(2) HXF_NORM(3) HXF_NORM(4) HXF_NORM(5) HXF_NORM(6) HXF_NORM(7) HXF_NORM(8)
@@ -116,9 +122,10 @@ hipError_t resid_rmsnorm_launch(float* x, const float* part, int S, int part_row
 }
 
 hipError_t embed_rmsnorm_launch(const int32_t* ids, const uint16_t* E, const uint16_t* g, float* resid,
-                                uint16_t* out, int T, int d, float eps, hipStream_t st) {
+                                uint16_t* out, int T, int d, float eps, hipStream_t st, int out_kt) {
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_rmsnorm_kernel, dim3(T), dim3(256), 0, st, ids, E, g, resid, out, d, eps);
+  if (out_kt && (d % 32 || out_kt != d / 32)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(embed_rmsnorm_kernel, dim3(T), dim3(256), 0, st, ids, E, g, resid, out, d, eps, out_kt);
   return hipGetLastError();
 }
 

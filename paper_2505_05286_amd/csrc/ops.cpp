@@ -50,6 +50,12 @@ bool shapes_ok(int Hq, int Hkv, int dh) {
   return Hq > 0 && Hkv > 0 && Hq % Hkv == 0 && Hq / Hkv <= 16 && (dh == 64 || dh == 128);
 }
 
+// memcpy of a vector's elements; nothing for an empty one (whose data() may be null)
+template <typename T>
+void copy_vec(void* dst, const std::vector<T>& v) {
+  if (!v.empty()) std::memcpy(dst, v.data(), v.size() * sizeof(T));
+}
+
 }  // namespace
 
 extern "C" {
@@ -66,10 +72,16 @@ int64_t hxf_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
 }
 
 int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void* C, int32_t ldc, int32_t M, int32_t N,
-                int32_t K, int32_t epi, void* workspace, int64_t ws_bytes, void* stream) {
-  if (!A || !B || !C || M < 0 || N <= 0 || K <= 0 || K % 8 || lda < K || epi < 0 || epi > 3) return HXF_EINVAL;
+                int32_t K, int32_t flags, void* workspace, int64_t ws_bytes, void* stream) {
+  const int epi = flags & 0xFF;
+  const bool a_packed = flags & HXF_GEMM_A_PACKED, c_packed = flags & HXF_GEMM_C_PACKED;
+  if (flags & ~(0xFF | HXF_GEMM_A_PACKED | HXF_GEMM_C_PACKED)) return HXF_EINVAL;
+  if (!A || !B || !C || M < 0 || N <= 0 || K <= 0 || K % 8 || (!a_packed && lda < K) || epi < 0 || epi > 3)
+    return HXF_EINVAL;
   if (epi == HXF_EPI_SWIGLU && (!B2 || N % 32)) return HXF_EINVAL;
-  if (ldc < (epi == HXF_EPI_SWIGLU ? N / 2 : N)) return HXF_EINVAL;
+  if (!c_packed && ldc < (epi == HXF_EPI_SWIGLU ? N / 2 : N)) return HXF_EINVAL;
+  if ((a_packed || c_packed) && (M <= 512 || (a_packed && K % 32) || (c_packed && (epi != HXF_EPI_SWIGLU || N % 64))))
+    return HXF_EINVAL;
   if (M == 0) return HXF_OK;
   GemmPlan p = gemm_plan(M, N, K, 8, epi == HXF_EPI_SWIGLU);
   if (p.splits > 1 && (!workspace || ws_bytes < (int64_t)p.splits * M * N * 4)) return HXF_ENOMEM;
@@ -85,6 +97,8 @@ int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void*
   a.lda = lda;
   a.ldc = ldc;
   a.kt = (K + 31) / 32;
+  a.a_packed = a_packed ? 1 : 0;
+  a.c_kt = c_packed ? N / 64 : 0;
   return dev_rc(gemm_launch(a, epi, p, (hipStream_t)stream));
 }
 
@@ -159,8 +173,8 @@ int hxf_op_decode_plan(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* ctx, c
   *n_merges = (int32_t)P.merges.size();
   if ((int64_t)items_cap < (int64_t)P.items.size() || (int64_t)merges_cap < (int64_t)P.merges.size())
     return HXF_ENOMEM;
-  std::memcpy(items, P.items.data(), P.items.size() * sizeof(DecodeItem));
-  std::memcpy(merges, P.merges.data(), P.merges.size() * sizeof(MergeItem));
+  copy_vec(items, P.items);
+  copy_vec(merges, P.merges);
   return HXF_OK;
 }
 
@@ -179,8 +193,8 @@ int hxf_op_decode_attention(const void* q, const void* k_pool, const void* v_poo
   const DecodeLayout L = decode_layout(P, B, Hq, Hkv, dh);
   if (!workspace || ws_bytes < L.total) return HXF_ENOMEM;
   std::vector<uint8_t> host(L.off_o);
-  std::memcpy(host.data() + L.off_items, P.items.data(), P.items.size() * sizeof(DecodeItem));
-  std::memcpy(host.data() + L.off_merges, P.merges.data(), P.merges.size() * sizeof(MergeItem));
+  copy_vec(host.data() + L.off_items, P.items);
+  copy_vec(host.data() + L.off_merges, P.merges);
   auto* qrow = reinterpret_cast<int32_t*>(host.data() + L.off_qrow);
   for (int b = 0; b < B; ++b) qrow[b] = b;
   hipStream_t st = (hipStream_t)stream;
@@ -267,8 +281,8 @@ int hxf_op_prefill_plan(int32_t S, int32_t Hq, int32_t Hkv, const int32_t* pos0,
   *n_merges = (int32_t)P.merges.size();
   if ((int64_t)items_cap < (int64_t)P.items.size() || (int64_t)merges_cap < (int64_t)P.merges.size())
     return HXF_ENOMEM;
-  std::memcpy(items, P.items.data(), P.items.size() * sizeof(PrefillItem));
-  std::memcpy(merges, P.merges.data(), P.merges.size() * sizeof(PrefillMerge));
+  copy_vec(items, P.items);
+  copy_vec(merges, P.merges);
   return HXF_OK;
 }
 
@@ -293,8 +307,8 @@ int hxf_op_prefill_attention(const void* q, const void* k_pool, const void* v_po
   plan_prefill(entries, Hkv, qpi, P);
   const PrefillLayout L = prefill_layout(prefill_whole_items(S, Hkv, qpi, n_host), S, 128);
   std::vector<uint8_t> host(L.off_rp + (int64_t)S * 8);
-  std::memcpy(host.data(), P.items.data(), P.items.size() * sizeof(PrefillItem));
-  std::memcpy(host.data() + L.off_merges, P.merges.data(), P.merges.size() * sizeof(PrefillMerge));
+  copy_vec(host.data(), P.items);
+  copy_vec(host.data() + L.off_merges, P.merges);
   std::memcpy(host.data() + L.off_rp, row0, (size_t)S * 4);
   std::memcpy(host.data() + L.off_rp + S * 4, pos0, (size_t)S * 4);
   hipStream_t st = (hipStream_t)stream;

@@ -19,6 +19,7 @@ POLICY_PQ, POLICY_FCFS, POLICY_LLF = 0, 1, 2
 CLOCK_VIRTUAL, CLOCK_MEASURED = 0, 1
 EXEC_HIP, EXEC_NULL = 0, 1
 EPI_BF16, EPI_RESID, EPI_SWIGLU, EPI_F32 = 0, 1, 2, 3
+GEMM_A_PACKED, GEMM_C_PACKED = 0x100, 0x200   # layout flags or-ed into the epilogue (include/hxf_ops.h)
 
 
 class HxfError(RuntimeError):

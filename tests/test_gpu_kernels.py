@@ -98,6 +98,60 @@ def test_gemm_full_size_sampled(name, M_, N, K, epi):
     _gemm_case(M_, N, K, epi, seed=M_ + N + K, rows=rows)
 
 
+def _unpack_rows(packed_i16, M_, K):
+    """A packed-layout bf16 matrix (16 x 32 tiles, [k%32 / 8][r%16][k%8] inside) -> [M_, K] bits."""
+    kt = -(-K // 32)
+    m16 = -(-M_ // 16) * 16
+    a = packed_i16.detach().cpu().numpy().view(np.uint16)[:m16 * kt * 32]
+    return a.reshape(m16 // 16, kt, 4, 16, 8).transpose(0, 3, 1, 2, 4).reshape(m16, kt * 32)[:M_, :K]
+
+
+@pytest.mark.parametrize("M_,N,K,epi", [(2080, 6144, 4096, hxf.EPI_BF16), (2080, 4096, 4096, hxf.EPI_RESID),
+                                        (1031, 1000, 1408, hxf.EPI_F32), (600, 4096, 14336, hxf.EPI_RESID),
+                                        (513, 320, 32, hxf.EPI_BF16), (2080, 2 * 14336, 4096, hxf.EPI_SWIGLU),
+                                        (700, 2 * 1376, 512, hxf.EPI_SWIGLU)])
+def test_gemm_packed_activations(M_, N, K, epi):
+    """Prefill-sized GEMMs reading the activations in the packed tile layout give the
+    row-major call's result bit for bit; a SwiGLU output written packed holds the same values."""
+    t = torch()
+    rng = np.random.default_rng(M_ + N + K)
+    ab, _ = rand_bf16(rng, (M_, K))
+    rows = N // 2 if epi == hxf.EPI_SWIGLU else N
+    A = dev_bits(ab)
+    Ap = dev_packed(ab)                        # the activations through the weight packing kernel
+    Bs = [dev_packed(rand_bf16(rng, (rows, K), 0.05)[0]) for _ in range(2 if epi == hxf.EPI_SWIGLU else 1)]
+    B2 = Bs[-1].data_ptr() if len(Bs) > 1 else 0
+    f32 = epi in (hxf.EPI_RESID, hxf.EPI_F32)
+    base = rng.standard_normal((M_, rows)).astype(np.float32)
+
+    def out():
+        return (t.from_numpy(base.copy()).to("cuda:0") if f32 else t.zeros(M_ * rows, dtype=t.int16, device="cuda:0"))
+    log(f"gemm packed activations M={M_} N={N} K={K} epi={epi}")
+    ref, got = out(), out()
+    hxf.op_gemm(A.data_ptr(), K, Bs[0].data_ptr(), B2, ref.data_ptr(), rows, M_, N, K, epi)
+    hxf.op_gemm(Ap.data_ptr(), 0, Bs[0].data_ptr(), B2, got.data_ptr(), rows, M_, N, K, epi | hxf.GEMM_A_PACKED)
+    t.cuda.synchronize()
+    assert t.equal(ref, got)
+    if epi == hxf.EPI_SWIGLU:
+        cp = t.zeros(-(-M_ // 16) * 16 * rows, dtype=t.int16, device="cuda:0")
+        hxf.op_gemm(Ap.data_ptr(), 0, Bs[0].data_ptr(), B2, cp.data_ptr(), 0, M_, N, K,
+                    epi | hxf.GEMM_A_PACKED | hxf.GEMM_C_PACKED)
+        t.cuda.synchronize()
+        np.testing.assert_array_equal(_unpack_rows(cp, M_, rows), ref.cpu().numpy().view(np.uint16).reshape(M_, rows))
+
+
+def test_gemm_packed_flags_refused_off_their_shapes():
+    """The layout flags only where the big-tile kernel runs: M > 512, K % 32 == 0, SwiGLU for C."""
+    for M_, N, K, flags in ((512, 256, 256, hxf.EPI_BF16 | hxf.GEMM_A_PACKED),
+                            (1024, 256, 72, hxf.EPI_BF16 | hxf.GEMM_A_PACKED),
+                            (1024, 256, 256, hxf.EPI_BF16 | hxf.GEMM_C_PACKED),
+                            (1024, 2 * 688, 256, hxf.EPI_SWIGLU | hxf.GEMM_C_PACKED),
+                            (1024, 256, 256, hxf.EPI_BF16 | 0x400)):
+        with pytest.raises(hxf.HxfError) as e:
+            hxf.op_gemm(1, K, 1, 1, 1, N, M_, N, K, flags)
+        assert e.value.code == hxf.EINVAL
+
+
 @pytest.mark.parametrize("M_", [64, 256])
 def test_gemm_split_repeatable(M_):
     """Repeated split-K calls on one workspace give bit-identical results (the weight-
