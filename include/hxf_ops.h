@@ -46,10 +46,10 @@ enum { HXF_GEMM_A_PACKED = 0x100, HXF_GEMM_C_PACKED = 0x200 };
  * (split-K partials for M <= 512, enough for every epilogue; may be 0 bytes).
  * HXF_GEMM_A_PACKED: A is in the packed layout of the weights (hxf_op_pack_weight of the
  * row-major [M,K] activations, ceil(M/16)*16 rows; lda unused), so that a 16 x 32 block of
- * it is one contiguous kilobyte; M > 512 and K % 32 == 0 only.  HXF_GEMM_C_PACKED (SwiGLU,
- * M > 512, F % 32 == 0): C is written in that packed layout ([M,F] with ceil(F/32) tiles per
- * row tile; ldc unused), the form in which the down projection reads it.  Either flag on
- * another shape: HXF_EINVAL. */
+ * it is one contiguous kilobyte; K % 32 == 0 (and F % 32 == 0 for SwiGLU).
+ * HXF_GEMM_C_PACKED (SwiGLU, F % 32 == 0): C is written in that packed layout ([M,F] with
+ * F/32 tiles per row tile; ldc unused), the form in which the down projection reads it.
+ * Either flag on another shape: HXF_EINVAL. */
 int64_t hxf_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
 int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void* C, int32_t ldc, int32_t M, int32_t N,
                 int32_t K, int32_t epilogue, void* workspace, int64_t workspace_bytes, void* stream);

@@ -18,11 +18,7 @@ namespace hxf {
 namespace {
 
 constexpr int kMaxSplits = 8;
-// Iterations of more rows than this keep the GEMM activations (the normed hidden state,
-// the attention output, the SwiGLU output) in the packed tile layout of the weights, in
-// which a 16 x 32 block the prefill GEMMs stage is one contiguous kilobyte rather than 16
-// row pieces (the GEMMs of these sizes run on the big-tile kernel, which reads it).
-constexpr int kPackRows = 512;
+
 
 // memcpy of a vector's elements; nothing for an empty one (whose data() may be null)
 template <typename T>
@@ -105,8 +101,7 @@ WsPlan plan_workspace(const hxf_model_cfg& m, const hxf_sched_cfg& s) {
   p.off_meta = take(p.meta_bytes);
   p.off_rope = take((int64_t)m.max_context * (dh / 2) * 8);
   p.off_resid = take(p.t_max * d * 4);
-  // the GEMM activations of prefill-sized iterations are stored in the packed tile layout,
-  // whole 16-row tiles
+  // the GEMM activations are stored in the packed tile layout: whole 16-row tiles
   const int64_t t16 = (p.t_max + 15) / 16 * 16;
   p.off_h = take(t16 * d * 2);
   p.off_qkv = take(p.t_max * qkv * 2);
@@ -185,8 +180,7 @@ class HipExecutor : public Executor {
   // With `pending` set, a split-K plan leaves its partials in the workspace and
   // *pending = its split count (0 when the GEMM finished its own epilogue).
   // `kind` (HXF_PROF_*) names the projection for profiling.
-  // a_packed: A in the packed tile layout; c_kt > 0: the SwiGLU output packed (both only
-  // for prefill-sized M, see kPackRows).
+  // a_packed: A in the packed tile layout; c_kt > 0: the SwiGLU output packed.
   int gemm(const uint16_t* A, int lda, const uint16_t* B, const uint16_t* B2, void* C, int ldc, int M, int N, int K,
            int epi, int kind, std::string& err, int* pending = nullptr, bool a_packed = false, int c_kt = 0);
   // A pair of events for a profiled launch of `kind` (0-4 GEMMs, 5 prefill attention)
@@ -441,7 +435,10 @@ int HipExecutor::run(const std::vector<BatchEntry>& batch, std::vector<int32_t>&
   uint16_t* act = dev<uint16_t>(plan_.off_act);
   const float2* rope = dev<float2>(plan_.off_rope);
   const float scale_log2 = 1.4426950408889634f / std::sqrt((float)dh);
-  const bool pack = T > kPackRows && d % 32 == 0 && f % 32 == 0 && (hq * dh) % 32 == 0;
+  // The GEMM activations (the normed hidden state, the attention output, the SwiGLU output)
+  // are kept in the packed tile layout of the weights, in which a 16 x 32 block the GEMMs
+  // stage is one contiguous kilobyte rather than 16 row pieces, when the widths allow it.
+  const bool pack = d % 32 == 0 && f % 32 == 0 && (hq * dh) % 32 == 0;
   const int kt_h = pack ? d / 32 : 0, kt_attn = pack ? hq * dh / 32 : 0, kt_act = pack ? f / 32 : 0;
   const int64_t layer_pool = (int64_t)s_.n_blocks * hkv * kPage * dh;   // bf16 elements per K (or V) pool
   uint16_t* pool = reinterpret_cast<uint16_t*>(b_.kv_pool);

@@ -245,7 +245,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int S) {
       g += a.partial[z * MN + (size_t)row * a.N + lg];
       u += a.partial[z * MN + (size_t)row * a.N + lg + 16];
     }
-    reinterpret_cast<bf16_t*>(a.C)[(size_t)row * a.ldc + col] = f2bf(g / (1.f + __expf(-g)) * u);
+    reinterpret_cast<bf16_t*>(a.C)[a.c_kt ? packed_elem(row, col, a.c_kt) : (size_t)row * a.ldc + col] =
+        f2bf(g / (1.f + __expf(-g)) * u);
     return;
   }
   float s = 0.f;
@@ -312,20 +313,23 @@ __global__ __launch_bounds__(64 * ST_WV) void gemm_stream_kernel(GemmArgs a) {
   for (int j = 0; j < NTW; ++j) bsrc[j] = b_row(a, min(c0 + j * 16, a.N - 1) & ~15, SW) + lane * 8;
   // A block b = (row tile b / KB, 32-column block b % KB): lane reads row 16 (b / KB) + r
   // (rows past M repeat M-1)
+  // packed activations: the block's row tile (past M: the last one) with the lane's offset
   const bf16_t* arow[A_PER_W];
   int ablk[A_PER_W];
 #pragma unroll
   for (int u = 0; u < A_PER_W; ++u) {
     ablk[u] = min(w * A_PER_W + u, A_BLK - 1);
-    arow[u] = a.A + (size_t)min((ablk[u] / KB) * 16 + r, a.M - 1) * a.lda;
+    arow[u] = a.a_packed ? a.A + (size_t)min(ablk[u] / KB, (a.M - 1) / 16) * a.kt * 512 + lane * 8
+                         : a.A + (size_t)min((ablk[u] / KB) * 16 + r, a.M - 1) * a.lda;
   }
   auto issue = [&](int s, bf16_t* base) {
     const int k0 = kb + min(s, nst - 1) * KS;               // past the last stage: reload it (never read)
 #pragma unroll
     for (int u = 0; u < A_PER_W; ++u) {
       const int kk = ablk[u] % KB;
-      const int k = min(k0 + kk * 32 + g * 8, a.K - 8);      // stays in the row; the weights are zero past K
-      dma16(arow[u] + k, base + ablk[u] * 512);
+      // row-major: stays in the row (the weights are zero past K); packed: a whole tile
+      const size_t off = a.a_packed ? (size_t)min(k0 / 32 + kk, a.kt - 1) * 512 : (size_t)min(k0 + kk * 32 + g * 8, a.K - 8);
+      dma16(arow[u] + off, base + ablk[u] * 512);
     }
 #pragma unroll
     for (int j = 0; j < NTW; ++j)
@@ -407,7 +411,9 @@ __global__ __launch_bounds__(64 * ST_WV) void gemm_stream_kernel(GemmArgs a) {
           const int cq = c0 + q * 32;
           if (cq >= a.N) continue;
           const float gt = acc[i][2 * q][e], up = acc[i][2 * q + 1][e];
-          reinterpret_cast<bf16_t*>(a.C)[(size_t)row * a.ldc + (cq >> 5) * 16 + r] = f2bf(gt / (1.f + __expf(-gt)) * up);
+          const int oc = (cq >> 5) * 16 + r;
+          reinterpret_cast<bf16_t*>(a.C)[a.c_kt ? packed_elem(row, oc, a.c_kt) : (size_t)row * a.ldc + oc] =
+              f2bf(gt / (1.f + __expf(-gt)) * up);
         }
       } else {
 #pragma unroll
@@ -852,9 +858,10 @@ GemmPlan gemm_plan(int M, int N, int K, int max_splits, bool swiglu) {
 
 hipError_t gemm_launch(const GemmArgs& a, int epi, const GemmPlan& p, hipStream_t st, bool reduce, hipEvent_t e0,
                        hipEvent_t e1) {
-  // packed activations in or SwiGLU output packed: the big-tile kernel without split K only
-  if ((a.a_packed || a.c_kt) && (!p.big || p.splits > 1 || (epi == EPI_SWIGLU && a.N % 64 != 0) ||
-                                 (a.c_kt && (epi != EPI_SWIGLU || a.c_kt * 64 != a.N)) || (a.a_packed && a.K % 32)))
+  // packed activations in, or a packed SwiGLU output: the streaming and the big-tile kernels
+  // (and the split-K reduction) with K % 32 == 0 and F % 32 == 0
+  if ((a.a_packed && (a.K % 32 || !(p.stream || p.big) || (epi == EPI_SWIGLU && a.N % 64 != 0))) ||
+      (a.c_kt && (!(p.stream || p.big) || epi != EPI_SWIGLU || a.N % 64 != 0 || a.c_kt * 64 != a.N)))
     return hipErrorInvalidValue;
   switch (epi) {
     case EPI_BF16: return launch_epi<EPI_BF16>(a, p, st, reduce, e0, e1);

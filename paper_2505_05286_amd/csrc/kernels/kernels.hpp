@@ -44,7 +44,7 @@ struct GemmArgs {
   int lda, ldc;
   int k_chunk;
   int kt;              // K tiles of the packed weights, ceil(K / 32)
-  int a_packed;        // A is in the packed tile layout (lda unused); the big-tile kernel only
+  int a_packed;        // A is in the packed tile layout (lda unused); streaming and big-tile kernels
   int c_kt;            // SwiGLU: > 0 writes C in the packed tile layout with c_kt tiles per row tile
 };
 

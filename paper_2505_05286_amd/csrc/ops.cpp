@@ -80,7 +80,7 @@ int hxf_op_gemm(const void* A, int32_t lda, const void* B, const void* B2, void*
     return HXF_EINVAL;
   if (epi == HXF_EPI_SWIGLU && (!B2 || N % 32)) return HXF_EINVAL;
   if (!c_packed && ldc < (epi == HXF_EPI_SWIGLU ? N / 2 : N)) return HXF_EINVAL;
-  if ((a_packed || c_packed) && (M <= 512 || (a_packed && K % 32) || (c_packed && (epi != HXF_EPI_SWIGLU || N % 64))))
+  if ((a_packed && (K % 32 || (epi == HXF_EPI_SWIGLU && N % 64))) || (c_packed && (epi != HXF_EPI_SWIGLU || N % 64)))
     return HXF_EINVAL;
   if (M == 0) return HXF_OK;
   GemmPlan p = gemm_plan(M, N, K, 8, epi == HXF_EPI_SWIGLU);

@@ -109,10 +109,16 @@ def _unpack_rows(packed_i16, M_, K):
 @pytest.mark.parametrize("M_,N,K,epi", [(2080, 6144, 4096, hxf.EPI_BF16), (2080, 4096, 4096, hxf.EPI_RESID),
                                         (1031, 1000, 1408, hxf.EPI_F32), (600, 4096, 14336, hxf.EPI_RESID),
                                         (513, 320, 32, hxf.EPI_BF16), (2080, 2 * 14336, 4096, hxf.EPI_SWIGLU),
-                                        (700, 2 * 1376, 512, hxf.EPI_SWIGLU)])
+                                        (700, 2 * 1376, 512, hxf.EPI_SWIGLU), (64, 6144, 4096, hxf.EPI_BF16),
+                                        (64, 4096, 14336, hxf.EPI_RESID), (17, 1000, 1024, hxf.EPI_F32),
+                                        (64, 2 * 14336, 4096, hxf.EPI_SWIGLU), (33, 2 * 2048, 4096, hxf.EPI_SWIGLU),
+                                        (256, 6144, 4096, hxf.EPI_BF16), (256, 4096, 14336, hxf.EPI_RESID),
+                                        (256, 2 * 14336, 4096, hxf.EPI_SWIGLU), (129, 4096, 4096, hxf.EPI_F32),
+                                        (96, 20000, 256, hxf.EPI_F32)])
 def test_gemm_packed_activations(M_, N, K, epi):
-    """Prefill-sized GEMMs reading the activations in the packed tile layout give the
-    row-major call's result bit for bit; a SwiGLU output written packed holds the same values."""
+    """GEMMs reading the activations in the packed tile layout (the streaming kernel at decode
+    sizes, the big-tile kernel with or without split K above) give the row-major call's result
+    bit for bit; a SwiGLU output written packed holds the same values."""
     t = torch()
     rng = np.random.default_rng(M_ + N + K)
     ab, _ = rand_bf16(rng, (M_, K))
@@ -128,22 +134,26 @@ def test_gemm_packed_activations(M_, N, K, epi):
         return (t.from_numpy(base.copy()).to("cuda:0") if f32 else t.zeros(M_ * rows, dtype=t.int16, device="cuda:0"))
     log(f"gemm packed activations M={M_} N={N} K={K} epi={epi}")
     ref, got = out(), out()
-    hxf.op_gemm(A.data_ptr(), K, Bs[0].data_ptr(), B2, ref.data_ptr(), rows, M_, N, K, epi)
-    hxf.op_gemm(Ap.data_ptr(), 0, Bs[0].data_ptr(), B2, got.data_ptr(), rows, M_, N, K, epi | hxf.GEMM_A_PACKED)
+    wsn = hxf.op_gemm_workspace_bytes(M_, N, K)
+    ws = t.empty(max(wsn, 256), dtype=t.uint8, device="cuda:0")
+    hxf.op_gemm(A.data_ptr(), K, Bs[0].data_ptr(), B2, ref.data_ptr(), rows, M_, N, K, epi, ws.data_ptr(), wsn)
+    hxf.op_gemm(Ap.data_ptr(), 0, Bs[0].data_ptr(), B2, got.data_ptr(), rows, M_, N, K, epi | hxf.GEMM_A_PACKED,
+                ws.data_ptr(), wsn)
     t.cuda.synchronize()
     assert t.equal(ref, got)
     if epi == hxf.EPI_SWIGLU:
         cp = t.zeros(-(-M_ // 16) * 16 * rows, dtype=t.int16, device="cuda:0")
         hxf.op_gemm(Ap.data_ptr(), 0, Bs[0].data_ptr(), B2, cp.data_ptr(), 0, M_, N, K,
-                    epi | hxf.GEMM_A_PACKED | hxf.GEMM_C_PACKED)
+                    epi | hxf.GEMM_A_PACKED | hxf.GEMM_C_PACKED, ws.data_ptr(), wsn)
         t.cuda.synchronize()
         np.testing.assert_array_equal(_unpack_rows(cp, M_, rows), ref.cpu().numpy().view(np.uint16).reshape(M_, rows))
 
 
 def test_gemm_packed_flags_refused_off_their_shapes():
-    """The layout flags only where the big-tile kernel runs: M > 512, K % 32 == 0, SwiGLU for C."""
-    for M_, N, K, flags in ((512, 256, 256, hxf.EPI_BF16 | hxf.GEMM_A_PACKED),
+    """The layout flags need K % 32 == 0 (packed activations), SwiGLU with F % 32 == 0 (packed output)."""
+    for M_, N, K, flags in ((64, 256, 72, hxf.EPI_BF16 | hxf.GEMM_A_PACKED),
                             (1024, 256, 72, hxf.EPI_BF16 | hxf.GEMM_A_PACKED),
+                            (64, 2 * 688, 256, hxf.EPI_SWIGLU | hxf.GEMM_A_PACKED),
                             (1024, 256, 256, hxf.EPI_BF16 | hxf.GEMM_C_PACKED),
                             (1024, 2 * 688, 256, hxf.EPI_SWIGLU | hxf.GEMM_C_PACKED),
                             (1024, 256, 256, hxf.EPI_BF16 | 0x400)):
