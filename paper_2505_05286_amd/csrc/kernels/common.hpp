@@ -78,6 +78,10 @@ typedef __attribute__((address_space(1))) void* global_ptr_t;
 __device__ __forceinline__ void dma16(const void* g, void* lds_block) {
   __builtin_amdgcn_global_load_lds((global_ptr_t)g, (lds_ptr_t)lds_block, 16, 0, 0);
 }
+// The same with the non-temporal hint (data read once: the decode GEMMs' weight stream)
+__device__ __forceinline__ void dma16_nt(const void* g, void* lds_block) {
+  __builtin_amdgcn_global_load_lds((global_ptr_t)g, (lds_ptr_t)lds_block, 16, 0, 2);
+}
 
 // s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding)
 template <int N>
