@@ -374,23 +374,25 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
     }
   }
 
-  // DMA of key tile t into a stage: the two K pages, then the two V pages, as stored
-  auto issue = [&](int t, bf16_t* base) __attribute__((always_inline)) {
+  // DMA of key tile t into a stage: the two K pages, then the two V pages, as stored.  A
+  // wavefront's blocks all lie in one page of the tile (pg), whose block-table entry the
+  // caller passes in (read one step ahead, see below).
+  static_assert(K_W == V_W && (KT / 1024) % K_W == 0, "a wavefront's blocks in one page");
+  const int pg = (w * K_W) / (KT / 1024);
+  auto entry_of = [&](int t) __attribute__((always_inline)) {
     const int tt = tbase + min(t, ntiles - 1);
+    return bt[min(tt * 2 + pg, last_page)];
+  };
+  auto issue = [&](int entry, bf16_t* base) __attribute__((always_inline)) {
+    const size_t tile = kv_tile(it.kvh, a.n_blocks, entry, DH);
 #pragma unroll
     for (int u = 0; u < K_W; ++u) {
       const int blk = w * K_W + u;               // 1 KB block of the K tile
-      const int pg = blk / (KT / 1024);          // page of the tile (each page is KT / 2 elements)
-      const int page = min(tt * 2 + pg, last_page);
-      const size_t tile = kv_tile(it.kvh, a.n_blocks, bt[page], DH);
       dma16(a.k_pool + tile + (blk % (KT / 1024)) * 512 + lane * 8, base + blk * 512);
     }
 #pragma unroll
     for (int u = 0; u < V_W; ++u) {
       const int blk = w * V_W + u;               // 1 KB block of the V tile
-      const int pg = blk / (KT / 1024);
-      const int page = min(tt * 2 + pg, last_page);
-      const size_t tile = kv_tile(it.kvh, a.n_blocks, bt[page], DH);
       // the two 16-byte halves of dims 8..15 (mod 16) of a block swap places in LDS, so that
       // the 16 lanes of one V^T read pass hit distinct banks
       dma16(a.v_pool + tile + (blk % (KT / 1024)) * 512 + (lane ^ ((lane >> 4) & 1)) * 8, base + KT + blk * 512);
@@ -416,18 +418,27 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   const int k_off = ((lane & 31) >> 4) * (KT / 2) + (lane & 15) * 8 + h * 128;
   const int v_off = KT + (lane & 31) * 16 + (h ^ ((lane >> 3) & 1)) * 8;
 
+  // One key tile.  Every LDS operand of the tile is requested first: the K fragments feed
+  // the QK^T chain as they arrive, and the V^T fragments are in registers by the time the
+  // softmax is done, so a wavefront alone on its SIMD does not wait on LDS between MFMAs.
   auto compute = [&](const bf16_t* base, int t) __attribute__((always_inline)) {
+    bf16x8 kf[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(base + k_off + ks * 256));
+    uint4 vv[2][DT];
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) vv[st][dt] = *reinterpret_cast<const uint4*>(base + v_off + (st * DH + dt * 32) * 16);
     f32x16 s[PT];
 #pragma unroll
     for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[pt][e] = 0.f;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 kf = as_bf16x8(*reinterpret_cast<const uint4*>(base + k_off + ks * 256));
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int pt = 0; pt < PT; ++pt) s[pt] = mfma32x32x16(kf, qf[pt][ks], s[pt]);
-    }
+      for (int pt = 0; pt < PT; ++pt) s[pt] = mfma32x32x16(kf[ks], qf[pt][ks], s[pt]);
     const int k0 = (tbase + t) * 32;
     const bool edge = (k0 + 32 > kend) || (k0 + 31 > pos0 + it.q0);   // wavefront-uniform: a mask is needed
     if (edge) {
@@ -448,8 +459,7 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
       float v = s[pt][0];
 #pragma unroll
       for (int r = 1; r < 16; ++r) v = fmaxf(v, s[pt][r]);
-      v = fmaxf(v, __shfl_xor(v, 32, kWave));
-      mx[pt] = v * a.scale_log2;
+      mx[pt] = half_swap_max(v) * a.scale_log2;
     }
     bool grow = false;
 #pragma unroll
@@ -487,31 +497,44 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
       }
     }
     // V^T . P^T; past the end of the context the V entries are zeroed (garbage may be NaN)
+    if (k0 + 32 > kend) {
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      const int tok0 = k0 + st * 16 + h * 4;      // keys of this lane's k slots: tok0 + 0..3, tok0 + 8..11
+      for (int st = 0; st < 2; ++st) {
+        const int tok0 = k0 + st * 16 + h * 4;    // keys of this lane's k slots: tok0 + 0..3, tok0 + 8..11
+        const uint2 lo = keep_mask(kend - tok0), hi = keep_mask(kend - tok0 - 8);
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        uint4 vv = *reinterpret_cast<const uint4*>(base + v_off + (st * DH + dt * 32) * 16);
-        if (k0 + 32 > kend) {
-          const uint2 lo = keep_mask(kend - tok0), hi = keep_mask(kend - tok0 - 8);
-          vv.x &= lo.x; vv.y &= lo.y; vv.z &= hi.x; vv.w &= hi.y;
+        for (int dt = 0; dt < DT; ++dt) {
+          vv[st][dt].x &= lo.x;
+          vv[st][dt].y &= lo.y;
+          vv[st][dt].z &= hi.x;
+          vv[st][dt].w &= hi.y;
         }
-#pragma unroll
-        for (int pt = 0; pt < PT; ++pt) o[pt][dt] = mfma32x32x16(as_bf16x8(vv), pf[pt][st], o[pt][dt]);
       }
     }
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) o[pt][dt] = mfma32x32x16(as_bf16x8(vv[st][dt]), pf[pt][st], o[pt][dt]);
   };
 
-  static_for<NS - 1>([&](auto ic) { issue(decltype(ic)::value, slot(ic)); });
+  // The block-table entry of the DMA issued at a step is loaded at the end of the step
+  // before (a scalar load that the wait at the loop head drains together with the DMA
+  // wait), so that no LDS read waits on it.
+  static_for<NS - 1>([&](auto ic) { issue(entry_of(decltype(ic)::value), slot(ic)); });
+  int next_entry = entry_of(NS - 1);
   int t0 = 0;
   for (; t0 + NS <= ntiles; t0 += NS) {
     static_for<NS>([&](auto ic) {
       constexpr int J = decltype(ic)::value;
-      wait_vmcnt<(NS - 2) * PER_W>();
+      wait_vmcnt_lgkm0<(NS - 2) * PER_W>();
       __builtin_amdgcn_s_barrier();
-      issue(t0 + J + NS - 1, slot(std::integral_constant<int, J + NS - 1>{}));
+      issue(next_entry, slot(std::integral_constant<int, J + NS - 1>{}));
+      __builtin_amdgcn_sched_barrier(0);   // the DMAs go out before this tile's LDS reads
       compute(slot(ic), t0 + J);
+      __builtin_amdgcn_sched_barrier(0);
+      next_entry = entry_of(t0 + J + NS);
     });
   }
   wait_vmcnt<0>();

@@ -78,6 +78,79 @@ __global__ __launch_bounds__(NT) void rmsnorm_kernel(float* x, const int32_t* ro
   norm_store<NT>(x4, g, out, r, out_kt, d, eps, red);
 }
 
+// Many rows (prefill-sized iterations): one wavefront per row, four rows per workgroup.
+// The row's V float4 per lane are loaded together and kept in registers, so the second
+// pass (scale and store) reads no memory and every wavefront has its whole row in flight.
+// The residual update sums the S partials of an element in split order, as above; the
+// sum of squares is the lane's own V elements, then a wavefront sum.
+template <int S, int V>
+__global__ __launch_bounds__(256) void rmsnorm_rows_kernel(float* x, const int32_t* rows, const float* part,
+                                                          int part_rows, const uint16_t* g, uint16_t* out, int n_rows,
+                                                          int d, float eps, int out_kt) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= n_rows) return;
+  const int lane = threadIdx.x & 63;
+  const int src = rows ? rows[r] : r;
+  float4* x4 = reinterpret_cast<float4*>(x + (size_t)src * d);
+  float4 v[V];
+#pragma unroll
+  for (int j = 0; j < V; ++j) v[j] = x4[j * 64 + lane];
+  if constexpr (S > 0) {
+    const float4* p4 = reinterpret_cast<const float4*>(part + (size_t)src * d);
+    const size_t zs = (size_t)part_rows * d / 4;
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      float4 q[S];
+#pragma unroll
+      for (int z = 0; z < S; ++z) q[z] = p4[z * zs + j * 64 + lane];
+      float4 sm = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int z = 0; z < S; ++z) {
+        sm.x += q[z].x; sm.y += q[z].y; sm.z += q[z].z; sm.w += q[z].w;
+      }
+      v[j].x += sm.x; v[j].y += sm.y; v[j].z += sm.z; v[j].w += sm.w;
+      x4[j * 64 + lane] = v[j];
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < V; ++j) ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
+  const float rs = rsqrtf(wave_sum(ss) / (float)d + eps);
+  const uint2* g2 = reinterpret_cast<const uint2*>(g);
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int i = j * 64 + lane;
+    const uint2 gg = g2[i];
+    const float g0 = bf2f(gg.x & 0xFFFF), g1 = bf2f(gg.x >> 16), g2v = bf2f(gg.y & 0xFFFF), g3 = bf2f(gg.y >> 16);
+    const size_t o = out_kt ? packed_elem(r, 4 * i, out_kt) : (size_t)r * d + 4 * i;
+    *reinterpret_cast<uint2*>(out + o) =
+        make_uint2(pack_bf2(v[j].x * rs * g0, v[j].y * rs * g1), pack_bf2(v[j].z * rs * g2v, v[j].w * rs * g3));
+  }
+}
+
+template <int S>
+hipError_t rmsnorm_rows_launch(float* x, const float* part, int part_rows, const int32_t* rows, const uint16_t* g,
+                               uint16_t* out, int n_rows, int d, float eps, hipStream_t st, int out_kt) {
+  const dim3 grid((n_rows + 3) / 4);
+#define HXF_ROWS(VV)                                                                                          \
+  case VV:                                                                                                    \
+    hipLaunchKernelGGL((rmsnorm_rows_kernel<S, VV>), grid, dim3(256), 0, st, x, rows, part, part_rows, g, out, \
+                       n_rows, d, eps, out_kt);                                                               \
+    return hipGetLastError();
+  switch (d / 256) {
+    HXF_ROWS(4) HXF_ROWS(8) HXF_ROWS(16) HXF_ROWS(20) HXF_ROWS(24) HXF_ROWS(32)
+  }
+#undef HXF_ROWS
+  return hipErrorNotSupported;
+}
+
+// d / 256 float4 per lane for which the one-wavefront-per-row kernel is built
+inline bool rows_kernel_fits(int d, int S) {
+  if (d % 256 || S > 4) return false;
+  const int v = d / 256;
+  return v == 4 || v == 8 || v == 16 || v == 20 || v == 24 || v == 32;
+}
+
 __global__ __launch_bounds__(256) void embed_rmsnorm_kernel(const int32_t* ids, const uint16_t* E, const uint16_t* g,
                                                             float* resid, uint16_t* out, int d, float eps, int out_kt) {
   __shared__ float red[4];
@@ -104,6 +177,15 @@ hipError_t resid_rmsnorm_launch(float* x, const float* part, int S, int part_row
                                 int out_kt) {
   if (n_rows <= 0) return hipSuccess;
   if (out_kt && (d % 32 || out_kt != d / 32)) return hipErrorInvalidValue;
+  if (n_rows > 256 && rows_kernel_fits(d, S)) {
+    switch (S) {
+      case 0: return rmsnorm_rows_launch<0>(x, part, part_rows, rows, g, out, n_rows, d, eps, st, out_kt);
+      case 1: return rmsnorm_rows_launch<1>(x, part, part_rows, rows, g, out, n_rows, d, eps, st, out_kt);
+      case 2: return rmsnorm_rows_launch<2>(x, part, part_rows, rows, g, out, n_rows, d, eps, st, out_kt);
+      case 3: return rmsnorm_rows_launch<3>(x, part, part_rows, rows, g, out, n_rows, d, eps, st, out_kt);
+      case 4: return rmsnorm_rows_launch<4>(x, part, part_rows, rows, g, out, n_rows, d, eps, st, out_kt);
+    }
+  }
 #define HXF_NORM(SS)                                                                                        \
   case SS:                                                                                                  \
     if (n_rows <= 256)                                                                                      \

@@ -182,7 +182,10 @@ def test_gemm_split_repeatable(M_):
     assert t.equal(outs[0], outs[1]) and t.equal(outs[0], outs[2])
 
 
-@pytest.mark.parametrize("d,rows", [(256, 7), (4096, 64), (5120, 33)])
+# rows // 2 + 1 rows are normed: up to 256 one workgroup per row, above that one wavefront per
+# row for d / 256 in {4, 8, 16, 20, 24, 32} (3072: the per-workgroup kernel at 301 rows)
+@pytest.mark.parametrize("d,rows", [(256, 7), (4096, 64), (5120, 33), (4096, 600), (5120, 520), (8192, 1040),
+                                    (1024, 1000), (3072, 600)])
 def test_rmsnorm_and_embed(d, rows):
     t = torch()
     rng = np.random.default_rng(d + rows)
