@@ -58,6 +58,49 @@ __global__ __launch_bounds__(NT) void rmsnorm_kernel(float* x, const int32_t* ro
   const int r = blockIdx.x;
   const int src = rows ? rows[r] : r;
   float4* x4 = reinterpret_cast<float4*>(x + (size_t)src * d);
+  const int n4 = d >> 2;
+  if (n4 <= 2 * NT) {
+    // at most two float4 per thread (d <= 8 NT): kept in registers between the two passes,
+    // the same arithmetic in the same order as the loop below
+    float4 v[2];
+    float ss = 0.f;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int i = threadIdx.x + u * NT;
+      if (i >= n4) continue;
+      if constexpr (S > 0) {
+        const float4* p4 = reinterpret_cast<const float4*>(part + (size_t)src * d);
+        const size_t zs = (size_t)part_rows * d / 4;
+        float4 q[S];
+#pragma unroll
+        for (int z = 0; z < S; ++z) q[z] = p4[z * zs + i];
+        float4 sm = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int z = 0; z < S; ++z) {
+          sm.x += q[z].x; sm.y += q[z].y; sm.z += q[z].z; sm.w += q[z].w;
+        }
+        v[u] = x4[i];
+        v[u].x += sm.x; v[u].y += sm.y; v[u].z += sm.z; v[u].w += sm.w;
+        x4[i] = v[u];
+      } else {
+        v[u] = x4[i];
+      }
+      ss += v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w;
+    }
+    const float rs = rsqrtf(block_sum<NT>(ss, red) / (float)d + eps);
+    const uint2* g2 = reinterpret_cast<const uint2*>(g);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int i = threadIdx.x + u * NT;
+      if (i >= n4) continue;
+      const uint2 gg = g2[i];
+      const float g0 = bf2f(gg.x & 0xFFFF), g1 = bf2f(gg.x >> 16), g2v = bf2f(gg.y & 0xFFFF), g3 = bf2f(gg.y >> 16);
+      const size_t o = out_kt ? packed_elem(r, 4 * i, out_kt) : (size_t)r * d + 4 * i;
+      *reinterpret_cast<uint2*>(out + o) =
+          make_uint2(pack_bf2(v[u].x * rs * g0, v[u].y * rs * g1), pack_bf2(v[u].z * rs * g2v, v[u].w * rs * g3));
+    }
+    return;
+  }
   if constexpr (S > 0) {
     const float4* p4 = reinterpret_cast<const float4*>(part + (size_t)src * d);
     const size_t zs = (size_t)part_rows * d / 4;
