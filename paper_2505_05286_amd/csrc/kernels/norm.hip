@@ -1,5 +1,6 @@
-// RMSNorm over the fp32 residual stream (one workgroup per row, fp32 math,
-// bf16 output), optionally fused with the token-embedding gather.
+// RMSNorm over the fp32 residual stream (one workgroup per row up to 256 rows, one
+// wavefront per row beyond; fp32 math, bf16 output), optionally fused with the
+// token-embedding gather.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -50,7 +51,8 @@ __device__ __forceinline__ void norm_store(const float4* x4, const uint16_t* g, 
 // GEMM's own reduction would have, and the updated row is stored back.  The S
 // partial loads of an element are independent and issued together.  NT threads per
 // row: 1024 for the few rows of a decode batch (one round of loads per row instead of
-// four), 256 otherwise.
+// four), 256 for more rows whose width or split count the one-wavefront kernel below
+// is not built for.
 template <int S, int NT>
 __global__ __launch_bounds__(NT) void rmsnorm_kernel(float* x, const int32_t* rows, const float* part, int part_rows,
                                                      const uint16_t* g, uint16_t* out, int d, float eps, int out_kt) {
