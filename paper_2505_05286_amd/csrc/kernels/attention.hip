@@ -314,17 +314,17 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeAttnArgs a) {
 }
 
 // Chunked-prefill causal attention, one workgroup per (chunk, kv-head, block of
-// 256/G queries): the 256 (query, head) pairs of the block are the columns of
+// 128·PT/G queries): the 128·PT (query, head) pairs of the block are the columns of
 //   S^T[32 keys x 32 pairs] = K[32 x dh] . Q^T[dh x 32]       (v_mfma_f32_32x32x16_bf16)
 //   O^T[32 dims x 32 pairs] += V^T[32 x 32 keys] . P^T[32 x 32]
-// (64 pairs per wavefront, two 32-pair tiles).  Tiles of 32 keys (two pages)
-// of K and V are moved into LDS by the DMA path, five tiles in flight, and
-// shared by the four wavefronts.  A lane of the S^T accumulator holds keys
-// 8m + 4h + i (h = lane / 32) of its pair; taken in the order m = 2s, 2s + 1
-// these are the 8 keys of the P^T operand for the 16-key step s (page s of the
-// tile); the V pool stores each page row with its tokens in that order (see
+// (PT tiles of 32 pairs per wavefront; the library launches PT = 1, 128 pairs per
+// workgroup).  Tiles of 32 keys (two pages) of K and V are moved into LDS by the DMA
+// path, five tiles in flight, and shared by the four wavefronts.  A lane of the S^T
+// accumulator holds keys 8m + 4h + i (h = lane / 32) of its pair; taken in the order
+// m = 2s, 2s + 1 these are the 8 keys of the P^T operand for the 16-key step s (page s
+// of the tile); the V pool stores each page row with its tokens in that order (see
 // v_pos), so the V^T operand of a lane is one contiguous 16-byte LDS read.  Softmax is
-// online in log2 units, one cross-lane exchange (xor 32) per tile for the max.
+// online in log2 units, one exchange of the wavefront halves per tile for the max.
 template <int DH, int PT>
 __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
   constexpr int KS = DH / 16;                  // 16-dim steps of QK^T
@@ -357,7 +357,7 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
       (const __attribute__((address_space(4))) int32_t*)(a.bt + (size_t)it.entry * a.bt_stride);
   const int h = lane >> 5;
 
-  // this lane's two pairs (columns lane % 32 of the wavefront's two pair tiles)
+  // this lane's pairs (column lane % 32 of each of the wavefront's PT pair tiles)
   int qpos[PT];
   bf16x8 qf[PT][KS];
 #pragma unroll
@@ -451,7 +451,7 @@ __global__ __launch_bounds__(256) void prefill_flash_kernel(PrefillAttnArgs a) {
         }
     }
     // raw-score maxima (the scale is positive), then one wavefront-wide decision for
-    // both pair tiles: the reference max only moves when a score exceeds it by more
+    // all pair tiles: the reference max only moves when a score exceeds it by more
     // than 2^8 (the exponentials then stay below 256, harmless in fp32 and bf16)
     float mx[PT];
 #pragma unroll
