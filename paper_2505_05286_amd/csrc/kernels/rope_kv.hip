@@ -43,12 +43,13 @@ __device__ __forceinline__ void proj_values4(const uint16_t* row, const float* p
 template <int S>
 __global__ __launch_bounds__(64) void rope_kv_kernel(uint16_t* qkv, const float* part, int T, const int32_t* pos,
                                                      const int32_t* slot, const float2* cs, uint16_t* k_pool,
-                                                     uint16_t* v_pool, int64_t n_blocks, int Hq, int Hkv, int dh) {
+                                                     uint16_t* v_pool, int64_t n_blocks, int Hq, int Hkv, int dh,
+                                                     int write_v) {
   const int t = blockIdx.x;
   const int h = blockIdx.y * 4 + (threadIdx.x >> 4);
   const int half = dh >> 1;
   const int i = (threadIdx.x & 15) * 4;
-  if (h >= Hq + 2 * Hkv || i >= half) return;
+  if (h >= Hq + 2 * Hkv || i >= half || (!write_v && h >= Hq + Hkv)) return;
   const int width = (Hq + 2 * Hkv) * dh;
   uint16_t* row = qkv + (size_t)t * width;
   const float* prow = part + (size_t)t * width;
@@ -59,7 +60,7 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(uint16_t* qkv, const float*
   proj_values4<S>(row, prow, zs, h * dh + i + half, b, rb);
   const int s = slot[t];
   const int blk = s / kPage, off = s % kPage;
-  if (h >= Hq + Hkv) {                                     // v: no rotation
+  if (h >= Hq + Hkv) {                                     // v: no rotation (write_v == 1 only)
     uint16_t* vp = v_pool + kv_tile(h - Hq - Hkv, n_blocks, blk, dh);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -90,6 +91,48 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(uint16_t* qkv, const float*
   }
 }
 
+// The V rows of prefill-sized batches: one workgroup per (16 consecutive tokens, kv-head).
+// A page row of V holds one dimension of 16 tokens (32 bytes), so a token's V row lands
+// as dh scattered 2-byte stores; here the 16 x dh block is staged in LDS and, when the 16
+// tokens fill one page in order (a prefill chunk's whole pages), written as dh page rows
+// of 16 contiguous bytes per lane.  Otherwise each value goes to its own slot.
+template <int DH>
+__global__ __launch_bounds__(256) void v_page_kernel(const uint16_t* qkv, int T, const int32_t* slot,
+                                                     uint16_t* v_pool, int64_t n_blocks, int Hq, int Hkv) {
+  __shared__ uint16_t tile[16][DH + 8];   // [token][dimension]; the pad spreads the column reads over banks
+  const int t0 = blockIdx.x * 16, kvh = blockIdx.y;
+  const int tok = threadIdx.x / 16, ch = threadIdx.x % 16;   // load: 8 dimensions of one token
+  const int width = (Hq + 2 * Hkv) * DH;
+  const uint16_t* vrow = qkv + (size_t)(Hq + Hkv + kvh) * DH;
+  const bool have = ch < DH / 8 && t0 + tok < T;
+  if (have) {
+    const uint4 v = *reinterpret_cast<const uint4*>(vrow + (size_t)(t0 + tok) * width + ch * 8);
+    *reinterpret_cast<uint4*>(&tile[tok][ch * 8]) = v;
+  }
+  const int s0 = t0 < T ? slot[t0] : 0;
+  const bool in_order = threadIdx.x >= 16 || (t0 + (int)threadIdx.x < T && slot[t0 + threadIdx.x] == s0 + (int)threadIdx.x);
+  const bool whole_page = __syncthreads_and(in_order) && s0 % kPage == 0;   // also orders the LDS writes
+  if (whole_page) {
+    // thread (d, half): stored positions 8 half .. 8 half + 7 of page row d, i.e. the tokens
+    // v_pos(position) (v_pos swaps bits 2 and 3, so it is its own inverse)
+    const int d = threadIdx.x / 2, half = threadIdx.x % 2;
+    if (d < DH) {
+      uint16_t e[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) e[j] = tile[v_pos(half * 8 + j)][d];
+      uint16_t* vp = v_pool + kv_tile(kvh, n_blocks, s0 / kPage, DH) + d * kPage + half * 8;
+      *reinterpret_cast<uint4*>(vp) = make_uint4(e[0] | ((uint32_t)e[1] << 16), e[2] | ((uint32_t)e[3] << 16),
+                                                 e[4] | ((uint32_t)e[5] << 16), e[6] | ((uint32_t)e[7] << 16));
+    }
+    return;
+  }
+  if (!have) return;
+  const int sl = slot[t0 + tok];
+  uint16_t* vp = v_pool + kv_tile(kvh, n_blocks, sl / kPage, DH) + v_pos(sl % kPage);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) vp[(ch * 8 + j) * kPage] = tile[tok][ch * 8 + j];
+}
+
 __global__ __launch_bounds__(256) void kv_scatter_kernel(const uint16_t* k, const uint16_t* v, const int32_t* slot,
                                                          uint16_t* k_pool, uint16_t* v_pool, int64_t n_blocks, int Hkv,
                                                          int dh) {
@@ -116,17 +159,25 @@ hipError_t rope_kv_partials_launch(uint16_t* qkv, const float* part, int S, cons
                                    int Hq, int Hkv, int dh, hipStream_t st) {
   if (T <= 0) return hipSuccess;
   if (dh > 128 || dh % 8) return hipErrorInvalidValue;
-  const dim3 grid(T, (Hq + 2 * Hkv + 3) / 4);
+  // prefill-sized batches without split partials write V through v_page_kernel
+  const bool v_pages = S == 0 && T >= 64 && (dh == 128 || dh == 64);
+  const dim3 grid(T, ((v_pages ? Hq + Hkv : Hq + 2 * Hkv) + 3) / 4);
 #define HXF_ROPE(SS)                                                                                            \
   case SS:                                                                                                      \
     hipLaunchKernelGGL(rope_kv_kernel<SS>, grid, dim3(64), 0, st, qkv, part, T, pos, slot, cs, k_pool, v_pool, \
-                       n_blocks, Hq, Hkv, dh);                                                                 \
+                       n_blocks, Hq, Hkv, dh, v_pages ? 0 : 1);                                                \
     break;
   switch (S) {
     HXF_ROPE(0) HXF_ROPE(1) HXF_ROPE(2) HXF_ROPE(3) HXF_ROPE(4) HXF_ROPE(5) HXF_ROPE(6) HXF_ROPE(7) HXF_ROPE(8)
     default: return hipErrorInvalidValue;
   }
 #undef HXF_ROPE
+  if (hipError_t e = hipGetLastError(); e != hipSuccess || !v_pages) return e;
+  const dim3 vgrid((T + 15) / 16, Hkv);
+  if (dh == 128)
+    hipLaunchKernelGGL(v_page_kernel<128>, vgrid, dim3(256), 0, st, qkv, T, slot, v_pool, n_blocks, Hq, Hkv);
+  else
+    hipLaunchKernelGGL(v_page_kernel<64>, vgrid, dim3(256), 0, st, qkv, T, slot, v_pool, n_blocks, Hq, Hkv);
   return hipGetLastError();
 }
 

@@ -261,6 +261,49 @@ def test_rope_kv_write(hq, hkv, dh):
     np.testing.assert_array_equal(flatv[slots], v)
 
 
+@pytest.mark.parametrize("hq,hkv,dh", [(32, 8, 128), (4, 2, 64), (40, 8, 128)])
+def test_rope_kv_write_prefill_rows(hq, hkv, dh):
+    """A prefill-sized batch (V rows staged per 16 tokens and written as whole page rows):
+    12 whole pages in order, 32 tokens from the middle of a page on, a 16-token group whose
+    slots run in order but start mid-page, then 90 tokens in scattered slots."""
+    t = torch()
+    rng = np.random.default_rng(7 * hq + dh)
+    nb, maxpos = 80, 9000
+    perm = rng.permutation(nb)
+    whole = [int(b) * 16 + j for b in perm[:12] for j in range(16)]
+    mid = [int(perm[12]) * 16 + 5 + j for j in range(11)] + [int(perm[13]) * 16 + j for j in range(16)] + \
+          [int(perm[14]) * 16 + j for j in range(5)]
+    shifted = [int(perm[15]) * 16 + 3 + j for j in range(13)] + [int(perm[16]) * 16 + j for j in range(3)]
+    free = np.array([int(b) * 16 + j for b in perm[17:] for j in range(16)])
+    rest = [int(x) for x in rng.permutation(free)[:90]]
+    slots = np.array(whole + mid + shifted + rest, np.int32)
+    assert len(set(slots.tolist())) == len(slots)
+    T = len(slots)
+    qkvb, qkvf = rand_bf16(rng, (T, (hq + 2 * hkv) * dh))
+    pos = rng.integers(0, maxpos, T).astype(np.int32)
+    table = t.empty(maxpos * dh // 2 * 2, dtype=t.float32, device="cuda:0")
+    hxf.op_rope_table(table.data_ptr(), maxpos, dh, 10000.0)
+    qkv = dev_bits(qkvb)
+    kp, vp = _make_pools(nb, hkv, dh)
+    pos_d, slots_d = i32(pos), i32(slots)
+    log(f"rope/kv write prefill rows T={T} hq={hq} hkv={hkv} dh={dh}")
+    hxf.op_rope_kv_write(qkv.data_ptr(), pos_d.data_ptr(), slots_d.data_ptr(), table.data_ptr(), kp.data_ptr(),
+                         vp.data_ptr(), nb, T, hq, hkv, dh)
+    t.cuda.synchronize()
+    q = qkvf[:, : hq * dh].reshape(T, hq, dh)
+    k = qkvf[:, hq * dh:(hq + hkv) * dh].reshape(T, hkv, dh)
+    v = qkvf[:, (hq + hkv) * dh:].reshape(T, hkv, dh)
+    got_q = host_f64(qkv).reshape(T, -1)[:, : hq * dh].reshape(T, hq, dh)
+    np.testing.assert_allclose(got_q, M.apply_rope(q, pos, 1e4), rtol=2 ** -7, atol=2e-3)
+    K, V = _logical_pool(kp, vp, nb, hkv, dh)
+    np.testing.assert_allclose(K.reshape(nb * 16, hkv, dh)[slots], M.apply_rope(k, pos, 1e4), rtol=2 ** -7,
+                               atol=2e-3)
+    np.testing.assert_array_equal(V.reshape(nb * 16, hkv, dh)[slots], v)
+    # slots nobody wrote stay zero
+    untouched = np.setdiff1d(np.arange(nb * 16), slots)
+    assert not V.reshape(nb * 16, hkv, dh)[untouched].any()
+
+
 def _fill_paged(rng, ctxs, hkv, dh, extra_blocks=3):
     """Random K/V for sequences of the given lengths written through the library's
     scatter op into randomly permuted pages.  Returns pools, block tables and the
