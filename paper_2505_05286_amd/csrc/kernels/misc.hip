@@ -23,7 +23,23 @@ __global__ __launch_bounds__(1024) void argmax_kernel(const float* logits, int32
   int bi = 0x7FFFFFFF;
   const int n4 = V >> 2;
   const float4* r4 = reinterpret_cast<const float4*>(row);
-  for (int i = threadIdx.x; i < n4; i += 1024) {
+  // four loads in flight per thread, then the comparisons (their order does not matter:
+  // better() breaks ties by index)
+  int i = threadIdx.x;
+  for (; i + 3 * 1024 < n4; i += 4 * 1024) {
+    float4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = r4[i + u * 1024];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = 4 * (i + u * 1024);
+      better(bv, bi, v[u].x, j);
+      better(bv, bi, v[u].y, j + 1);
+      better(bv, bi, v[u].z, j + 2);
+      better(bv, bi, v[u].w, j + 3);
+    }
+  }
+  for (; i < n4; i += 1024) {
     const float4 v = r4[i];
     better(bv, bi, v.x, 4 * i);
     better(bv, bi, v.y, 4 * i + 1);
