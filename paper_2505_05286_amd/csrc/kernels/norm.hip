@@ -196,13 +196,58 @@ inline bool rows_kernel_fits(int d, int S) {
   return v == 4 || v == 8 || v == 16 || v == 20 || v == 24 || v == 32;
 }
 
+// The embedding gather + first RMSNorm for many rows: one wavefront per row, as
+// rmsnorm_rows_kernel (the gathered row stays in registers for the norm).
+template <int V>
+__global__ __launch_bounds__(256) void embed_rmsnorm_rows_kernel(const int32_t* ids, const uint16_t* E,
+                                                                const uint16_t* g, float* resid, uint16_t* out,
+                                                                int n_rows, int d, float eps, int out_kt) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= n_rows) return;
+  const int lane = threadIdx.x & 63;
+  const uint2* e2 = reinterpret_cast<const uint2*>(E + (size_t)ids[r] * d);
+  float4* r4 = reinterpret_cast<float4*>(resid + (size_t)r * d);
+  uint2 e[V];
+#pragma unroll
+  for (int j = 0; j < V; ++j) e[j] = e2[j * 64 + lane];
+  float4 v[V];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    v[j] = make_float4(bf2f(e[j].x & 0xFFFF), bf2f(e[j].x >> 16), bf2f(e[j].y & 0xFFFF), bf2f(e[j].y >> 16));
+    r4[j * 64 + lane] = v[j];
+    ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
+  }
+  const float rs = rsqrtf(wave_sum(ss) / (float)d + eps);
+  const uint2* g2 = reinterpret_cast<const uint2*>(g);
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int i = j * 64 + lane;
+    const uint2 gg = g2[i];
+    const float g0 = bf2f(gg.x & 0xFFFF), g1 = bf2f(gg.x >> 16), g2v = bf2f(gg.y & 0xFFFF), g3 = bf2f(gg.y >> 16);
+    const size_t o = out_kt ? packed_elem(r, 4 * i, out_kt) : (size_t)r * d + 4 * i;
+    *reinterpret_cast<uint2*>(out + o) =
+        make_uint2(pack_bf2(v[j].x * rs * g0, v[j].y * rs * g1), pack_bf2(v[j].z * rs * g2v, v[j].w * rs * g3));
+  }
+}
+
 __global__ __launch_bounds__(256) void embed_rmsnorm_kernel(const int32_t* ids, const uint16_t* E, const uint16_t* g,
                                                             float* resid, uint16_t* out, int d, float eps, int out_kt) {
   __shared__ float red[4];
   const int t = blockIdx.x;
   const uint2* e2 = reinterpret_cast<const uint2*>(E + (size_t)ids[t] * d);
   float4* r4 = reinterpret_cast<float4*>(resid + (size_t)t * d);
-  for (int i = threadIdx.x; i < (d >> 2); i += 256) {
+  // four gathers in flight per thread
+  int i = threadIdx.x;
+  for (; i + 3 * 256 < (d >> 2); i += 4 * 256) {
+    uint2 e[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) e[u] = e2[i + u * 256];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      r4[i + u * 256] = make_float4(bf2f(e[u].x & 0xFFFF), bf2f(e[u].x >> 16), bf2f(e[u].y & 0xFFFF), bf2f(e[u].y >> 16));
+  }
+  for (; i < (d >> 2); i += 256) {
     const uint2 e = e2[i];
     r4[i] = make_float4(bf2f(e.x & 0xFFFF), bf2f(e.x >> 16), bf2f(e.y & 0xFFFF), bf2f(e.y >> 16));
   }
@@ -252,6 +297,18 @@ hipError_t embed_rmsnorm_launch(const int32_t* ids, const uint16_t* E, const uin
                                 uint16_t* out, int T, int d, float eps, hipStream_t st, int out_kt) {
   if (T <= 0) return hipSuccess;
   if (out_kt && (d % 32 || out_kt != d / 32)) return hipErrorInvalidValue;
+  if (T > 256 && rows_kernel_fits(d, 0)) {
+    const dim3 grid((T + 3) / 4);
+#define HXF_EROWS(VV)                                                                                           \
+  case VV:                                                                                                      \
+    hipLaunchKernelGGL(embed_rmsnorm_rows_kernel<VV>, grid, dim3(256), 0, st, ids, E, g, resid, out, T, d, eps, \
+                       out_kt);                                                                                 \
+    return hipGetLastError();
+    switch (d / 256) {
+      HXF_EROWS(4) HXF_EROWS(8) HXF_EROWS(16) HXF_EROWS(20) HXF_EROWS(24) HXF_EROWS(32)
+    }
+#undef HXF_EROWS
+  }
   hipLaunchKernelGGL(embed_rmsnorm_kernel, dim3(T), dim3(256), 0, st, ids, E, g, resid, out, d, eps, out_kt);
   return hipGetLastError();
 }
